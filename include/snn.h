@@ -1,0 +1,155 @@
+/*
+ * snn.h -- C ABI of the MI355X (gfx950) sparse spiking BPTT library (libsnn.so).
+ *
+ * Method: Perez-Nieves & Goodman, "Sparse Spiking Gradient Descent", NeurIPS 2021.
+ * One fully connected layer of leaky integrate-and-fire (LIF) neurons at a time:
+ *   forward       V[t+1] = alpha V[t] + sum_i S_in[t,i] W[i,j] - S_out[t,j]   (Sec. 2.1, Eq. (lif),
+ *                 V_rest = V_r = 0, V[0] = 0), S_out[t,j] = V[t,j] > theta    (Eq. (spike_fn))
+ *   active set    |V[t,j] - theta| < b_th                                      (Definition 1)
+ *   spike deriv.  g(V) = 1/(beta |V - theta| + 1)^2 on the active set, else 0  (Definition 2; Sec. 3)
+ *   backward      dW_ij = sum_t G_j[t] trace_i[t],  G = eps * dS/dV           (Eq. (w_grad))
+ *                 eps_in_i[t] = sum_j W_ij delta_j[t], only where the input
+ *                 neuron i is active at t                                      (Eq. (s_grad), Sec. 2.2)
+ *                 delta_j[t] = alpha delta_j[t+1] + G_j[t+1], delta[T-1] = 0   (Proposition 1, App. B)
+ *
+ * Conventions shared by every entry point
+ *   Layout       Time-major, row-major, contiguous: a [T,B,N] tensor holds element (t,b,n) at
+ *                (t*B + b)*N + n. A "row" is one (t,b) pair, r = t*B + b. W is [N_in, N_out].
+ *                Spikes are uint8, any nonzero byte is a spike. Real tensors are float32.
+ *   Memory       Every tensor pointer is DEVICE memory owned by the caller; labels too.
+ *                The library allocates and frees nothing. Scratch memory comes from the
+ *                caller's workspace (device memory, at least the size the matching
+ *                *_workspace() query returns, 256-byte aligned).
+ *   Streams      `stream` is a hipStream_t (NULL = the default stream). Every call only
+ *                enqueues work on it and returns; nothing synchronises the host.
+ *   Errors       Arguments are checked on the host before any HIP call; a bad argument
+ *                returns SNN_ERR_INVALID_ARG and enqueues nothing. Sizes outside what the
+ *                kernels support return SNN_ERR_UNSUPPORTED. A failed launch returns
+ *                SNN_ERR_HIP. Checked: null required pointers, dimensions <= 0, element
+ *                counts T*B*N >= 2^31, alpha outside (0,1] or NaN, NaN theta, NaN or
+ *                negative beta and b_th, a workspace smaller than the query's size.
+ *   State        The library keeps no state between calls; calls on different streams
+ *                may run concurrently if their outputs do not overlap.
+ */
+#ifndef SNN_H
+#define SNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SNN_OK = 0,
+  SNN_ERR_INVALID_ARG = -1,
+  SNN_ERR_UNSUPPORTED = -2,
+  SNN_ERR_HIP = -3
+} snn_status;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* snn_status_string(int status);
+
+/*
+ * LIF forward of one layer (Sec. 2.1, Eqs. (lif), (spike_fn), (lif_unrolled)).
+ *   s_in     [T,B,N_in]  uint8 input spikes (read)
+ *   W        [N_in,N_out] float32 weights (read)
+ *   alpha    leak factor exp(-dt/tau), in (0,1]
+ *   theta    threshold V_th; +INFINITY gives the non-spiking readout of Sec. 3
+ *   V        [T,B,N_out] float32 membrane potential (written), V[0] = 0
+ *   s_out    [T,B,N_out] uint8 output spikes (written), s_out[t] = V[t] > theta
+ *   trace_in [T,B,N_in]  float32 input trace (written unless NULL):
+ *            trace[0] = 0, trace[t+1] = alpha*trace[t] + s_in[t]  (the filtered input that
+ *            Eq. (w_grad) reuses from the forward)
+ * Arithmetic is float32 with every operation rounded separately (no fused multiply-add) and
+ * the weighted input of a row summed over its spiking inputs in ascending input index starting
+ * from +0.0, so V and s_out are a deterministic function of the inputs.
+ * s_in[T-1] does not enter V. Supported: N_in <= 4096.
+ */
+snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
+                           float alpha, float theta, float* V, uint8_t* s_out, float* trace_in,
+                           void* stream);
+
+/*
+ * Active-set compaction (Definition 1) with the truncated spike derivative (Definition 2).
+ *   V        [T,B,N] float32 (read)
+ *   active   |V - theta| < b_th in float32, strictly (b_th = +INFINITY: every finite V)
+ *   row_ptr  int32 [T*B + 1] (written): exclusive prefix of per-row counts, row_ptr[T*B] = nnz
+ *   col_idx  int32 [capacity] (written): neuron index n of each active entry, ascending in a row
+ *   g_act    float32 [capacity] (written unless NULL): 1/(beta |V - theta| + 1)^2 at each entry
+ *   capacity length of col_idx / g_act; entries at positions >= capacity are not written
+ *   nnz_dev  int64 [1] device (written): the true nnz, even when it exceeds capacity. The
+ *            caller checks nnz <= capacity after the stream has run.
+ * Integer outputs are a deterministic function of V.
+ */
+size_t snn_active_compact_workspace(int T, int B, int N);
+snn_status snn_active_compact(const float* V, int T, int B, int N, float theta, float b_th, float beta,
+                              int32_t* row_ptr, int32_t* col_idx, float* g_act, int64_t capacity,
+                              int64_t* nnz_dev, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Sparse backward of one layer (Sec. 2.2: sparse dW and sparse spike gradient, Proposition 1).
+ *   W          [N_in,N_out] float32 (read)
+ *   trace_in   [T,B,N_in]  float32 input trace from snn_lif_forward (read)
+ *   alpha      the layer's leak factor
+ *   out_*      CSR of this layer's active set (from snn_active_compact, or from snn_readout_ce
+ *              for the readout): out_row_ptr [T*B+1], out_col_idx / out_g / eps_out [out_cap].
+ *              out_g NULL means a derivative factor of 1 (the readout). eps_out is the loss
+ *              gradient w.r.t. this layer's spikes at each entry. G = eps_out * out_g.
+ *   in_*       CSR of the INPUT layer's active set, in_row_ptr [T*B+1], in_col_idx [in_cap];
+ *              NULL for the first layer (no spike gradient is propagated to the data).
+ *   eps_in     float32 [in_cap] (written unless in_* is NULL): sum_j W_ij delta_j[t] at each
+ *              input-active entry (t,b,i), aligned with in_col_idx -- the next call's eps_out.
+ *   dW         [N_in,N_out] float32 (overwritten).
+ *   out_cap / in_cap are the allocated lengths of the entry arrays; entries at or beyond them
+ *   are ignored, so a CSR whose compaction overflowed its capacity is read safely (and gives
+ *   a truncated result).
+ * Supported: N_out <= 4096.
+ */
+size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out);
+snn_status snn_sparse_backward(const float* W, const float* trace_in, int T, int B, int N_in, int N_out,
+                               float alpha, const int32_t* out_row_ptr, const int32_t* out_col_idx,
+                               const float* out_g, const float* eps_out, int64_t out_cap,
+                               const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap,
+                               float* eps_in, float* dW, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+/*
+ * Dense surrogate BPTT of one layer on matrix cores: the baseline the sparse rule is
+ * measured against (Table 1, "Original").
+ *   W, trace_in as above; V [T,B,N_out] (read); eps_out [T,B,N_out] dense loss gradient
+ *   w.r.t. this layer's spikes (read).
+ *   G = eps_out * g(V) * 1[|V - theta| < b_th]; b_th = +INFINITY gives full surrogate BPTT;
+ *   theta = +INFINITY marks the readout, whose factor is 1 (G = eps_out).
+ *   grad_in [T,B,N_in] float32 (written unless NULL) = delta W^T, unmasked.
+ *   dW [N_in,N_out] float32 (overwritten) = sum_t trace_in[t]^T G[t].
+ */
+size_t snn_dense_backward_workspace(int T, int B, int N_in, int N_out);
+snn_status snn_dense_backward_ref(const float* W, const float* trace_in, const float* V,
+                                  const float* eps_out, int T, int B, int N_in, int N_out, float alpha,
+                                  float theta, float b_th, float beta, float* grad_in, float* dW,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Readout loss helper (App. E cross-entropy), outside the measured backward.
+ *   V_out  [T,B,C] float32 readout membrane potential (read); labels int32 [B] device (read)
+ *   mode 0 logits a[b,c] = max_t V_out[t,b,c] (first maximal t); mode 1 a = sum_t V_out.
+ *   loss   float32 [1] device (written): mean over b of -log softmax(a)[b, label_b];
+ *          NaN if a label is outside [0, C).
+ *   CSR of the entries the loss reads, with eps = dL/da = (p - onehot)/B there:
+ *   mode 0 nnz = B*C (the arg-max entries), mode 1 nnz = T*B*C (every entry);
+ *   row_ptr int32 [T*B+1], col_idx int32 [nnz], eps float32 [nnz] (written).
+ *   eps_dense [T,B,C] float32 (written unless NULL): dL/dV_out densely (zero where the loss
+ *   does not read V_out), the input of the dense baseline's readout step.
+ */
+size_t snn_readout_ce_workspace(int T, int B, int C, int mode);
+snn_status snn_readout_ce(const float* V_out, const int32_t* labels, int T, int B, int C, int mode,
+                          int32_t* row_ptr, int32_t* col_idx, float* eps, float* loss, float* eps_dense,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SNN_H */

@@ -69,10 +69,11 @@ def network_backward(fwd: dict, Ws, W_out, alphas, alpha_out, labels, mode: str,
                      theta, b_th, beta, absolute: bool = False):
     """Gradients of the whole network (O2), top down.
 
-    fwd: output of forward.network_forward. With absolute=True every weight and
-    every loss gradient is replaced by its absolute value, which yields the
-    magnitude envelope used to state tolerances (the same contraction with
-    absolute values; traces, alpha and g are non-negative already).
+    fwd: output of forward.network_forward. With absolute=True every weight is
+    replaced by its absolute value and the loss gradient (p - y)/B by (p + y)/B,
+    which yields the magnitude envelope used to state tolerances: every sum and
+    difference of the chain taken with its terms in absolute value (traces, alpha
+    and g are non-negative already).
     Returns dict with
       loss, dLda, readout (the readout_grad dict),
       dW_out, dW[l],
@@ -81,7 +82,7 @@ def network_backward(fwd: dict, Ws, W_out, alphas, alpha_out, labels, mode: str,
     """
     L = len(Ws)
     ro = readout_grad(fwd["V_out"], labels, mode)
-    G_out = np.abs(ro["G"]) if absolute else ro["G"]
+    G_out = ro["G_abs"] if absolute else ro["G"]
     Wo = np.abs(W_out) if absolute else W_out
     dW_out, eps = layer_backward(G_out, Wo, fwd["trace_out"], alpha_out, grad_in=True)
     dW = [None] * L

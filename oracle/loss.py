@@ -26,8 +26,12 @@ def readout_logits(V_out: np.ndarray, mode: str):
     raise ValueError(mode)
 
 
-def cross_entropy(a: np.ndarray, labels: np.ndarray):
-    """Mean cross-entropy of softmax(a) and dL/da = (p - onehot) / B, float64."""
+def cross_entropy(a: np.ndarray, labels: np.ndarray, magnitude: bool = False):
+    """Mean cross-entropy of softmax(a) and dL/da = (p - onehot) / B, float64.
+
+    With magnitude=True the second result is (p + onehot) / B instead: the difference taken
+    with its terms in absolute value, i.e. the scale on which rounding of p acts.
+    """
     a = np.asarray(a, dtype=np.float64)
     B, C = a.shape
     z = a - a.max(axis=1, keepdims=True)
@@ -36,7 +40,7 @@ def cross_entropy(a: np.ndarray, labels: np.ndarray):
     idx = (np.arange(B), np.asarray(labels))
     loss = -np.log(p[idx]).mean()
     d = p.copy()
-    d[idx] -= 1.0
+    d[idx] += 1.0 if magnitude else -1.0
     return loss, d / B
 
 
@@ -46,11 +50,13 @@ def readout_grad(V_out: np.ndarray, labels: np.ndarray, mode: str):
     The CSR lists the entries of V_out that the loss reads (the arg-max entries
     for 'max', every entry for 'sum'), rows r = t*B + b, with eps = dL/da there;
     its derivative factor is 1 (the readout does not spike).
-    Returns dict(loss, dLda, G, row_ptr, col_idx, eps).
+    Also returns G_abs, the same tensor built from (p + onehot)/B (see cross_entropy).
+    Returns dict(loss, dLda, G, G_abs, row_ptr, col_idx, eps, tstar).
     """
     T, B, C = V_out.shape
     a, tstar = readout_logits(V_out, mode)
     loss, dLda = cross_entropy(a, labels)
+    _, dLda_abs = cross_entropy(a, labels, magnitude=True)
     m = np.zeros((T, B, C), bool)
     if mode == "max":
         bb, cc = np.meshgrid(np.arange(B), np.arange(C), indexing="ij")
@@ -58,9 +64,10 @@ def readout_grad(V_out: np.ndarray, labels: np.ndarray, mode: str):
     else:
         m[:] = True
     G = np.where(m, dLda[None], 0.0)
+    G_abs = np.where(m, dLda_abs[None], 0.0)
     rows, cols = np.nonzero(m.reshape(T * B, C))
     row_ptr = np.zeros(T * B + 1, np.int64)
     np.cumsum(np.bincount(rows, minlength=T * B), out=row_ptr[1:])
     eps = dLda[rows % B, cols]
-    return {"loss": loss, "dLda": dLda, "G": G, "row_ptr": row_ptr, "col_idx": cols.astype(np.int64), "eps": eps,
+    return {"loss": loss, "dLda": dLda, "G": G, "G_abs": G_abs, "row_ptr": row_ptr, "col_idx": cols.astype(np.int64), "eps": eps,
             "tstar": tstar}

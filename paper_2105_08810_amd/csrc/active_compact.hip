@@ -1,0 +1,141 @@
+// Active-set compaction (Definition 1) into CSR, with the truncated spike derivative
+// g(V) = 1/(beta |V - theta| + 1)^2 at each active entry (Definition 2; surrogate of Sec. 3).
+//
+// Three passes over rows r = t*B + b of V [T*B, N]:
+//   count  one wavefront per row: predicate per element, wave ballot + popcount -> counts[r]
+//   scan   device-wide exclusive scan -> row_ptr, nnz
+//   fill   one wavefront per row: ballot + lane prefix (mbcnt) give each active element its
+//          slot, so col_idx is ascending inside a row; entries at slots >= capacity are dropped.
+// The predicate |V - theta| < b_th is evaluated in float32 exactly as written (one rounded
+// subtraction, then fabs and a strict compare), so the integer outputs are bit-exact.
+#include "common.h"
+
+namespace snn {
+namespace {
+
+constexpr int kRowsPerBlock = 4;  // one wavefront per row
+constexpr int kThreads = kRowsPerBlock * kWave;
+
+__device__ __forceinline__ bool is_active(float v, float theta, float bth) { return fabsf(v - theta) < bth; }
+
+__device__ __forceinline__ float surrogate(float v, float theta, float beta) {
+  const float x = __fadd_rn(__fmul_rn(beta, fabsf(v - theta)), 1.0f);
+  return 1.0f / __fmul_rn(x, x);
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void compact_count(const float* __restrict__ V, int rows, int N, float theta,
+                                                          float bth, int32_t* __restrict__ counts) {
+  const int l = lane_id();
+  const int r = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
+  if (r >= rows) return;
+  const float* row = V + (size_t)r * N;
+  int c = 0;
+  if (VEC) {
+    for (int j = 4 * l; j < N; j += 4 * kWave) {
+      const float4 v = *reinterpret_cast<const float4*>(row + j);
+      c += is_active(v.x, theta, bth) + is_active(v.y, theta, bth) + is_active(v.z, theta, bth) +
+           is_active(v.w, theta, bth);
+    }
+  } else {
+    for (int j = l; j < N; j += kWave) c += is_active(row[j], theta, bth);
+  }
+  c = wave_sum_int(c);
+  if (l == 0) counts[r] = c;
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void compact_fill(const float* __restrict__ V, int rows, int N, float theta,
+                                                         float bth, float beta, const int32_t* __restrict__ row_ptr,
+                                                         int32_t* __restrict__ col_idx, float* __restrict__ g_act,
+                                                         int64_t cap) {
+  const int l = lane_id();
+  const int r = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
+  if (r >= rows) return;
+  const float* row = V + (size_t)r * N;
+  int64_t base = row_ptr[r];
+  if (VEC) {
+    // lane l holds elements 4l..4l+3 of each 256-wide slice; ascending order is (lane, q)
+    for (int j0 = 0; j0 < N; j0 += 4 * kWave) {
+      const int j = j0 + 4 * l;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (j < N) v = *reinterpret_cast<const float4*>(row + j);
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+      bool a[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) a[q] = (j < N) && is_active(vv[q], theta, bth);
+      const uint64_t m0 = __ballot(a[0]), m1 = __ballot(a[1]), m2 = __ballot(a[2]), m3 = __ballot(a[3]);
+      int64_t pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (a[q]) {
+          if (pos < cap) {
+            col_idx[pos] = j + q;
+            if (g_act) g_act[pos] = surrogate(vv[q], theta, beta);
+          }
+          ++pos;
+        }
+      }
+      base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+    }
+  } else {
+    for (int j0 = 0; j0 < N; j0 += kWave) {
+      const int j = j0 + l;
+      const float v = j < N ? row[j] : 0.0f;
+      const bool a = (j < N) && is_active(v, theta, bth);
+      const uint64_t m = __ballot(a);
+      const int64_t pos = base + mask_prefix(m);
+      if (a && pos < cap) {
+        col_idx[pos] = j;
+        if (g_act) g_act[pos] = surrogate(v, theta, beta);
+      }
+      base += __popcll(m);
+    }
+  }
+}
+
+}  // namespace
+}  // namespace snn
+
+using namespace snn;
+
+extern "C" size_t snn_active_compact_workspace(int T, int B, int N) {
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return 0;
+  const int rows = T * B;
+  Carve c(nullptr);
+  c.take<int32_t>(rows);
+  c.take<int32_t>(scan_temp_elems(rows));
+  return c.off;
+}
+
+extern "C" snn_status snn_active_compact(const float* V, int T, int B, int N, float theta, float b_th, float beta,
+                                         int32_t* row_ptr, int32_t* col_idx, float* g_act, int64_t capacity,
+                                         int64_t* nnz_dev, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!V || !row_ptr || !nnz_dev || !workspace) return SNN_ERR_INVALID_ARG;
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return SNN_ERR_INVALID_ARG;
+  if (isnan(theta) || isnan(b_th) || b_th < 0.0f || isnan(beta) || beta < 0.0f) return SNN_ERR_INVALID_ARG;
+  if (capacity < 0 || (capacity > 0 && !col_idx)) return SNN_ERR_INVALID_ARG;
+  if (workspace_bytes < snn_active_compact_workspace(T, B, N)) return SNN_ERR_INVALID_ARG;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int rows = T * B;
+  Carve ws(workspace);
+  int32_t* counts = ws.take<int32_t>(rows);
+  int32_t* temp = ws.take<int32_t>(scan_temp_elems(rows));
+  const bool vec = (N % 4) == 0 && (reinterpret_cast<uintptr_t>(V) % 16) == 0;
+  const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock);
+  if (vec)
+    hipLaunchKernelGGL(compact_count<true>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, counts);
+  else
+    hipLaunchKernelGGL(compact_count<false>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, counts);
+  launch_exclusive_scan(counts, rows, row_ptr, nnz_dev, temp, s);
+  if (capacity > 0) {
+    if (vec)
+      hipLaunchKernelGGL(compact_fill<true>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, row_ptr,
+                         col_idx, g_act, capacity);
+    else
+      hipLaunchKernelGGL(compact_fill<false>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, row_ptr,
+                         col_idx, g_act, capacity);
+  }
+  return launch_status();
+}

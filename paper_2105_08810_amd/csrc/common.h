@@ -1,0 +1,86 @@
+// Shared host/device helpers of libsnn (internal header).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/snn.h"
+
+namespace snn {
+
+constexpr int kWave = 64;  // CDNA4 wavefront width
+
+// ------------------------------------------------------------------ host-side checks
+
+inline bool bad_dim(int x) { return x <= 0; }
+
+// Element count of a [T,B,N] tensor must stay below 2^31 (int32 CSR offsets and indexing).
+inline bool too_big(int T, int B, int N) {
+  return (int64_t)T * (int64_t)B * (int64_t)N >= ((int64_t)1 << 31);
+}
+
+inline bool bad_alpha(float a) { return !(a > 0.0f && a <= 1.0f); }  // also rejects NaN
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline snn_status launch_status() {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? SNN_OK : SNN_ERR_HIP;
+}
+
+// Bump allocator over the caller's workspace.
+struct Carve {
+  char* base;
+  size_t off = 0;
+  explicit Carve(void* p) : base(static_cast<char*>(p)) {}
+  template <class T>
+  T* take(size_t n) {
+    T* p = reinterpret_cast<T*>(base ? base + off : nullptr);
+    off += align256(n * sizeof(T));
+    return p;
+  }
+};
+
+// Number of compute units of the current device (cached per process and device).
+int cu_count();
+
+// Exclusive scan of counts[0..n) into out[0..n] (out[n] = total) and *total64 = total.
+// temp must hold scan_temp_elems(n) int32 values.
+size_t scan_temp_elems(int n);
+void launch_exclusive_scan(const int32_t* counts, int n, int32_t* out, int64_t* total64, int32_t* temp,
+                           hipStream_t stream);
+
+// ------------------------------------------------------------------ device helpers
+
+__device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
+
+// Lanes below the calling lane that have bits set in mask.
+__device__ __forceinline__ int mask_prefix(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Inclusive prefix over the wave's lanes.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    int u = __shfl_up(v, off, kWave);
+    if (l >= off) v += u;
+  }
+  return v;
+}
+
+}  // namespace snn

@@ -1,0 +1,131 @@
+"""A whole network through libsnn: LIF forward of every layer, readout loss, active-set
+compaction, the sparse backward chain and the dense baseline chain.
+
+This is orchestration only -- allocation and the order of C-ABI calls; every number is
+computed by the HIP kernels. The network is the paper's fully connected stack (Sec. 3): L LIF
+layers then an infinite-threshold readout with a cross-entropy loss (App. E).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import torch
+
+from . import snn
+
+INF = float("inf")
+
+
+@dataclass
+class Network:
+    X: torch.Tensor  # [T, B, N_in] uint8
+    Ws: List[torch.Tensor]
+    W_out: torch.Tensor
+    alphas: List[float]
+    alpha_out: float
+    labels: torch.Tensor  # [B] int32
+    loss_mode: int  # 0 = max over t, 1 = sum over t
+    theta: float = 1.0
+    beta: float = 100.0
+    # forward state
+    V: List[torch.Tensor] = field(default_factory=list)
+    S: List[torch.Tensor] = field(default_factory=list)
+    trace: List[torch.Tensor] = field(default_factory=list)
+    V_out: Optional[torch.Tensor] = None
+    S_out: Optional[torch.Tensor] = None
+    trace_out: Optional[torch.Tensor] = None
+
+    @property
+    def T(self):
+        return self.X.shape[0]
+
+    @property
+    def B(self):
+        return self.X.shape[1]
+
+    @property
+    def L(self):
+        return len(self.Ws)
+
+    def allocate(self):
+        """Forward buffers, allocated once so repeated steps reuse them."""
+        dev = self.X.device
+        T, B = self.T, self.B
+        sizes = [self.X.shape[2]] + [W.shape[1] for W in self.Ws]
+        self.V = [torch.empty((T, B, n), dtype=torch.float32, device=dev) for n in sizes[1:]]
+        self.S = [torch.empty((T, B, n), dtype=torch.uint8, device=dev) for n in sizes[1:]]
+        self.trace = [torch.empty((T, B, n), dtype=torch.float32, device=dev) for n in sizes[:-1]]
+        C = self.W_out.shape[1]
+        self.V_out = torch.empty((T, B, C), dtype=torch.float32, device=dev)
+        self.S_out = torch.empty((T, B, C), dtype=torch.uint8, device=dev)
+        self.trace_out = torch.empty((T, B, sizes[-1]), dtype=torch.float32, device=dev)
+        return self
+
+    def forward(self):
+        if not self.V:
+            self.allocate()
+        x = self.X
+        T, B = self.T, self.B
+        for l, W in enumerate(self.Ws):
+            snn.snn_lif_forward(x, W, T, B, W.shape[0], W.shape[1], self.alphas[l], self.theta, self.V[l],
+                                self.S[l], self.trace[l])
+            x = self.S[l]
+        snn.snn_lif_forward(x, self.W_out, T, B, self.W_out.shape[0], self.W_out.shape[1], self.alpha_out, INF,
+                            self.V_out, self.S_out, self.trace_out)
+        return self
+
+    def readout(self, dense=False):
+        """Readout CSR, eps at its entries, loss (device scalar) and, if asked, dL/dV_out densely."""
+        return snn.readout_ce(self.V_out, self.labels, self.loss_mode, dense=dense)
+
+    def compact(self, b_th, capacities: Optional[List[int]] = None) -> List[snn.Csr]:
+        caps = capacities or [None] * self.L
+        return [snn.active_compact(self.V[l], self.theta, b_th, self.beta, caps[l]) for l in range(self.L)]
+
+    def sparse_backward(self, csrs: List[snn.Csr], ro=None):
+        """Readout backward, then every LIF layer top down. Returns (dW list, dW_out, eps list)
+        where eps[l] is the gradient w.r.t. layer l's spikes at its active entries."""
+        if ro is None:
+            ro = self.readout()
+        ro_csr, ro_eps = ro[0], ro[1]
+        dW_out, eps = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro_csr, ro_eps,
+                                          inp=csrs[self.L - 1])
+        dWs: List[Optional[torch.Tensor]] = [None] * self.L
+        epss: List[Optional[torch.Tensor]] = [None] * self.L
+        for l in range(self.L - 1, -1, -1):
+            epss[l] = eps
+            dWs[l], eps = snn.sparse_backward(self.Ws[l], self.trace[l], self.alphas[l], csrs[l], eps,
+                                              inp=csrs[l - 1] if l > 0 else None)
+        return dWs, dW_out, epss
+
+    def dense_backward(self, b_th, ro=None):
+        """The dense baseline chain. Returns (dW list, dW_out, eps_dense list)."""
+        if ro is None or ro[3] is None:
+            ro = self.readout(dense=True)
+        dW_out, eps = snn.dense_backward_ref(self.W_out, self.trace_out, self.V_out, ro[3], self.alpha_out, INF,
+                                             INF, self.beta, grad_in=True)
+        dWs: List[Optional[torch.Tensor]] = [None] * self.L
+        epss: List[Optional[torch.Tensor]] = [None] * self.L
+        for l in range(self.L - 1, -1, -1):
+            epss[l] = eps
+            dWs[l], eps = snn.dense_backward_ref(self.Ws[l], self.trace[l], self.V[l], eps, self.alphas[l],
+                                                 self.theta, b_th, self.beta, grad_in=l > 0)
+        return dWs, dW_out, epss
+
+
+def from_inputs(inp, device="cuda") -> Network:
+    """Network on the device from a synth.Inputs bundle (host arrays)."""
+    dev = torch.device(device)
+    cfg = inp.cfg
+    return Network(
+        X=torch.from_numpy(inp.X).to(dev),
+        Ws=[torch.from_numpy(W).to(dev) for W in inp.Ws],
+        W_out=torch.from_numpy(inp.W_out).to(dev),
+        alphas=[float(a) for a in inp.alphas],
+        alpha_out=float(inp.alpha_out),
+        labels=torch.from_numpy(inp.labels.astype("int32")).to(dev),
+        loss_mode=0 if cfg.loss_mode == "max" else 1,
+        theta=float(cfg.theta),
+        beta=float(cfg.beta),
+    )

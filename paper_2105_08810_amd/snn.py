@@ -1,0 +1,245 @@
+"""Python binding of libsnn's C ABI (argument marshalling only).
+
+Every function below has the name of the C entry point it calls and takes torch tensors in
+place of device pointers; all computation happens in the HIP kernels of libsnn.so. Tensors
+must be CUDA(HIP) tensors on the current device, contiguous, with the dtype the header
+states. Work is enqueued on torch's current stream and nothing is synchronised, except in
+the convenience helpers that say so.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsnn.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "snn.h")
+
+SNN_OK, SNN_ERR_INVALID_ARG, SNN_ERR_UNSUPPORTED, SNN_ERR_HIP = 0, -1, -2, -3
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_F = ctypes.c_float
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+
+_SIGNATURES = {
+    "snn_status_string": (ctypes.c_char_p, [_I]),
+    "snn_lif_forward": (_I, [_P, _P, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P]),
+    "snn_active_compact_workspace": (_SZ, [_I, _I, _I]),
+    "snn_active_compact": (_I, [_P, _I, _I, _I, _F, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_sparse_backward_workspace": (_SZ, [_I, _I, _I, _I]),
+    "snn_sparse_backward": (_I, [_P, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
+                                 _P]),
+    "snn_dense_backward_workspace": (_SZ, [_I, _I, _I, _I]),
+    "snn_dense_backward_ref": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _F, _F, _F, _F, _P, _P, _P, _SZ, _P]),
+    "snn_readout_ce_workspace": (_SZ, [_I, _I, _I, _I]),
+    "snn_readout_ce": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+}
+
+_lib = None
+
+
+class SnnError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {status_string(status)} ({status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsnn.so (raises if it has not been built: there is no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2105_08810_amd.build`")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(l, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = l
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().snn_status_string(int(status)).decode()
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor") -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check(fn: str, status: int):
+    if status != SNN_OK:
+        raise SnnError(fn, status)
+
+
+def workspace(nbytes: int, device=None) -> torch.Tensor:
+    """Device workspace of at least nbytes (256-byte aligned by the caching allocator)."""
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device or "cuda")
+
+
+# ------------------------------------------------------------------ entry points
+
+def snn_lif_forward(s_in, W, T, B, N_in, N_out, alpha, theta, V, s_out, trace_in=None, stream=None):
+    _check("snn_lif_forward", lib().snn_lif_forward(
+        _ptr(s_in, torch.uint8, "s_in"), _ptr(W, torch.float32, "W"), T, B, N_in, N_out, float(alpha), float(theta),
+        _ptr(V, torch.float32, "V"), _ptr(s_out, torch.uint8, "s_out"), _ptr(trace_in, torch.float32, "trace_in"),
+        _stream(stream)))
+
+
+def snn_active_compact_workspace(T, B, N) -> int:
+    return int(lib().snn_active_compact_workspace(T, B, N))
+
+
+def snn_active_compact(V, T, B, N, theta, b_th, beta, row_ptr, col_idx, g_act, capacity, nnz_dev, ws,
+                       stream=None):
+    _check("snn_active_compact", lib().snn_active_compact(
+        _ptr(V, torch.float32, "V"), T, B, N, float(theta), float(b_th), float(beta),
+        _ptr(row_ptr, torch.int32, "row_ptr"), _ptr(col_idx, torch.int32, "col_idx"),
+        _ptr(g_act, torch.float32, "g_act"), int(capacity), _ptr(nnz_dev, torch.int64, "nnz_dev"),
+        _ptr(ws, None, "workspace"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_sparse_backward_workspace(T, B, N_in, N_out) -> int:
+    return int(lib().snn_sparse_backward_workspace(T, B, N_in, N_out))
+
+
+def snn_sparse_backward(W, trace_in, T, B, N_in, N_out, alpha, out_row_ptr, out_col_idx, out_g, eps_out, out_cap,
+                        in_row_ptr, in_col_idx, in_cap, eps_in, dW, ws, stream=None):
+    _check("snn_sparse_backward", lib().snn_sparse_backward(
+        _ptr(W, torch.float32, "W"), _ptr(trace_in, torch.float32, "trace_in"), T, B, N_in, N_out, float(alpha),
+        _ptr(out_row_ptr, torch.int32, "out_row_ptr"), _ptr(out_col_idx, torch.int32, "out_col_idx"),
+        _ptr(out_g, torch.float32, "out_g"), _ptr(eps_out, torch.float32, "eps_out"), int(out_cap),
+        _ptr(in_row_ptr, torch.int32, "in_row_ptr"), _ptr(in_col_idx, torch.int32, "in_col_idx"), int(in_cap),
+        _ptr(eps_in, torch.float32, "eps_in"), _ptr(dW, torch.float32, "dW"),
+        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_dense_backward_workspace(T, B, N_in, N_out) -> int:
+    return int(lib().snn_dense_backward_workspace(T, B, N_in, N_out))
+
+
+def snn_dense_backward_ref(W, trace_in, V, eps_out, T, B, N_in, N_out, alpha, theta, b_th, beta, grad_in, dW, ws,
+                           stream=None):
+    _check("snn_dense_backward_ref", lib().snn_dense_backward_ref(
+        _ptr(W, torch.float32, "W"), _ptr(trace_in, torch.float32, "trace_in"), _ptr(V, torch.float32, "V"),
+        _ptr(eps_out, torch.float32, "eps_out"), T, B, N_in, N_out, float(alpha), float(theta), float(b_th),
+        float(beta), _ptr(grad_in, torch.float32, "grad_in"), _ptr(dW, torch.float32, "dW"),
+        _ptr(ws, None, "workspace"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_readout_ce_workspace(T, B, C, mode) -> int:
+    return int(lib().snn_readout_ce_workspace(T, B, C, mode))
+
+
+def snn_readout_ce(V_out, labels, T, B, C, mode, row_ptr, col_idx, eps, loss, eps_dense, ws, stream=None):
+    _check("snn_readout_ce", lib().snn_readout_ce(
+        _ptr(V_out, torch.float32, "V_out"), _ptr(labels, torch.int32, "labels"), T, B, C, int(mode),
+        _ptr(row_ptr, torch.int32, "row_ptr"), _ptr(col_idx, torch.int32, "col_idx"),
+        _ptr(eps, torch.float32, "eps"), _ptr(loss, torch.float32, "loss"),
+        _ptr(eps_dense, torch.float32, "eps_dense"), _ptr(ws, None, "workspace"), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+# ------------------------------------------------------------------ allocation helpers
+
+def lif_forward(s_in: torch.Tensor, W: torch.Tensor, alpha, theta, want_trace=True):
+    """Allocate outputs and run snn_lif_forward. Returns (V, s_out, trace or None)."""
+    T, B, N_in = s_in.shape
+    N_out = W.shape[1]
+    V = torch.empty((T, B, N_out), dtype=torch.float32, device=s_in.device)
+    S = torch.empty((T, B, N_out), dtype=torch.uint8, device=s_in.device)
+    tr = torch.empty((T, B, N_in), dtype=torch.float32, device=s_in.device) if want_trace else None
+    snn_lif_forward(s_in, W, T, B, N_in, N_out, alpha, theta, V, S, tr)
+    return V, S, tr
+
+
+class Csr:
+    """Device CSR of an active set: row_ptr [T*B+1], col_idx / g [capacity], nnz (int64 device scalar)."""
+
+    def __init__(self, row_ptr, col_idx, g, nnz_dev, capacity):
+        self.row_ptr, self.col_idx, self.g, self.nnz_dev, self.capacity = row_ptr, col_idx, g, nnz_dev, capacity
+
+    def nnz(self) -> int:
+        return int(self.nnz_dev.item())
+
+
+def active_compact(V: torch.Tensor, theta, b_th, beta, capacity: Optional[int] = None, with_g=True) -> Csr:
+    """Allocate and run snn_active_compact. Without a capacity it first counts (one host sync)."""
+    T, B, N = V.shape
+    dev = V.device
+    ws = workspace(snn_active_compact_workspace(T, B, N), dev)
+    row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device=dev)
+    nnz = torch.empty(1, dtype=torch.int64, device=dev)
+    if capacity is None:
+        snn_active_compact(V, T, B, N, theta, b_th, beta, row_ptr, None, None, 0, nnz, ws)
+        capacity = int(nnz.item())
+    cap = max(int(capacity), 1)
+    col = torch.empty(cap, dtype=torch.int32, device=dev)
+    g = torch.empty(cap, dtype=torch.float32, device=dev) if with_g else None
+    snn_active_compact(V, T, B, N, theta, b_th, beta, row_ptr, col, g, cap, nnz, ws)
+    return Csr(row_ptr, col, g, nnz, cap)
+
+
+def readout_ce(V_out: torch.Tensor, labels: torch.Tensor, mode: int, dense=False):
+    """Allocate and run snn_readout_ce. Returns (Csr with g=None, eps, loss, eps_dense or None)."""
+    T, B, C = V_out.shape
+    dev = V_out.device
+    nnz = B * C if mode == 0 else T * B * C
+    row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device=dev)
+    col = torch.empty(nnz, dtype=torch.int32, device=dev)
+    eps = torch.empty(nnz, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    ed = torch.empty((T, B, C), dtype=torch.float32, device=dev) if dense else None
+    ws = workspace(snn_readout_ce_workspace(T, B, C, mode), dev)
+    snn_readout_ce(V_out, labels, T, B, C, mode, row_ptr, col, eps, loss, ed, ws)
+    nnz_dev = torch.full((1,), nnz, dtype=torch.int64, device=dev)
+    return Csr(row_ptr, col, None, nnz_dev, nnz), eps, loss, ed
+
+
+def sparse_backward(W, trace_in, alpha, out: Csr, eps_out, inp: Optional[Csr] = None, ws=None):
+    """Allocate outputs and run snn_sparse_backward. Returns (dW, eps_in or None)."""
+    T, B, N_in = trace_in.shape
+    N_out = W.shape[1]
+    dev = W.device
+    dW = torch.empty((N_in, N_out), dtype=torch.float32, device=dev)
+    eps_in = torch.empty(inp.capacity, dtype=torch.float32, device=dev) if inp is not None else None
+    if ws is None:
+        ws = workspace(snn_sparse_backward_workspace(T, B, N_in, N_out), dev)
+    snn_sparse_backward(W, trace_in, T, B, N_in, N_out, alpha, out.row_ptr, out.col_idx, out.g, eps_out,
+                        out.capacity, None if inp is None else inp.row_ptr, None if inp is None else inp.col_idx,
+                        0 if inp is None else inp.capacity, eps_in, dW, ws)
+    return dW, eps_in
+
+
+def dense_backward_ref(W, trace_in, V, eps_out, alpha, theta, b_th, beta, grad_in=True, ws=None):
+    """Allocate outputs and run snn_dense_backward_ref. Returns (dW, grad_in or None)."""
+    T, B, N_in = trace_in.shape
+    N_out = W.shape[1]
+    dev = W.device
+    dW = torch.empty((N_in, N_out), dtype=torch.float32, device=dev)
+    gi = torch.empty((T, B, N_in), dtype=torch.float32, device=dev) if grad_in else None
+    if ws is None:
+        ws = workspace(snn_dense_backward_workspace(T, B, N_in, N_out), dev)
+    snn_dense_backward_ref(W, trace_in, V, eps_out, T, B, N_in, N_out, alpha, theta, b_th, beta, gi, dW, ws)
+    return dW, gi
+
+
+INF = math.inf

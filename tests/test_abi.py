@@ -1,0 +1,133 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the header declares, and
+rejects bad arguments before any HIP call (so these run without a GPU)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2105_08810_amd import snn
+
+NAN = float("nan")
+INF = math.inf
+FAKE = 0x1000  # never dereferenced: every call below must fail validation first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(snn.LIB_PATH):
+        from paper_2105_08810_amd import build
+        build.build(verbose=False)
+    return snn.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    with open(snn.HEADER) as f:
+        text = f.read()
+    declared = set(re.findall(r"\b(snn_[a-z_]+)\s*\(", text))
+    assert {"snn_lif_forward", "snn_active_compact", "snn_sparse_backward", "snn_dense_backward_ref"} <= declared
+    raw = ctypes.CDLL(snn.LIB_PATH)
+    for name in sorted(declared):
+        assert hasattr(raw, name), name
+    assert declared == set(snn._SIGNATURES), "binding and header disagree"
+
+
+def test_status_strings(lib):
+    assert snn.status_string(0) == "SNN_OK"
+    assert snn.status_string(-1) == "SNN_ERR_INVALID_ARG"
+    assert snn.status_string(-2) == "SNN_ERR_UNSUPPORTED"
+    assert snn.status_string(-3) == "SNN_ERR_HIP"
+    assert snn.status_string(12345) == "SNN_UNKNOWN_STATUS"
+
+
+def _fwd(lib, **kw):
+    a = dict(s_in=FAKE, W=FAKE, T=10, B=4, N_in=32, N_out=16, alpha=0.9, theta=1.0, V=FAKE, s_out=FAKE,
+             trace=FAKE, stream=None)
+    a.update(kw)
+    return lib.snn_lif_forward(a["s_in"], a["W"], a["T"], a["B"], a["N_in"], a["N_out"], a["alpha"], a["theta"],
+                               a["V"], a["s_out"], a["trace"], a["stream"])
+
+
+@pytest.mark.parametrize("kw", [dict(s_in=None), dict(W=None), dict(V=None), dict(s_out=None), dict(T=0),
+                                dict(B=-1), dict(N_in=0), dict(N_out=0), dict(alpha=0.0), dict(alpha=1.5),
+                                dict(alpha=NAN), dict(theta=NAN), dict(T=70000, B=70000)])
+def test_forward_rejects(lib, kw):
+    assert _fwd(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_forward_unsupported_width(lib):
+    assert _fwd(lib, N_in=5000) == snn.SNN_ERR_UNSUPPORTED
+
+
+def _cmp(lib, **kw):
+    a = dict(V=FAKE, T=10, B=4, N=16, theta=1.0, b_th=0.2, beta=100.0, row_ptr=FAKE, col_idx=FAKE, g=FAKE, cap=100,
+             nnz=FAKE, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return lib.snn_active_compact(a["V"], a["T"], a["B"], a["N"], a["theta"], a["b_th"], a["beta"], a["row_ptr"],
+                                  a["col_idx"], a["g"], a["cap"], a["nnz"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(V=None), dict(row_ptr=None), dict(nnz=None), dict(ws=None), dict(N=0),
+                                dict(b_th=-0.1), dict(b_th=NAN), dict(theta=NAN), dict(beta=NAN), dict(beta=-1.0),
+                                dict(cap=-1), dict(col_idx=None), dict(ws_bytes=8)])
+def test_compact_rejects(lib, kw):
+    assert _cmp(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_workspace_queries(lib):
+    assert lib.snn_active_compact_workspace(10, 4, 16) > 0
+    assert lib.snn_active_compact_workspace(0, 4, 16) == 0
+    assert lib.snn_sparse_backward_workspace(500, 256, 1024, 1024) > 0
+    assert lib.snn_sparse_backward_workspace(10, 4, 0, 16) == 0
+    assert lib.snn_dense_backward_workspace(500, 256, 1024, 1024) >= 2 * 500 * 256 * 1024 * 4
+    assert lib.snn_readout_ce_workspace(10, 4, 3, 0) > 0
+    assert lib.snn_readout_ce_workspace(10, 4, 3, 2) == 0
+    # deterministic: the same dimensions always give the same size
+    assert lib.snn_sparse_backward_workspace(100, 256, 784, 200) == lib.snn_sparse_backward_workspace(100, 256, 784,
+                                                                                                       200)
+
+
+def _sb(lib, **kw):
+    a = dict(W=FAKE, tr=FAKE, T=10, B=4, N_in=32, N_out=16, alpha=0.9, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE,
+             ocap=10, irp=FAKE, ici=FAKE, icap=10, eps_in=FAKE, dW=FAKE, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.snn_sparse_backward(a["W"], a["tr"], a["T"], a["B"], a["N_in"], a["N_out"], a["alpha"], a["orp"],
+                                   a["oci"], a["og"], a["oeps"], a["ocap"], a["irp"], a["ici"], a["icap"],
+                                   a["eps_in"], a["dW"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(W=None), dict(tr=None), dict(orp=None), dict(dW=None), dict(oci=None),
+                                dict(oeps=None), dict(alpha=2.0), dict(ocap=-1), dict(icap=-5), dict(ws_bytes=16),
+                                dict(irp=None), dict(eps_in=None), dict(T=0), dict(N_out=-3)])
+def test_sparse_backward_rejects(lib, kw):
+    assert _sb(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_sparse_backward_unsupported_width(lib):
+    assert _sb(lib, N_out=5000) == snn.SNN_ERR_UNSUPPORTED
+
+
+def _db(lib, **kw):
+    a = dict(W=FAKE, tr=FAKE, V=FAKE, eps=FAKE, T=10, B=4, N_in=32, N_out=16, alpha=0.9, theta=1.0, b_th=0.2,
+             beta=100.0, gi=FAKE, dW=FAKE, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.snn_dense_backward_ref(a["W"], a["tr"], a["V"], a["eps"], a["T"], a["B"], a["N_in"], a["N_out"],
+                                      a["alpha"], a["theta"], a["b_th"], a["beta"], a["gi"], a["dW"], a["ws"],
+                                      a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(W=None), dict(eps=None), dict(dW=None), dict(V=None), dict(b_th=-1.0),
+                                dict(beta=NAN), dict(theta=NAN), dict(alpha=-0.5), dict(ws_bytes=4), dict(B=0)])
+def test_dense_backward_rejects(lib, kw):
+    assert _db(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(mode=2), dict(V=None), dict(labels=None), dict(C=0), dict(ws_bytes=1)])
+def test_readout_rejects(lib, kw):
+    a = dict(V=FAKE, labels=FAKE, T=10, B=4, C=3, mode=0, rp=FAKE, ci=FAKE, eps=FAKE, loss=FAKE, dense=None,
+             ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    st = lib.snn_readout_ce(a["V"], a["labels"], a["T"], a["B"], a["C"], a["mode"], a["rp"], a["ci"], a["eps"],
+                            a["loss"], a["dense"], a["ws"], a["ws_bytes"], None)
+    assert st == snn.SNN_ERR_INVALID_ARG

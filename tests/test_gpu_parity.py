@@ -1,0 +1,221 @@
+"""GPU path (through the C ABI) against the CPU oracle, element by element.
+
+Bar: spikes, V, traces and active-set CSR bit-exact; gradients within 1e-4 of the oracle's
+magnitude envelope, |x - r| <= 1e-4 * r_abs, where r_abs is the same contraction taken with
+absolute values (so cancellation cannot hide or fake an error).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2105_08810_amd import pipeline, snn
+from synth import CONFIGS, make_inputs
+from synth.inputs import Config
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-4
+F64 = np.float64
+
+
+def _oracle(inp, b_th):
+    cfg = inp.cfg
+    f = oracle.network_forward(inp.X, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, np.float32(cfg.theta))
+    args = (inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, inp.labels, cfg.loss_mode, cfg.theta, b_th, cfg.beta)
+    r = oracle.network_backward(f, *args)
+    env = oracle.network_backward(f, *args, absolute=True)
+    csrs = [oracle.active_csr(V, cfg.theta, b_th, cfg.beta) for V in f["V"]]
+    return f, r, env, csrs
+
+
+def _gpu(inp, b_th, dense=True):
+    net = pipeline.from_inputs(inp).forward()
+    ro = net.readout(dense=True)
+    csrs = net.compact(b_th)
+    dWs, dW_out, epss = net.sparse_backward(csrs, ro)
+    out = {"net": net, "ro": ro, "csrs": csrs, "dW": dWs, "dW_out": dW_out, "eps": epss}
+    if dense:
+        ddW, ddW_out, deps = net.dense_backward(b_th, ro)
+        out.update(ddW=ddW, ddW_out=ddW_out, deps=deps)
+    torch.cuda.synchronize()
+    return out
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def assert_bits(x, r, what):
+    x, r = np.asarray(x), np.asarray(r)
+    assert x.shape == r.shape, (what, x.shape, r.shape)
+    if x.dtype == np.float32:
+        same = x.view(np.uint32) == r.view(np.uint32)
+    else:
+        same = x == r
+    if not same.all():
+        k = np.argwhere(~same)[0]
+        raise AssertionError(f"{what}: {int((~same).sum())} of {same.size} differ, first at {tuple(k)}: "
+                             f"{x[tuple(k)]!r} vs {r[tuple(k)]!r}")
+
+
+def assert_env(x, r, env, what, tol=TOL):
+    x = np.asarray(x, F64)
+    err = np.abs(x - r)
+    bad = err > tol * env + 1e-30
+    if bad.any():
+        ratio = (err / np.maximum(env, 1e-300)).max()
+        raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} outside 1e-4 envelope, worst err/env {ratio:.3g}")
+    return float(err.max() / max(np.abs(r).max(), 1e-300))
+
+
+def check_all(inp, b_th, g, ref, dense=True):
+    f, r, env, ocsr = ref
+    net = g["net"]
+    # forward, bit for bit
+    for l in range(net.L):
+        assert_bits(_np(net.V[l]), f["V"][l], f"V[{l}]")
+        assert_bits(_np(net.S[l]), f["S"][l], f"S[{l}]")
+        assert_bits(_np(net.trace[l]), f["trace"][l], f"trace[{l}]")
+    assert_bits(_np(net.V_out), f["V_out"], "V_out")
+    assert_bits(_np(net.trace_out), f["trace_out"], "trace_out")
+    # active sets, bit for bit; g to float32 rounding
+    for l, (c, (rp, ci, gg)) in enumerate(zip(g["csrs"], ocsr)):
+        nnz = c.nnz()
+        assert nnz == rp[-1], (l, nnz, rp[-1])
+        assert_bits(_np(c.row_ptr).astype(np.int64), rp, f"row_ptr[{l}]")
+        assert_bits(_np(c.col_idx)[:nnz].astype(np.int64), ci, f"col_idx[{l}]")
+        assert np.allclose(_np(c.g)[:nnz], gg, rtol=2e-6, atol=0), f"g[{l}]"
+    # readout
+    ro_csr, ro_eps, loss = g["ro"][0], g["ro"][1], g["ro"][2]
+    rro = r["readout"]
+    assert abs(float(loss.item()) - rro["loss"]) <= 1e-5 * max(1.0, abs(rro["loss"]))
+    assert_bits(_np(ro_csr.row_ptr).astype(np.int64), rro["row_ptr"], "readout row_ptr")
+    assert_bits(_np(ro_csr.col_idx).astype(np.int64), rro["col_idx"], "readout col_idx")
+    # dL/da = (softmax(a) - y)/B: float32 logits (a sum over T steps in mode 'sum') move p by a
+    # relative amount of the logits' rounding, so the bar is the gradient bar relative to max |dL/da|
+    assert np.abs(_np(ro_eps) - rro["eps"]).max() <= TOL * np.abs(rro["eps"]).max()
+    # sparse gradients
+    assert_env(_np(g["dW_out"]), r["dW_out"], env["dW_out"], "dW_out")
+    for l in range(net.L):
+        assert_env(_np(g["dW"][l]), r["dW"][l], env["dW"][l], f"dW[{l}]")
+        rp, ci, _ = ocsr[l]
+        nnz = int(rp[-1])
+        ref_e = oracle.csr_values(r["eps"][l], rp, ci)
+        env_e = oracle.csr_values(env["eps"][l], rp, ci)
+        assert_env(_np(g["eps"][l])[:nnz], ref_e, env_e, f"eps[{l}] at active entries")
+    if dense:
+        assert_env(_np(g["ddW_out"]), r["dW_out"], env["dW_out"], "dense dW_out")
+        for l in range(net.L):
+            assert_env(_np(g["ddW"][l]), r["dW"][l], env["dW"][l], f"dense dW[{l}]")
+            assert_env(_np(g["deps"][l]), r["eps"][l], env["eps"][l], f"dense eps[{l}]")
+
+
+_CACHE = {}
+
+
+def _case(name, batch=None):
+    key = (name, None if batch is None else tuple(batch))
+    if key not in _CACHE:
+        _CACHE[key] = make_inputs(CONFIGS[name], batch)
+    return _CACHE[key]
+
+
+def _ragged():
+    cfg = Config("ragged", 201, T=37, B=3, sizes=(61, 37, 29, 5), tau_ratio_hidden=0.15, tau_ratio_out=0.1,
+                 loss_mode="max", b_th=0.3, kind="bernoulli", rate=0.1)
+    return make_inputs(cfg, sigmas=[0.25, 0.3, 1 / math.sqrt(29)])
+
+
+def _ragged_sum():
+    cfg = Config("ragged_sum", 202, T=9, B=5, sizes=(130, 70, 3), tau_ratio_hidden=0.2, tau_ratio_out=0.1,
+                 loss_mode="sum", b_th=0.25, kind="bernoulli", rate=0.15)
+    return make_inputs(cfg, sigmas=[0.2, 1 / math.sqrt(70)])
+
+
+@pytest.mark.parametrize("name,batch,b_th", [
+    ("tiny", None, 0.2),
+    ("tiny", None, math.inf),
+    ("latency", None, 0.2),
+    ("audio", None, 0.2),
+    ("event", None, 0.05),
+    ("event", None, 0.2),
+    ("event", None, 0.5),
+    ("stress", list(range(8)), 0.02),
+    ("stress", list(range(8)), 0.2),
+    ("stress", list(range(8)), 0.8),
+])
+def test_parity_configs(name, batch, b_th):
+    print(f"\n[case] {name} batch={'all' if batch is None else len(batch)} b_th={b_th}", flush=True)
+    inp = _case(name, batch)
+    ref = _oracle(inp, b_th)
+    g = _gpu(inp, b_th, dense=True)
+    check_all(inp, b_th, g, ref, dense=True)
+
+
+@pytest.mark.parametrize("maker,b_th", [(_ragged, 0.3), (_ragged, math.inf), (_ragged_sum, 0.25)])
+def test_parity_ragged_shapes(maker, b_th):
+    """Sizes that are not multiples of 4, 64 or any tile (unaligned paths, partial tiles)."""
+    inp = maker()
+    print(f"\n[case] {inp.cfg.name} b_th={b_th}", flush=True)
+    check_all(inp, b_th, _gpu(inp, b_th), _oracle(inp, b_th))
+
+
+def test_zero_band_is_empty():
+    inp = _case("tiny")
+    ref = _oracle(inp, 0.0)
+    g = _gpu(inp, 0.0)
+    for c in g["csrs"]:
+        assert c.nnz() == 0
+    for l in range(len(inp.Ws)):
+        assert np.all(_np(g["dW"][l]) == 0) and np.all(_np(g["ddW"][l]) == 0)
+    check_all(inp, 0.0, g, ref)
+
+
+def test_degenerate_time_and_batch():
+    """T = 1 (no update at all), T = 2 and B = 1."""
+    for T, B in ((1, 2), (2, 1), (3, 1)):
+        cfg = Config(f"deg{T}{B}", 203, T=T, B=B, sizes=(16, 8, 3), tau_ratio_hidden=0.1, tau_ratio_out=0.1,
+                     loss_mode="max", b_th=2.0, kind="bernoulli", rate=0.5)
+        inp = make_inputs(cfg, sigmas=[0.6, 0.5])
+        check_all(inp, 2.0, _gpu(inp, 2.0), _oracle(inp, 2.0))
+
+
+def test_compaction_capacity_overflow_is_safe():
+    """A capacity below nnz: the true nnz is reported and nothing past capacity is written."""
+    inp = _case("latency", list(range(16)))
+    net = pipeline.from_inputs(inp).forward()
+    V = net.V[0]
+    T, B, N = V.shape
+    full = snn.active_compact(V, 1.0, 0.2, 100.0)
+    nnz = full.nnz()
+    cap = nnz // 2
+    col = torch.full((cap + 64,), -7, dtype=torch.int32, device="cuda")
+    gg = torch.full((cap + 64,), -7.0, dtype=torch.float32, device="cuda")
+    row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device="cuda")
+    nnz_dev = torch.empty(1, dtype=torch.int64, device="cuda")
+    ws = snn.workspace(snn.snn_active_compact_workspace(T, B, N))
+    snn.snn_active_compact(V, T, B, N, 1.0, 0.2, 100.0, row_ptr, col, gg, cap, nnz_dev, ws)
+    torch.cuda.synchronize()
+    assert int(nnz_dev.item()) == nnz
+    assert torch.equal(col[:cap], full.col_idx[:cap]) and torch.equal(gg[:cap], full.g[:cap])
+    assert bool((col[cap:] == -7).all()) and bool((gg[cap:] == -7.0).all())
+    # the backward reads such a CSR safely (entries past capacity are ignored)
+    eps = torch.ones(cap, dtype=torch.float32, device="cuda")
+    trunc = snn.Csr(row_ptr, col[:cap].contiguous(), gg[:cap].contiguous(), nnz_dev, cap)
+    dW, _ = snn.sparse_backward(net.Ws[0], net.trace[0], net.alphas[0], trunc, eps)
+    torch.cuda.synchronize()
+    assert torch.isfinite(dW).all()
+
+
+def test_run_to_run_determinism():
+    inp = _case("latency", list(range(32)))
+    a = _gpu(inp, 0.2, dense=False)
+    b = _gpu(inp, 0.2, dense=False)
+    for l in range(len(inp.Ws)):
+        assert torch.equal(a["net"].V[l], b["net"].V[l])
+        assert torch.equal(a["csrs"][l].row_ptr, b["csrs"][l].row_ptr)
+        n = a["csrs"][l].nnz()
+        assert torch.equal(a["csrs"][l].col_idx[:n], b["csrs"][l].col_idx[:n])
+        assert torch.equal(a["eps"][l][:n], b["eps"][l][:n])  # grad_in sums in a fixed order
