@@ -1,11 +1,13 @@
 // Sparse backward of one LIF layer (Sec. 2.2): only active neurons carry gradient.
 //
 // dW (sparse form of Eq. (w_grad)): dW[:, j] += G[t,b,j] * trace[t,b,:] for every active
-//   output entry (t,b,j), G = eps * g. A block owns a tile of TI input neurons for ALL output
-//   neurons in LDS (layout [N_out][TI+1], so lanes over i hit distinct banks) and a chunk of
-//   rows; each lane group streams the trace slice of one row and adds G*trace into column j
-//   with LDS float64 atomics. Each block writes its tile once; a deterministic reduction over
-//   row chunks produces dW. Trace bytes are read exactly once over the whole grid.
+//   output entry (t,b,j), G = eps * g. A block owns 64 input neurons (one per lane) times a
+//   slab of up to kSlab output neurons in LDS as float64 accumulators ([slab][65]), and a
+//   chunk of rows. A wavefront streams the 256-byte trace slices of a batch of rows, finds
+//   each row's entries inside the slab with two ballots (column indices are ascending inside
+//   a row), and adds G*trace into the slab row by row; every entry is uniform across the
+//   wavefront, so one float64 LDS atomic covers 64 multiply-adds. Blocks write their slab
+//   once; a fixed-order reduction over row chunks produces dW.
 //
 // grad_in (sparse form of Eq. (s_grad)): eps_in[t,b,i] = sum_j W[i,j] delta[t,b,j] at the
 //   input layer's active entries, with delta[t] = alpha delta[t+1] + G[t+1] (Proposition 1's
@@ -21,7 +23,9 @@ namespace snn {
 namespace {
 
 constexpr int kDwThreads = 1024;
-constexpr int kRowsPerBatch = 32;
+constexpr int kRowsPerBatch = 8;  // rows a wavefront has in flight
+constexpr int kSlab = 256;        // output neurons per LDS slab
+constexpr int kLd = kWave + 1;    // padded slab row: 64 inputs + 1
 constexpr int kDwWaves = kDwThreads / kWave;
 constexpr size_t kLdsBudget = 150 * 1024;
 constexpr int kWalkThreads = 256;
@@ -30,26 +34,22 @@ constexpr int kGinBatch = 4;
 constexpr int kAssumedCUs = 256;
 
 struct DwPlan {
-  int TI, n_itiles, n_chunks, rows_per_chunk;
+  int n_itiles, n_slabs, slab, n_chunks, rows_per_chunk;
   size_t lds;
 };
 
 DwPlan plan_dw(int T, int B, int N_in, int N_out) {
   DwPlan p{};
   const int TB = T * B;
-  p.TI = 8;
-  for (int ti : {64, 32, 16, 8}) {
-    if ((size_t)N_out * (ti + 1) * sizeof(double) <= kLdsBudget) {
-      p.TI = ti;
-      break;
-    }
-  }
-  p.lds = (size_t)N_out * (p.TI + 1) * sizeof(double);
-  p.n_itiles = (N_in + p.TI - 1) / p.TI;
+  p.n_slabs = (N_out + kSlab - 1) / kSlab;
+  p.slab = (N_out + p.n_slabs - 1) / p.n_slabs;
+  p.lds = (size_t)p.slab * kLd * sizeof(double);
+  p.n_itiles = (N_in + kWave - 1) / kWave;
   const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(2, (160 * 1024) / p.lds));
   const int target = kAssumedCUs * per_cu;
-  int nc = (target + p.n_itiles - 1) / p.n_itiles;
-  nc = std::min(nc, std::max(1, TB / (4 * N_out)));  // partial tiles stay small next to the trace
+  const int tiles = p.n_itiles * p.n_slabs;
+  int nc = (target + tiles - 1) / tiles;
+  nc = std::min(nc, std::max(1, TB / (4 * N_out)));  // partial slabs stay small next to the trace
   nc = std::min(nc, 64);
   nc = std::max(nc, 1);
   p.rows_per_chunk = (TB + nc - 1) / nc;
@@ -79,101 +79,81 @@ __device__ __forceinline__ float rdlane(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Each wavefront takes batches of kRowsPerBatch consecutive rows. G = 64/TI lane groups each
-// own every G-th row of the batch; lane il of a group holds trace[r, i0 + il]. All loads of
-// a batch (row pointers, trace slices, the first TI entries of every row) are issued before
-// any is used, so a wavefront keeps a whole batch in flight; the entries are then broadcast
-// inside each group with readlane (no LDS traffic besides the accumulation itself).
-template <int TI, bool HAS_G>
-__global__ __launch_bounds__(kDwThreads) void dw_tile_kernel(const float* __restrict__ trace, int TB, int N_in,
+// Block (it, sl, c): inputs [64 it, 64 it + 64), outputs [sl*slab, ...), rows of chunk c.
+// Blocks of one chunk are numbered so that they land on one XCD and share its L2 lines.
+template <bool HAS_G>
+__global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __restrict__ trace, int TB, int N_in,
                                                              int N_out, const int32_t* __restrict__ row_ptr,
                                                              const int32_t* __restrict__ col_idx,
                                                              const float* __restrict__ g,
                                                              const float* __restrict__ eps, int64_t cap,
                                                              float* __restrict__ out, int rows_per_chunk,
-                                                             int n_itiles) {
-  // float64 accumulators: gfx950 executes ds_add_f64 about twenty times faster than ds_add_f32
-  extern __shared__ double tile[];  // [N_out][TI + 1]
-  constexpr int G = kWave / TI;
-  constexpr int LD = TI + 1;
-  constexpr int RB = (16 * G < kRowsPerBatch) ? 16 * G : kRowsPerBatch;  // rows per wavefront batch
-  constexpr int KR = RB / G;                                            // rows per lane group
-  const int it = blockIdx.x % n_itiles;
-  const int c = blockIdx.x / n_itiles;
-  const int i0 = it * TI;
+                                                             int n_itiles, int n_slabs, int slab) {
+  extern __shared__ double acc[];  // [slab][kLd]
+  int id = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) id = (id & 7) * (nb >> 3) + (id >> 3);
+  const int tiles = n_itiles * n_slabs;
+  const int c = id / tiles;
+  const int it = (id - c * tiles) % n_itiles;
+  const int sl = (id - c * tiles) / n_itiles;
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int l = tid % kWave;
-  const int il = l % TI;
-  const int sub = l / TI;
-  const bool has_i = i0 + il < N_in;
+  const int i = it * kWave + l;
+  const bool has_i = i < N_in;
+  const int ic = has_i ? i : N_in - 1;
+  const int j0 = sl * slab;
+  const int j1 = min(N_out, j0 + slab);
 
-  for (int k = tid; k < N_out * LD; k += kDwThreads) tile[k] = 0.0;
+  for (int k = tid; k < slab * kLd; k += kDwThreads) acc[k] = 0.0;
   __syncthreads();
 
-  // Loads below are unconditional, from indices clamped into range, and masked afterwards with
-  // selects: a branch around a load would make the compiler wait for it before the next one.
   const int r_lo = c * rows_per_chunk;
   const int r_hi = min(TB, r_lo + rows_per_chunk);
-  const int ic = has_i ? i0 + il : 0;
-  for (int rb = r_lo + w * RB; rb < r_hi; rb += kDwWaves * RB) {
-    // row pointers first, then the trace slices: waiting for the former leaves the latter in flight
-    const int rp_raw = row_ptr[min(rb + min(l, RB), r_hi)];
-    float tr[KR];
+  for (int rb = r_lo + w * kRowsPerBatch; rb < r_hi; rb += kDwWaves * kRowsPerBatch) {
+    // every load of the batch is issued before any is used; indices are clamped into range
+    // and the results masked afterwards, since a branch around a load serialises the loads
+    const int rp_raw = row_ptr[min(rb + min(l, kRowsPerBatch), r_hi)];
+    float tr[kRowsPerBatch];
 #pragma unroll
-    for (int k = 0; k < KR; ++k) tr[k] = trace[(size_t)min(rb + sub + G * k, r_hi - 1) * N_in + ic];
+    for (int k = 0; k < kRowsPerBatch; ++k) tr[k] = trace[(size_t)min(rb + k, r_hi - 1) * N_in + ic];
     __builtin_amdgcn_sched_barrier(0);
     const int rp = clamp_entry(rp_raw, cap);
+    int jr[kRowsPerBatch];
+    float er[kRowsPerBatch], gr[kRowsPerBatch];
 #pragma unroll
-    for (int k = 0; k < KR; ++k) tr[k] = (rb + sub + G * k < r_hi && has_i) ? tr[k] : 0.0f;
-    int jv[KR];
-    float ev[KR], gr[KR];
-#pragma unroll
-    for (int k = 0; k < KR; ++k) {
-      const int q = sub + G * k;
-      const int e0 = __shfl(rp, q, kWave);
-      const int cnt = __shfl(rp, q + 1, kWave) - e0;
-      const int e = il < cnt ? e0 + il : 0;  // cap >= 1 here; lanes past the row are masked later
-      jv[k] = col_idx[e];
-      ev[k] = eps[e];
+    for (int k = 0; k < kRowsPerBatch; ++k) {
+      const int e0 = rdlane(rp, k);
+      const int cnt = rdlane(rp, k + 1) - e0;
+      const int e = min(e0 + min(l, max(cnt - 1, 0)), (int)cap - 1);  // cap >= 1 here
+      jr[k] = col_idx[e];
+      er[k] = eps[e];
       gr[k] = HAS_G ? g[e] : 1.0f;
     }
-    __builtin_amdgcn_sched_barrier(0);  // keep every load of the batch ahead of any use
-    float gv[KR];
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int k = 0; k < KR; ++k) gv[k] = ev[k] * gr[k];
-#pragma unroll
-    for (int k = 0; k < KR; ++k) {
-      const int q = sub + G * k;
-      const int e0 = __shfl(rp, q, kWave);
-      const int cnt = __shfl(rp, q + 1, kWave) - e0;
-      int mc = 0;
-#pragma unroll
-      for (int g2 = 0; g2 < G; ++g2) mc = max(mc, rdlane(cnt, g2 * TI));
-      for (int base = 0; base < mc; base += TI) {
-        if (base > 0) {  // rows longer than TI entries: next window
-          const int e = base + il < cnt ? e0 + base + il : 0;
-          const int jj = col_idx[e];
-          const float ee = eps[e];
-          const float gg = HAS_G ? g[e] : 1.0f;
-          jv[k] = jj;
-          gv[k] = ee * gg;
+    for (int k = 0; k < kRowsPerBatch; ++k) {
+      const int r = rb + k;
+      const float t = (r < r_hi && has_i) ? tr[k] : 0.0f;
+      const int e0 = rdlane(rp, k);
+      const int cnt = rdlane(rp, k + 1) - e0;
+      for (int base = 0; base < cnt; base += kWave) {
+        int jv = jr[k];
+        float gv = er[k] * gr[k];
+        if (base > 0) {  // rows with more than 64 entries: next window
+          const int e = e0 + min(base + l, cnt - 1);
+          jv = col_idx[e];
+          gv = eps[e] * (HAS_G ? g[e] : 1.0f);
         }
-        const int ns = min(TI, mc - base);
-        for (int s = 0; s < ns; ++s) {
-          int j = -1;
-          float Gv = 0.0f;
-#pragma unroll
-          for (int g2 = 0; g2 < G; ++g2) {
-            const int jj = rdlane(jv[k], g2 * TI + s);
-            const float gg = rdlane(gv[k], g2 * TI + s);
-            if (sub == g2) {
-              j = jj;
-              Gv = gg;
-            }
-          }
-          if (base + s < cnt && (unsigned)j < (unsigned)N_out && has_i)
-            atomicAdd(&tile[j * LD + il], (double)(Gv * tr[k]));
+        const bool valid = base + l < cnt;
+        // column indices ascend inside a row: the slab's entries are one contiguous run
+        const int lo = __popcll(__ballot(valid && jv < j0));
+        const int hi = lo + __popcll(__ballot(valid && jv >= j0 && jv < j1));
+        for (int s = lo; s < hi; ++s) {
+          const int jj = rdlane(jv, s) - j0;
+          const float G = rdlane(gv, s);
+          atomicAdd(&acc[jj * kLd + l], (double)(G * t));
         }
       }
     }
@@ -181,10 +161,11 @@ __global__ __launch_bounds__(kDwThreads) void dw_tile_kernel(const float* __rest
   __syncthreads();
 
   float* dst = out + (size_t)c * N_in * N_out;
-  for (int k = tid; k < TI * N_out; k += kDwThreads) {
-    const int ii = k / N_out;
-    const int jj = k - ii * N_out;
-    if (i0 + ii < N_in) dst[(size_t)(i0 + ii) * N_out + jj] = (float)tile[jj * LD + ii];
+  const int width = j1 - j0;
+  for (int k = tid; k < kWave * width; k += kDwThreads) {
+    const int ii = k / width;
+    const int jj = k - ii * width;
+    if (it * kWave + ii < N_in) dst[(size_t)(it * kWave + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
   }
 }
 
@@ -256,11 +237,31 @@ __global__ void gin_carries(int T, int B, int N_out, float alpha, int P, int C, 
   }
 }
 
+// Sum over the wavefront of four values at once (one per entry u): two exchanges across
+// halves and across rows leave each 16-lane row holding entry u = row index summed over 4
+// lanes; four DPP steps then finish the sum inside the row. Returns the total of entry
+// (lane >> 4) in every lane of that row.
+__device__ __forceinline__ float wave_sum4(float a0, float a1, float a2, float a3) {
+  const int l = lane_id();
+  const bool b5 = (l >> 5) & 1;
+  const bool b4 = (l >> 4) & 1;
+  const float s0 = b5 ? a0 : a2, s1 = b5 ? a1 : a3;
+  const float k0 = b5 ? a2 : a0, k1 = b5 ? a3 : a1;
+  const float c0 = k0 + __shfl_xor(s0, 32, kWave);
+  const float c1 = k1 + __shfl_xor(s1, 32, kWave);
+  float v = (b4 ? c1 : c0) + __shfl_xor(b4 ? c0 : c1, 16, kWave);
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true));   // quad_perm 1,0,3,2
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, true));   // quad_perm 2,3,0,1
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, true));  // row_half_mirror
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, true));  // row_mirror
+  return v;
+}
+
 // One wavefront per (chunk c, sample b). delta[b, 0:N_out] lives in registers: lane l holds
 // j = l + 64 m. The row pointers of all steps of the chunk are loaded once; at each step the
-// input-active entries are taken kGinBatch at a time so that kGinBatch * NJ W loads are in
-// flight, each reduced over the wavefront; then delta <- alpha delta + G[t] with the step's
-// active outputs broadcast by readlane.
+// input-active entries are taken four at a time (4 * NJ W loads in flight) and reduced
+// together; then delta <- alpha delta + G[t], each active output added by the lane that owns
+// its column (a uniform register index).
 template <int NJ>
 __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict__ W, int T, int B, int N_in,
                                                          int N_out, float alpha, int P, int C,
@@ -303,19 +304,14 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
 #pragma unroll
       for (int u = 0; u < kGinBatch; ++u) {
         const int x = ici[min(e + u, i1 - 1)];
-        iv[u] = (e + u < i1) ? x : -1;
+        iv[u] = (e + u < i1 && (unsigned)x < (unsigned)N_in) ? x : -1;
       }
       float wv[kGinBatch][NJ];
 #pragma unroll
       for (int u = 0; u < kGinBatch; ++u) {
-        const bool ok = (unsigned)iv[u] < (unsigned)N_in;
-        const float* wr = W + (size_t)(ok ? iv[u] : 0) * N_out;
+        const float* wr = W + (size_t)(iv[u] >= 0 ? iv[u] : 0) * N_out;
 #pragma unroll
-        for (int m = 0; m < NJ; ++m) {
-          const int j = l + kWave * m;
-          const float x = wr[min(j, N_out - 1)];
-          wv[u][m] = (ok && j < N_out) ? x : 0.0f;
-        }
+        for (int m = 0; m < NJ; ++m) wv[u][m] = wr[min(l + kWave * m, N_out - 1)];
       }
       __builtin_amdgcn_sched_barrier(0);
       float acc[kGinBatch];
@@ -323,13 +319,13 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
       for (int u = 0; u < kGinBatch; ++u) {
         acc[u] = 0.0f;
 #pragma unroll
-        for (int m = 0; m < NJ; ++m) acc[u] += wv[u][m] * d[m];
+        for (int m = 0; m < NJ; ++m)
+          if (l + kWave * m < N_out) acc[u] += wv[u][m] * d[m];
+        acc[u] = iv[u] >= 0 ? acc[u] : 0.0f;
       }
-#pragma unroll
-      for (int u = 0; u < kGinBatch; ++u) {
-        const float s = wave_sum(acc[u]);
-        if (l == 0 && e + u < i1) eps_in[e + u] = s;
-      }
+      const float tot = wave_sum4(acc[0], acc[1], acc[2], acc[3]);
+      const int u = l >> 4;
+      if ((l & 15) == 0 && e + u < i1) eps_in[e + u] = tot;
     }
     // delta[t-1] = alpha delta[t] + G[t]
 #pragma unroll
@@ -348,11 +344,8 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
         const int j = rdlane(jv, s);
         const float G = rdlane(gv, s);
         if ((unsigned)j < (unsigned)N_out) {
-          const int jm = j / kWave;
-          const bool mine = l == (j % kWave);
-#pragma unroll
-          for (int m = 0; m < NJ; ++m)
-            if (m == jm && mine) d[m] += G;
+          const int jm = j / kWave;  // uniform: a register index, not a branch per m
+          d[jm] += (l == j % kWave) ? G : 0.0f;
         }
       }
     }
@@ -410,34 +403,28 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
   float* part = p.n_chunks > 1 ? ws.take<float>((size_t)p.n_chunks * N_in * N_out) : dW;
   float* Lbuf = ws.take<float>((size_t)wp.C * B * N_out);
 
-  const dim3 dgrid((unsigned)(p.n_itiles * p.n_chunks));
-  if (out_cap == 0) {  // no active entry: dW = 0, and no entry array may be read
+  if (out_cap == 0) {  // no active output entry: dW = 0 and eps_in = 0; no entry array is read
     hipLaunchKernelGGL(fill_zero, dim3((unsigned)std::min<size_t>(((size_t)N_in * N_out + 255) / 256, 4096)),
                        dim3(256), 0, s, dW, (size_t)N_in * N_out);
+    if (grad_in && in_cap > 0)
+      hipLaunchKernelGGL(fill_zero, dim3((unsigned)std::min<int64_t>((in_cap + 255) / 256, 4096)), dim3(256), 0, s,
+                         eps_in, (size_t)in_cap);
     return launch_status();
   }
-#define SNN_DW2(TI_, HG_)                                                                                 \
-  do {                                                                                                     \
-    (void)hipFuncSetAttribute((const void*)dw_tile_kernel<TI_, HG_>,                                       \
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);                     \
-    hipLaunchKernelGGL((dw_tile_kernel<TI_, HG_>), dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in,  \
-                       N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, part, p.rows_per_chunk,   \
-                       p.n_itiles);                                                                        \
-  } while (0)
-#define SNN_DW(TI_)             \
-  do {                          \
-    if (out_g)                  \
-      SNN_DW2(TI_, true);       \
-    else                        \
-      SNN_DW2(TI_, false);      \
-  } while (0)
-  switch (p.TI) {
-    case 64: SNN_DW(64); break;
-    case 32: SNN_DW(32); break;
-    case 16: SNN_DW(16); break;
-    default: SNN_DW(8); break;
+  const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
+  if (out_g) {
+    (void)hipFuncSetAttribute((const void*)dw_slab_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)p.lds);
+    hipLaunchKernelGGL(dw_slab_kernel<true>, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out,
+                       out_row_ptr, out_col_idx, out_g, eps_out, out_cap, part, p.rows_per_chunk, p.n_itiles,
+                       p.n_slabs, p.slab);
+  } else {
+    (void)hipFuncSetAttribute((const void*)dw_slab_kernel<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)p.lds);
+    hipLaunchKernelGGL(dw_slab_kernel<false>, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out,
+                       out_row_ptr, out_col_idx, out_g, eps_out, out_cap, part, p.rows_per_chunk, p.n_itiles,
+                       p.n_slabs, p.slab);
   }
-#undef SNN_DW
   if (p.n_chunks > 1) {
     const size_t n = (size_t)N_in * N_out;
     const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
