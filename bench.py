@@ -95,6 +95,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=16)
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--serial", action="store_true", help="no auxiliary stream in the sparse backward")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the path is single-device here (multi-GPU is design only)",
@@ -118,11 +119,13 @@ def main():
     ro = net.readout(dense=not args.no_dense)
     csrs = net.compact(b_th)
     caps = [c.capacity for c in csrs]
-    ws_sp = [snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[l], sizes[l + 1])) for l in range(L)]
-    ws_ro = snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[L], sizes[L + 1]))
+    ws_sp = [snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[l], sizes[l + 1], caps[l]))
+             for l in range(L)]
+    ws_ro = snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[L], sizes[L + 1], ro[0].capacity))
     ws_dn = None if args.no_dense else snn.workspace(
         max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
     stream = torch.cuda.current_stream()
+    aux = None if args.serial else torch.cuda.Stream()  # default priority
 
     def step(ev):
         ev[0].record(stream)
@@ -133,12 +136,12 @@ def main():
         cs = net.compact(b_th, caps)
         ev[3].record(stream)
         dW_out, eps = snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1], inp=cs[L - 1],
-                                          ws=ws_ro)
+                                          ws=ws_ro, aux_stream=aux)
         ev[4].record(stream)
         for l in range(L - 1, -1, -1):
             ev[5 + 2 * (L - 1 - l)].record(stream)
             _, eps = snn.sparse_backward(net.Ws[l], net.trace[l], net.alphas[l], cs[l], eps,
-                                         inp=cs[l - 1] if l > 0 else None, ws=ws_sp[l])
+                                         inp=cs[l - 1] if l > 0 else None, ws=ws_sp[l], aux_stream=aux)
             ev[6 + 2 * (L - 1 - l)].record(stream)
         k = 5 + 2 * L
         if not args.no_dense:

@@ -104,16 +104,21 @@ snn_status snn_active_compact(const float* V, int T, int B, int N, float theta, 
  *   dW         [N_in,N_out] float32 (overwritten).
  *   out_cap / in_cap are the allocated lengths of the entry arrays; entries at or beyond them
  *   are ignored, so a CSR whose compaction overflowed its capacity is read safely (and gives
- *   a truncated result).
+ *   a truncated result). The workspace size depends on out_cap (a slab-major copy of the
+ *   active entries is built in it).
+ *   aux_stream (may be NULL): a second hipStream_t. When given, the spike-gradient part runs on
+ *   it beside the dW part on `stream`; the call makes aux_stream wait for the work already on
+ *   `stream`, and `stream` wait for the aux work, so work enqueued on `stream` afterwards sees
+ *   both results. Creates two HIP events per call.
  * Supported: N_out <= 4096.
  */
-size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out);
+size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out, int64_t out_cap);
 snn_status snn_sparse_backward(const float* W, const float* trace_in, int T, int B, int N_in, int N_out,
                                float alpha, const int32_t* out_row_ptr, const int32_t* out_col_idx,
                                const float* out_g, const float* eps_out, int64_t out_cap,
                                const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap,
                                float* eps_in, float* dW, void* workspace, size_t workspace_bytes,
-                               void* stream);
+                               void* stream, void* aux_stream);
 
 /*
  * Dense surrogate BPTT of one layer on matrix cores: the baseline the sparse rule is

@@ -1,11 +1,15 @@
 // Active-set compaction (Definition 1) into CSR, with the truncated spike derivative
 // g(V) = 1/(beta |V - theta| + 1)^2 at each active entry (Definition 2; surrogate of Sec. 3).
 //
-// Three passes over rows r = t*B + b of V [T*B, N]:
-//   count  one wavefront per row: predicate per element, wave ballot + popcount -> counts[r]
+// Three passes over rows r = t*B + b of V [T*B, N]; V is read once unless a row holds more
+// than kStage active entries:
+//   count  one wavefront per row: predicate per element, wave ballot + lane prefix (mbcnt)
+//          give each active element its rank in the row; the first kStage (column, g) pairs are
+//          staged in the workspace and the row's count is written
 //   scan   device-wide exclusive scan -> row_ptr, nnz
-//   fill   one wavefront per row: ballot + lane prefix (mbcnt) give each active element its
-//          slot, so col_idx is ascending inside a row; entries at slots >= capacity are dropped.
+//   fill   one wavefront per row copies the staged pairs to their CSR slots (col_idx stays
+//          ascending inside a row); a row with more than kStage entries is re-read from V for
+//          the rest. Entries at slots >= capacity are dropped.
 // The predicate |V - theta| < b_th is evaluated in float32 exactly as written (one rounded
 // subtraction, then fabs and a strict compare), so the integer outputs are bit-exact.
 #include "common.h"
@@ -15,6 +19,12 @@ namespace {
 
 constexpr int kRowsPerBlock = 4;  // one wavefront per row
 constexpr int kThreads = kRowsPerBlock * kWave;
+constexpr int kStage = 64;  // staged entries per row
+
+struct Staged {
+  int32_t j;
+  float g;
+};
 
 __device__ __forceinline__ bool is_active(float v, float theta, float bth) { return fabsf(v - theta) < bth; }
 
@@ -25,35 +35,14 @@ __device__ __forceinline__ float surrogate(float v, float theta, float beta) {
 
 template <bool VEC>
 __global__ __launch_bounds__(kThreads) void compact_count(const float* __restrict__ V, int rows, int N, float theta,
-                                                          float bth, int32_t* __restrict__ counts) {
+                                                          float bth, float beta, int32_t* __restrict__ counts,
+                                                          Staged* __restrict__ stage, int scap) {
   const int l = lane_id();
   const int r = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
   if (r >= rows) return;
   const float* row = V + (size_t)r * N;
-  int c = 0;
-  if (VEC) {
-    for (int j = 4 * l; j < N; j += 4 * kWave) {
-      const float4 v = *reinterpret_cast<const float4*>(row + j);
-      c += is_active(v.x, theta, bth) + is_active(v.y, theta, bth) + is_active(v.z, theta, bth) +
-           is_active(v.w, theta, bth);
-    }
-  } else {
-    for (int j = l; j < N; j += kWave) c += is_active(row[j], theta, bth);
-  }
-  c = wave_sum_int(c);
-  if (l == 0) counts[r] = c;
-}
-
-template <bool VEC>
-__global__ __launch_bounds__(kThreads) void compact_fill(const float* __restrict__ V, int rows, int N, float theta,
-                                                         float bth, float beta, const int32_t* __restrict__ row_ptr,
-                                                         int32_t* __restrict__ col_idx, float* __restrict__ g_act,
-                                                         int64_t cap) {
-  const int l = lane_id();
-  const int r = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
-  if (r >= rows) return;
-  const float* row = V + (size_t)r * N;
-  int64_t base = row_ptr[r];
+  Staged* st = stage + (size_t)r * scap;
+  int base = 0;
   if (VEC) {
     // lane l holds elements 4l..4l+3 of each 256-wide slice; ascending order is (lane, q)
     for (int j0 = 0; j0 < N; j0 += 4 * kWave) {
@@ -65,13 +54,70 @@ __global__ __launch_bounds__(kThreads) void compact_fill(const float* __restrict
 #pragma unroll
       for (int q = 0; q < 4; ++q) a[q] = (j < N) && is_active(vv[q], theta, bth);
       const uint64_t m0 = __ballot(a[0]), m1 = __ballot(a[1]), m2 = __ballot(a[2]), m3 = __ballot(a[3]);
-      int64_t pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+      int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if (a[q]) {
-          if (pos < cap) {
-            col_idx[pos] = j + q;
-            if (g_act) g_act[pos] = surrogate(vv[q], theta, beta);
+          if (pos < scap) st[pos] = Staged{j + q, surrogate(vv[q], theta, beta)};
+          ++pos;
+        }
+      }
+      base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+    }
+  } else {
+    for (int j0 = 0; j0 < N; j0 += kWave) {
+      const int j = j0 + l;
+      const float v = j < N ? row[j] : 0.0f;
+      const bool a = (j < N) && is_active(v, theta, bth);
+      const uint64_t m = __ballot(a);
+      const int pos = base + mask_prefix(m);
+      if (a && pos < scap) st[pos] = Staged{j, surrogate(v, theta, beta)};
+      base += __popcll(m);
+    }
+  }
+  if (l == 0) counts[r] = base;
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void compact_fill(const float* __restrict__ V, int rows, int N, float theta,
+                                                         float bth, float beta, const int32_t* __restrict__ row_ptr,
+                                                         const Staged* __restrict__ stage, int scap,
+                                                         int32_t* __restrict__ col_idx, float* __restrict__ g_act,
+                                                         int64_t cap) {
+  const int l = lane_id();
+  const int r = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
+  if (r >= rows) return;
+  const int64_t dst = row_ptr[r];
+  const int cnt = row_ptr[r + 1] - row_ptr[r];
+  const Staged* st = stage + (size_t)r * scap;
+  for (int k = l; k < min(cnt, scap); k += kWave) {
+    const Staged x = st[k];
+    if (dst + k < cap) {
+      col_idx[dst + k] = x.j;
+      if (g_act) g_act[dst + k] = x.g;
+    }
+  }
+  if (cnt <= scap) return;
+  // more active entries than staged: walk the row again and place ranks >= scap
+  const float* row = V + (size_t)r * N;
+  int base = 0;
+  if (VEC) {
+    for (int j0 = 0; j0 < N; j0 += 4 * kWave) {
+      const int j = j0 + 4 * l;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (j < N) v = *reinterpret_cast<const float4*>(row + j);
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+      bool a[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) a[q] = (j < N) && is_active(vv[q], theta, bth);
+      const uint64_t m0 = __ballot(a[0]), m1 = __ballot(a[1]), m2 = __ballot(a[2]), m3 = __ballot(a[3]);
+      int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (a[q]) {
+          if (pos >= scap && dst + pos < cap) {
+            col_idx[dst + pos] = j + q;
+            if (g_act) g_act[dst + pos] = surrogate(vv[q], theta, beta);
           }
           ++pos;
         }
@@ -84,10 +130,10 @@ __global__ __launch_bounds__(kThreads) void compact_fill(const float* __restrict
       const float v = j < N ? row[j] : 0.0f;
       const bool a = (j < N) && is_active(v, theta, bth);
       const uint64_t m = __ballot(a);
-      const int64_t pos = base + mask_prefix(m);
-      if (a && pos < cap) {
-        col_idx[pos] = j;
-        if (g_act) g_act[pos] = surrogate(v, theta, beta);
+      const int pos = base + mask_prefix(m);
+      if (a && pos >= scap && dst + pos < cap) {
+        col_idx[dst + pos] = j;
+        if (g_act) g_act[dst + pos] = surrogate(v, theta, beta);
       }
       base += __popcll(m);
     }
@@ -105,6 +151,7 @@ extern "C" size_t snn_active_compact_workspace(int T, int B, int N) {
   Carve c(nullptr);
   c.take<int32_t>(rows);
   c.take<int32_t>(scan_temp_elems(rows));
+  c.take<Staged>((size_t)rows * std::min(N, kStage));
   return c.off;
 }
 
@@ -122,20 +169,24 @@ extern "C" snn_status snn_active_compact(const float* V, int T, int B, int N, fl
   Carve ws(workspace);
   int32_t* counts = ws.take<int32_t>(rows);
   int32_t* temp = ws.take<int32_t>(scan_temp_elems(rows));
+  const int scap = std::min(N, kStage);
+  Staged* stage = ws.take<Staged>((size_t)rows * scap);
   const bool vec = (N % 4) == 0 && (reinterpret_cast<uintptr_t>(V) % 16) == 0;
   const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock);
   if (vec)
-    hipLaunchKernelGGL(compact_count<true>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, counts);
+    hipLaunchKernelGGL(compact_count<true>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, counts, stage,
+                       scap);
   else
-    hipLaunchKernelGGL(compact_count<false>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, counts);
+    hipLaunchKernelGGL(compact_count<false>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, counts,
+                       stage, scap);
   launch_exclusive_scan(counts, rows, row_ptr, nnz_dev, temp, s);
   if (capacity > 0) {
     if (vec)
       hipLaunchKernelGGL(compact_fill<true>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, row_ptr,
-                         col_idx, g_act, capacity);
+                         stage, scap, col_idx, g_act, capacity);
     else
       hipLaunchKernelGGL(compact_fill<false>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, row_ptr,
-                         col_idx, g_act, capacity);
+                         stage, scap, col_idx, g_act, capacity);
   }
   return launch_status();
 }

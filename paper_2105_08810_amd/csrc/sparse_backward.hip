@@ -79,14 +79,59 @@ __device__ __forceinline__ float rdlane(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Block (it, sl, c): inputs [64 it, 64 it + 64), outputs [sl*slab, ...), rows of chunk c.
-// Blocks of one chunk are numbered so that they land on one XCD and share its L2 lines.
+// Slab-major copy of the active entries. For slab s and row r, sp[s*TB + r] is where row r's
+// entries with s*slab <= j < (s+1)*slab start; each record holds the entry's byte offset inside
+// its slab row of the LDS accumulator and G = eps * g.
+struct SlabRec {
+  int32_t off;
+  float G;
+};
+
+__global__ void slab_count(int TB, int n_slabs, int slab, const int32_t* __restrict__ row_ptr,
+                           const int32_t* __restrict__ col_idx, int64_t cap, int32_t* __restrict__ cnt) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= TB) return;
+  const int e0 = clamp_entry(row_ptr[r], cap);
+  const int e1 = clamp_entry(row_ptr[r + 1], cap);
+  int e = e0;
+  for (int sl = 0; sl < n_slabs; ++sl) {  // columns ascend: each slab's run follows the previous one
+    const int end = (sl + 1) * slab;
+    const int start = e;
+    while (e < e1 && col_idx[e] < end) ++e;
+    cnt[(size_t)sl * TB + r] = e - start;
+  }
+}
+
 template <bool HAS_G>
+__global__ void slab_fill(int TB, int N_out, int slab, const int32_t* __restrict__ row_ptr,
+                          const int32_t* __restrict__ col_idx, const float* __restrict__ g,
+                          const float* __restrict__ eps, int64_t cap, const int32_t* __restrict__ sp,
+                          SlabRec* __restrict__ rec) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= TB) return;
+  const int e0 = clamp_entry(row_ptr[r], cap);
+  const int e1 = clamp_entry(row_ptr[r + 1], cap);
+  int cur = -1, pos = 0;
+  for (int e = e0; e < e1; ++e) {
+    const int j = col_idx[e];
+    if ((unsigned)j >= (unsigned)N_out) continue;
+    const int sl = j / slab;
+    if (sl != cur) {
+      cur = sl;
+      pos = sp[(size_t)sl * TB + r];
+    }
+    SlabRec x;
+    x.off = (j - sl * slab) * kLd * (int)sizeof(double);
+    x.G = eps[e] * (HAS_G ? g[e] : 1.0f);
+    rec[pos++] = x;
+  }
+}
+
+// Block (it, sl, c): inputs [64 it, 64 it + 64), outputs of slab sl, rows of chunk c. Blocks of
+// one chunk are numbered so that they land on one XCD and share its L2 lines.
 __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __restrict__ trace, int TB, int N_in,
-                                                             int N_out, const int32_t* __restrict__ row_ptr,
-                                                             const int32_t* __restrict__ col_idx,
-                                                             const float* __restrict__ g,
-                                                             const float* __restrict__ eps, int64_t cap,
+                                                             int N_out, const int32_t* __restrict__ sp,
+                                                             const SlabRec* __restrict__ rec, int64_t nrec,
                                                              float* __restrict__ out, int rows_per_chunk,
                                                              int n_itiles, int n_slabs, int slab) {
   extern __shared__ double acc[];  // [slab][kLd]
@@ -105,6 +150,8 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   const int ic = has_i ? i : N_in - 1;
   const int j0 = sl * slab;
   const int j1 = min(N_out, j0 + slab);
+  const int32_t* spl = sp + (size_t)sl * TB;
+  char* accb = reinterpret_cast<char*>(acc) + l * (int)sizeof(double);
 
   for (int k = tid; k < slab * kLd; k += kDwThreads) acc[k] = 0.0;
   __syncthreads();
@@ -112,48 +159,39 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   const int r_lo = c * rows_per_chunk;
   const int r_hi = min(TB, r_lo + rows_per_chunk);
   for (int rb = r_lo + w * kRowsPerBatch; rb < r_hi; rb += kDwWaves * kRowsPerBatch) {
-    // every load of the batch is issued before any is used; indices are clamped into range
-    // and the results masked afterwards, since a branch around a load serialises the loads
-    const int rp_raw = row_ptr[min(rb + min(l, kRowsPerBatch), r_hi)];
+    // every load of the batch is issued before any is used (indices clamped into range,
+    // results masked afterwards: a branch around a load would serialise the loads)
+    const int spv = spl[min(rb + min(l, kRowsPerBatch), r_hi)];
     float tr[kRowsPerBatch];
 #pragma unroll
     for (int k = 0; k < kRowsPerBatch; ++k) tr[k] = trace[(size_t)min(rb + k, r_hi - 1) * N_in + ic];
     __builtin_amdgcn_sched_barrier(0);
-    const int rp = clamp_entry(rp_raw, cap);
-    int jr[kRowsPerBatch];
-    float er[kRowsPerBatch], gr[kRowsPerBatch];
-#pragma unroll
-    for (int k = 0; k < kRowsPerBatch; ++k) {
-      const int e0 = rdlane(rp, k);
-      const int cnt = rdlane(rp, k + 1) - e0;
-      const int e = min(e0 + min(l, max(cnt - 1, 0)), (int)cap - 1);  // cap >= 1 here
-      jr[k] = col_idx[e];
-      er[k] = eps[e];
-      gr[k] = HAS_G ? g[e] : 1.0f;
-    }
+    const int base = rdlane(spv, 0);
+    const int n = rdlane(spv, kRowsPerBatch) - base;
+    const int2* rec2 = reinterpret_cast<const int2*>(rec);
+    const int2 ra = rec2[min((int64_t)base + l, nrec - 1)];  // lane s holds the batch's record s
     __builtin_amdgcn_sched_barrier(0);
+    if (n <= kWave) {  // common case: the batch's records are all in one register
 #pragma unroll
-    for (int k = 0; k < kRowsPerBatch; ++k) {
-      const int r = rb + k;
-      const float t = (r < r_hi && has_i) ? tr[k] : 0.0f;
-      const int e0 = rdlane(rp, k);
-      const int cnt = rdlane(rp, k + 1) - e0;
-      for (int base = 0; base < cnt; base += kWave) {
-        int jv = jr[k];
-        float gv = er[k] * gr[k];
-        if (base > 0) {  // rows with more than 64 entries: next window
-          const int e = e0 + min(base + l, cnt - 1);
-          jv = col_idx[e];
-          gv = eps[e] * (HAS_G ? g[e] : 1.0f);
-        }
-        const bool valid = base + l < cnt;
-        // column indices ascend inside a row: the slab's entries are one contiguous run
-        const int lo = __popcll(__ballot(valid && jv < j0));
-        const int hi = lo + __popcll(__ballot(valid && jv >= j0 && jv < j1));
+      for (int k = 0; k < kRowsPerBatch; ++k) {
+        const double t = (rb + k < r_hi && has_i) ? (double)tr[k] : 0.0;
+        const int lo = rdlane(spv, k) - base;
+        const int hi = rdlane(spv, k + 1) - base;
         for (int s = lo; s < hi; ++s) {
-          const int jj = rdlane(jv, s) - j0;
-          const float G = rdlane(gv, s);
-          atomicAdd(&acc[jj * kLd + l], (double)(G * t));
+          const int off = rdlane(ra.x, s);
+          const float G = __int_as_float(rdlane(ra.y, s));
+          atomicAdd(reinterpret_cast<double*>(accb + off), t * (double)G);
+        }
+      }
+    } else {  // dense batch: records read one by one (uniform addresses)
+#pragma unroll
+      for (int k = 0; k < kRowsPerBatch; ++k) {
+        const double t = (rb + k < r_hi && has_i) ? (double)tr[k] : 0.0;
+        const int lo = rdlane(spv, k);
+        const int hi = rdlane(spv, k + 1);
+        for (int s = lo; s < hi; ++s) {
+          const int2 x = rec2[s];
+          atomicAdd(reinterpret_cast<double*>(accb + x.x), t * (double)__int_as_float(x.y));
         }
       }
     }
@@ -366,14 +404,19 @@ void launch_walk(dim3 grid, size_t lds, hipStream_t s, const float* W, int T, in
 
 using namespace snn;
 
-extern "C" size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out) {
-  if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out)) return 0;
+extern "C" size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out) || out_cap < 0) return 0;
   if (too_big(T, B, N_in) || too_big(T, B, N_out)) return 0;
   const DwPlan p = plan_dw(T, B, N_in, N_out);
   const WalkPlan wp = plan_walk(T);
   Carve c(nullptr);
   if (p.n_chunks > 1) c.take<float>((size_t)p.n_chunks * N_in * N_out);
   c.take<float>((size_t)wp.C * B * N_out);
+  const int nsp = p.n_slabs * T * B;
+  c.take<int32_t>((size_t)nsp + 1);
+  c.take<int32_t>((size_t)nsp);
+  c.take<int32_t>(scan_temp_elems(nsp));
+  c.take<SlabRec>((size_t)std::max<int64_t>(out_cap, 1));
   return c.off;
 }
 
@@ -382,7 +425,7 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
                                           const float* out_g, const float* eps_out, int64_t out_cap,
                                           const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap,
                                           float* eps_in, float* dW, void* workspace, size_t workspace_bytes,
-                                          void* stream) {
+                                          void* stream, void* aux_stream) {
   if (!W || !trace_in || !out_row_ptr || !dW) return SNN_ERR_INVALID_ARG;
   if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out)) return SNN_ERR_INVALID_ARG;
   if (too_big(T, B, N_in) || too_big(T, B, N_out)) return SNN_ERR_INVALID_ARG;
@@ -391,7 +434,7 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
   const bool grad_in = in_row_ptr != nullptr;
   if (grad_in && in_cap > 0 && (!in_col_idx || !eps_in)) return SNN_ERR_INVALID_ARG;
   if (!grad_in && (in_col_idx || eps_in)) return SNN_ERR_INVALID_ARG;
-  const size_t need = snn_sparse_backward_workspace(T, B, N_in, N_out);
+  const size_t need = snn_sparse_backward_workspace(T, B, N_in, N_out, out_cap);
   if (need > 0 && (!workspace || workspace_bytes < need)) return SNN_ERR_INVALID_ARG;
   if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
 
@@ -402,6 +445,11 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
   Carve ws(workspace);
   float* part = p.n_chunks > 1 ? ws.take<float>((size_t)p.n_chunks * N_in * N_out) : dW;
   float* Lbuf = ws.take<float>((size_t)wp.C * B * N_out);
+  const int nsp = p.n_slabs * TB;
+  int32_t* sp = ws.take<int32_t>((size_t)nsp + 1);
+  int32_t* scnt = ws.take<int32_t>((size_t)nsp);
+  int32_t* stmp = ws.take<int32_t>(scan_temp_elems(nsp));
+  SlabRec* rec = ws.take<SlabRec>((size_t)std::max<int64_t>(out_cap, 1));
 
   if (out_cap == 0) {  // no active output entry: dW = 0 and eps_in = 0; no entry array is read
     hipLaunchKernelGGL(fill_zero, dim3((unsigned)std::min<size_t>(((size_t)N_in * N_out + 255) / 256, 4096)),
@@ -411,38 +459,30 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
                          eps_in, (size_t)in_cap);
     return launch_status();
   }
-  const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
-  if (out_g) {
-    (void)hipFuncSetAttribute((const void*)dw_slab_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)p.lds);
-    hipLaunchKernelGGL(dw_slab_kernel<true>, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out,
-                       out_row_ptr, out_col_idx, out_g, eps_out, out_cap, part, p.rows_per_chunk, p.n_itiles,
-                       p.n_slabs, p.slab);
-  } else {
-    (void)hipFuncSetAttribute((const void*)dw_slab_kernel<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)p.lds);
-    hipLaunchKernelGGL(dw_slab_kernel<false>, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out,
-                       out_row_ptr, out_col_idx, out_g, eps_out, out_cap, part, p.rows_per_chunk, p.n_itiles,
-                       p.n_slabs, p.slab);
+  // The spike gradient (L2-gather bound) and dW (LDS-atomic bound) use different parts of a
+  // CU; with an auxiliary stream they run side by side. aux waits for what is already on s,
+  // and s waits for aux before anything enqueued after this call.
+  hipStream_t sa = s;
+  hipEvent_t ev_in = nullptr, ev_out = nullptr;
+  const bool split = aux_stream && aux_stream != stream && grad_in && in_cap > 0;
+  if (split && hipEventCreateWithFlags(&ev_in, hipEventDisableTiming) == hipSuccess &&
+      hipEventCreateWithFlags(&ev_out, hipEventDisableTiming) == hipSuccess &&
+      hipEventRecord(ev_in, s) == hipSuccess &&
+      hipStreamWaitEvent(static_cast<hipStream_t>(aux_stream), ev_in, 0) == hipSuccess) {
+    sa = static_cast<hipStream_t>(aux_stream);
   }
-  if (p.n_chunks > 1) {
-    const size_t n = (size_t)N_in * N_out;
-    const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
-    hipLaunchKernelGGL(reduce_chunks, dim3(blocks), dim3(256), 0, s, part, p.n_chunks, n, dW);
-  }
-
   if (grad_in && in_cap > 0) {
     const int pairs = wp.C * B;
     const dim3 wgrid((pairs + kWalkWaves - 1) / kWalkWaves);
     const size_t lds = (size_t)kWalkWaves * N_out * sizeof(float);  // chunk sums only
-    hipLaunchKernelGGL(gin_chunk_sums, wgrid, dim3(kWalkThreads), lds, s, T, B, N_out, alpha, wp.P, wp.C,
+    hipLaunchKernelGGL(gin_chunk_sums, wgrid, dim3(kWalkThreads), lds, sa, T, B, N_out, alpha, wp.P, wp.C,
                        out_row_ptr, out_col_idx, out_g, eps_out, out_cap, Lbuf);
     const size_t BN = (size_t)B * N_out;
-    hipLaunchKernelGGL(gin_carries, dim3((unsigned)((BN + 255) / 256)), dim3(256), 0, s, T, B, N_out, alpha, wp.P,
+    hipLaunchKernelGGL(gin_carries, dim3((unsigned)((BN + 255) / 256)), dim3(256), 0, sa, T, B, N_out, alpha, wp.P,
                        wp.C, Lbuf);
     const int nj = (N_out + kWave - 1) / kWave;
 #define SNN_WALK(NJ_)                                                                                         \
-  launch_walk<NJ_>(wgrid, 0, s, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, \
+  launch_walk<NJ_>(wgrid, 0, sa, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, \
                    eps_out, out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)
     if (nj <= 1) SNN_WALK(1);
     else if (nj <= 2) SNN_WALK(2);
@@ -453,5 +493,32 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
     else SNN_WALK(64);
 #undef SNN_WALK
   }
+  // slab-major records of the active entries, then the slab accumulation
+  const unsigned rgrid = (unsigned)((TB + 255) / 256);
+  hipLaunchKernelGGL(slab_count, dim3(rgrid), dim3(256), 0, s, TB, p.n_slabs, p.slab, out_row_ptr, out_col_idx,
+                     out_cap, scnt);
+  launch_exclusive_scan(scnt, nsp, sp, nullptr, stmp, s);
+  if (out_g)
+    hipLaunchKernelGGL(slab_fill<true>, dim3(rgrid), dim3(256), 0, s, TB, N_out, p.slab, out_row_ptr, out_col_idx,
+                       out_g, eps_out, out_cap, sp, rec);
+  else
+    hipLaunchKernelGGL(slab_fill<false>, dim3(rgrid), dim3(256), 0, s, TB, N_out, p.slab, out_row_ptr, out_col_idx,
+                       out_g, eps_out, out_cap, sp, rec);
+  const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
+  (void)hipFuncSetAttribute((const void*)dw_slab_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+  hipLaunchKernelGGL(dw_slab_kernel, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out, sp, rec,
+                     out_cap, part, p.rows_per_chunk, p.n_itiles, p.n_slabs, p.slab);
+  if (p.n_chunks > 1) {
+    const size_t n = (size_t)N_in * N_out;
+    const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(reduce_chunks, dim3(blocks), dim3(256), 0, s, part, p.n_chunks, n, dW);
+  }
+
+  if (sa != s) {
+    if (hipEventRecord(ev_out, sa) != hipSuccess || hipStreamWaitEvent(s, ev_out, 0) != hipSuccess)
+      (void)hipStreamSynchronize(sa);  // never leave aux work unordered with later work on s
+  }
+  if (ev_in) (void)hipEventDestroy(ev_in);
+  if (ev_out) (void)hipEventDestroy(ev_out);
   return launch_status();
 }

@@ -83,20 +83,21 @@ class Network:
         caps = capacities or [None] * self.L
         return [snn.active_compact(self.V[l], self.theta, b_th, self.beta, caps[l]) for l in range(self.L)]
 
-    def sparse_backward(self, csrs: List[snn.Csr], ro=None):
+    def sparse_backward(self, csrs: List[snn.Csr], ro=None, aux_stream=None, workspaces=None):
         """Readout backward, then every LIF layer top down. Returns (dW list, dW_out, eps list)
         where eps[l] is the gradient w.r.t. layer l's spikes at its active entries."""
         if ro is None:
             ro = self.readout()
         ro_csr, ro_eps = ro[0], ro[1]
+        ws = workspaces or [None] * (self.L + 1)
         dW_out, eps = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro_csr, ro_eps,
-                                          inp=csrs[self.L - 1])
+                                          inp=csrs[self.L - 1], ws=ws[self.L], aux_stream=aux_stream)
         dWs: List[Optional[torch.Tensor]] = [None] * self.L
         epss: List[Optional[torch.Tensor]] = [None] * self.L
         for l in range(self.L - 1, -1, -1):
             epss[l] = eps
             dWs[l], eps = snn.sparse_backward(self.Ws[l], self.trace[l], self.alphas[l], csrs[l], eps,
-                                              inp=csrs[l - 1] if l > 0 else None)
+                                              inp=csrs[l - 1] if l > 0 else None, ws=ws[l], aux_stream=aux_stream)
         return dWs, dW_out, epss
 
     def dense_backward(self, b_th, ro=None):

@@ -32,9 +32,9 @@ _SIGNATURES = {
     "snn_lif_forward": (_I, [_P, _P, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P]),
     "snn_active_compact_workspace": (_SZ, [_I, _I, _I]),
     "snn_active_compact": (_I, [_P, _I, _I, _I, _F, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
-    "snn_sparse_backward_workspace": (_SZ, [_I, _I, _I, _I]),
+    "snn_sparse_backward_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_backward": (_I, [_P, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
-                                 _P]),
+                                 _P, _P]),
     "snn_dense_backward_workspace": (_SZ, [_I, _I, _I, _I]),
     "snn_dense_backward_ref": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _F, _F, _F, _F, _P, _P, _P, _SZ, _P]),
     "snn_readout_ce_workspace": (_SZ, [_I, _I, _I, _I]),
@@ -118,19 +118,20 @@ def snn_active_compact(V, T, B, N, theta, b_th, beta, row_ptr, col_idx, g_act, c
         _ptr(ws, None, "workspace"), ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def snn_sparse_backward_workspace(T, B, N_in, N_out) -> int:
-    return int(lib().snn_sparse_backward_workspace(T, B, N_in, N_out))
+def snn_sparse_backward_workspace(T, B, N_in, N_out, out_cap) -> int:
+    return int(lib().snn_sparse_backward_workspace(T, B, N_in, N_out, int(out_cap)))
 
 
 def snn_sparse_backward(W, trace_in, T, B, N_in, N_out, alpha, out_row_ptr, out_col_idx, out_g, eps_out, out_cap,
-                        in_row_ptr, in_col_idx, in_cap, eps_in, dW, ws, stream=None):
+                        in_row_ptr, in_col_idx, in_cap, eps_in, dW, ws, stream=None, aux_stream=None):
     _check("snn_sparse_backward", lib().snn_sparse_backward(
         _ptr(W, torch.float32, "W"), _ptr(trace_in, torch.float32, "trace_in"), T, B, N_in, N_out, float(alpha),
         _ptr(out_row_ptr, torch.int32, "out_row_ptr"), _ptr(out_col_idx, torch.int32, "out_col_idx"),
         _ptr(out_g, torch.float32, "out_g"), _ptr(eps_out, torch.float32, "eps_out"), int(out_cap),
         _ptr(in_row_ptr, torch.int32, "in_row_ptr"), _ptr(in_col_idx, torch.int32, "in_col_idx"), int(in_cap),
         _ptr(eps_in, torch.float32, "eps_in"), _ptr(dW, torch.float32, "dW"),
-        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream),
+        None if aux_stream is None else aux_stream.cuda_stream))
 
 
 def snn_dense_backward_workspace(T, B, N_in, N_out) -> int:
@@ -214,18 +215,19 @@ def readout_ce(V_out: torch.Tensor, labels: torch.Tensor, mode: int, dense=False
     return Csr(row_ptr, col, None, nnz_dev, nnz), eps, loss, ed
 
 
-def sparse_backward(W, trace_in, alpha, out: Csr, eps_out, inp: Optional[Csr] = None, ws=None):
-    """Allocate outputs and run snn_sparse_backward. Returns (dW, eps_in or None)."""
+def sparse_backward(W, trace_in, alpha, out: Csr, eps_out, inp: Optional[Csr] = None, ws=None, aux_stream=None):
+    """Allocate outputs and run snn_sparse_backward. Returns (dW, eps_in or None).
+    aux_stream (a torch.cuda.Stream) lets the spike-gradient part run beside dW."""
     T, B, N_in = trace_in.shape
     N_out = W.shape[1]
     dev = W.device
     dW = torch.empty((N_in, N_out), dtype=torch.float32, device=dev)
     eps_in = torch.empty(inp.capacity, dtype=torch.float32, device=dev) if inp is not None else None
     if ws is None:
-        ws = workspace(snn_sparse_backward_workspace(T, B, N_in, N_out), dev)
+        ws = workspace(snn_sparse_backward_workspace(T, B, N_in, N_out, out.capacity), dev)
     snn_sparse_backward(W, trace_in, T, B, N_in, N_out, alpha, out.row_ptr, out.col_idx, out.g, eps_out,
                         out.capacity, None if inp is None else inp.row_ptr, None if inp is None else inp.col_idx,
-                        0 if inp is None else inp.capacity, eps_in, dW, ws)
+                        0 if inp is None else inp.capacity, eps_in, dW, ws, aux_stream=aux_stream)
     return dW, eps_in
 
 

@@ -78,14 +78,18 @@ def test_compact_rejects(lib, kw):
 def test_workspace_queries(lib):
     assert lib.snn_active_compact_workspace(10, 4, 16) > 0
     assert lib.snn_active_compact_workspace(0, 4, 16) == 0
-    assert lib.snn_sparse_backward_workspace(500, 256, 1024, 1024) > 0
-    assert lib.snn_sparse_backward_workspace(10, 4, 0, 16) == 0
+    assert lib.snn_sparse_backward_workspace(500, 256, 1024, 1024, 10 ** 6) > 0
+    assert lib.snn_sparse_backward_workspace(10, 4, 0, 16, 10) == 0
+    assert lib.snn_sparse_backward_workspace(10, 4, 8, 16, -1) == 0
+    # the slab-major entry copy grows with the entry capacity
+    assert (lib.snn_sparse_backward_workspace(10, 4, 8, 16, 10 ** 5)
+            > lib.snn_sparse_backward_workspace(10, 4, 8, 16, 10))
     assert lib.snn_dense_backward_workspace(500, 256, 1024, 1024) >= 2 * 500 * 256 * 1024 * 4
     assert lib.snn_readout_ce_workspace(10, 4, 3, 0) > 0
     assert lib.snn_readout_ce_workspace(10, 4, 3, 2) == 0
     # deterministic: the same dimensions always give the same size
-    assert lib.snn_sparse_backward_workspace(100, 256, 784, 200) == lib.snn_sparse_backward_workspace(100, 256, 784,
-                                                                                                       200)
+    assert (lib.snn_sparse_backward_workspace(100, 256, 784, 200, 5000)
+            == lib.snn_sparse_backward_workspace(100, 256, 784, 200, 5000))
 
 
 def _sb(lib, **kw):
@@ -94,7 +98,7 @@ def _sb(lib, **kw):
     a.update(kw)
     return lib.snn_sparse_backward(a["W"], a["tr"], a["T"], a["B"], a["N_in"], a["N_out"], a["alpha"], a["orp"],
                                    a["oci"], a["og"], a["oeps"], a["ocap"], a["irp"], a["ici"], a["icap"],
-                                   a["eps_in"], a["dW"], a["ws"], a["ws_bytes"], None)
+                                   a["eps_in"], a["dW"], a["ws"], a["ws_bytes"], None, None)
 
 
 @pytest.mark.parametrize("kw", [dict(W=None), dict(tr=None), dict(orp=None), dict(dW=None), dict(oci=None),

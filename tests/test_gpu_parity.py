@@ -30,11 +30,11 @@ def _oracle(inp, b_th):
     return f, r, env, csrs
 
 
-def _gpu(inp, b_th, dense=True):
+def _gpu(inp, b_th, dense=True, aux=None):
     net = pipeline.from_inputs(inp).forward()
     ro = net.readout(dense=True)
     csrs = net.compact(b_th)
-    dWs, dW_out, epss = net.sparse_backward(csrs, ro)
+    dWs, dW_out, epss = net.sparse_backward(csrs, ro, aux_stream=aux)
     out = {"net": net, "ro": ro, "csrs": csrs, "dW": dWs, "dW_out": dW_out, "eps": epss}
     if dense:
         ddW, ddW_out, deps = net.dense_backward(b_th, ro)
@@ -222,3 +222,44 @@ def test_run_to_run_determinism():
         n = a["csrs"][l].nnz()
         assert torch.equal(a["csrs"][l].col_idx[:n], b["csrs"][l].col_idx[:n])
         assert torch.equal(a["eps"][l][:n], b["eps"][l][:n])  # grad_in sums in a fixed order
+
+
+@pytest.mark.parametrize("name,batch,b_th", [("latency", list(range(32)), 0.2), ("stress", list(range(8)), 0.2),
+                                             ("tiny", None, math.inf)])
+def test_aux_stream_overlap(name, batch, b_th):
+    """The spike gradient on a second stream beside dW: same results as on one stream, and
+    work enqueued afterwards on the main stream sees both."""
+    print(f"\n[case] aux stream {name} b_th={b_th}", flush=True)
+    inp = _case(name, batch)
+    aux = torch.cuda.Stream()
+    a = _gpu(inp, b_th, dense=False, aux=aux)
+    check_all(inp, b_th, a, _oracle(inp, b_th), dense=False)
+    b = _gpu(inp, b_th, dense=False)
+    for l in range(len(inp.Ws)):
+        n = a["csrs"][l].nnz()
+        assert torch.equal(a["eps"][l][:n], b["eps"][l][:n])  # fixed summation order on either stream
+
+
+@pytest.mark.parametrize("name,batch,b_th", [("latency", list(range(16)), math.inf), ("stress", [0, 1], 0.8),
+                                             ("ragged_sum", None, math.inf)])
+def test_compaction_long_rows(name, batch, b_th):
+    """Rows with more active entries than the count pass stages (every entry active, wide
+    bands), on aligned and unaligned widths: CSR bit-exact against the oracle."""
+    print(f"\n[case] long rows {name} b_th={b_th}", flush=True)
+    inp = _ragged_sum() if name == "ragged_sum" else _case(name, batch)
+    cfg = inp.cfg
+    f = oracle.network_forward(inp.X, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, np.float32(cfg.theta))
+    net = pipeline.from_inputs(inp).forward()
+    csrs = net.compact(b_th)
+    torch.cuda.synchronize()
+    longest = 0
+    for l, V in enumerate(f["V"]):
+        rp, ci, g = oracle.active_csr(V, cfg.theta, b_th, cfg.beta)
+        c = csrs[l]
+        n = c.nnz()
+        assert n == int(rp[-1])
+        assert_bits(_np(c.row_ptr).astype(np.int64), rp.astype(np.int64), f"row_ptr[{l}]")
+        assert_bits(_np(c.col_idx[:n]).astype(np.int64), ci.astype(np.int64), f"col_idx[{l}]")
+        assert_env(_np(c.g[:n]).astype(F64), g, np.abs(g), f"g[{l}]", tol=2e-6)
+        longest = max(longest, int(np.diff(rp).max()))
+    assert longest > 64  # the re-read path ran
