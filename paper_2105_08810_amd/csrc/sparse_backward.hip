@@ -1,8 +1,8 @@
 // Sparse backward of one LIF layer (Sec. 2.2): only active neurons carry gradient.
 //
 // dW (sparse form of Eq. (w_grad)): dW[:, j] += G[t,b,j] * trace[t,b,:] for every active
-//   output entry (t,b,j), G = eps * g. A block owns 64 input neurons (one per lane) times a
-//   slab of up to kSlab output neurons in LDS as float64 accumulators ([slab][65]), and a
+//   output entry (t,b,j), G = eps * g. A block owns 128 input neurons (two per lane) times a
+//   slab of up to kSlab output neurons in LDS as float64 accumulators ([slab][129]), and a
 //   chunk of rows. A wavefront streams the 256-byte trace slices of a batch of rows, finds
 //   each row's entries inside the slab with two ballots (column indices are ascending inside
 //   a row), and adds G*trace into the slab row by row; every entry is uniform across the
@@ -24,14 +24,17 @@ namespace {
 
 constexpr int kDwThreads = 1024;
 constexpr int kRowsPerBatch = 8;  // rows a wavefront has in flight
-constexpr int kSlab = 256;        // output neurons per LDS slab
-constexpr int kLd = kWave + 1;    // padded slab row: 64 inputs + 1
+constexpr int kSlab = 128;        // output neurons per LDS slab
+constexpr int kNi = 2;            // input neurons per lane: lane l holds inputs l and l + 64 of its tile
+constexpr int kItile = kNi * kWave;
+constexpr int kLd = kItile + 1;   // padded slab row: 128 inputs + 1
 constexpr int kDwWaves = kDwThreads / kWave;
 constexpr size_t kLdsBudget = 150 * 1024;
 constexpr int kWalkThreads = 256;
 constexpr int kWalkWaves = kWalkThreads / kWave;
 constexpr int kGinBatch = 4;
 constexpr int kAssumedCUs = 256;
+constexpr int kBufWord3 = 0x00020000;  // buffer descriptor word 3 on gfx9: 32-bit data format
 
 struct DwPlan {
   int n_itiles, n_slabs, slab, n_chunks, rows_per_chunk;
@@ -44,9 +47,9 @@ DwPlan plan_dw(int T, int B, int N_in, int N_out) {
   p.n_slabs = (N_out + kSlab - 1) / kSlab;
   p.slab = (N_out + p.n_slabs - 1) / p.n_slabs;
   p.lds = (size_t)p.slab * kLd * sizeof(double);
-  p.n_itiles = (N_in + kWave - 1) / kWave;
+  p.n_itiles = (N_in + kItile - 1) / kItile;
   const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(2, (160 * 1024) / p.lds));
-  const int target = kAssumedCUs * per_cu;
+  const int target = kAssumedCUs * per_cu * 2;  // two rounds: the last one evens out
   const int tiles = p.n_itiles * p.n_slabs;
   int nc = (target + tiles - 1) / tiles;
   nc = std::min(nc, std::max(1, TB / (4 * N_out)));  // partial slabs stay small next to the trace
@@ -63,7 +66,7 @@ struct WalkPlan {
 
 WalkPlan plan_walk(int T) {
   WalkPlan w{};
-  w.P = std::max(4, std::min(64, (T + 15) / 16));
+  w.P = std::max(4, std::min(64, (T + 31) / 32));
   w.C = (T + w.P - 1) / w.P;
   return w;
 }
@@ -127,8 +130,11 @@ __global__ void slab_fill(int TB, int N_out, int slab, const int32_t* __restrict
   }
 }
 
-// Block (it, sl, c): inputs [64 it, 64 it + 64), outputs of slab sl, rows of chunk c. Blocks of
-// one chunk are numbered so that they land on one XCD and share its L2 lines.
+// Block (it, sl, c): inputs [128 it, 128 it + 128), outputs of slab sl, rows of chunk c. Lane l
+// holds inputs 128 it + l and 128 it + 64 + l, so one record read, conversion and address serve
+// two float64 LDS atomics (the second at an immediate offset): on this hardware the VALU work of
+// an atomic adds to its LDS time instead of overlapping it. Blocks of one chunk are numbered so
+// that they land on one XCD and share its L2 lines.
 __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __restrict__ trace, int TB, int N_in,
                                                              int N_out, const int32_t* __restrict__ sp,
                                                              const SlabRec* __restrict__ rec, int64_t nrec,
@@ -145,9 +151,9 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int l = tid % kWave;
-  const int i = it * kWave + l;
-  const bool has_i = i < N_in;
-  const int ic = has_i ? i : N_in - 1;
+  const int i0 = it * kItile + l;
+  const int ic0 = min(i0, N_in - 1);  // lanes past N_in accumulate rows that are never written out
+  const int ic1 = min(i0 + kWave, N_in - 1);
   const int j0 = sl * slab;
   const int j1 = min(N_out, j0 + slab);
   const int32_t* spl = sp + (size_t)sl * TB;
@@ -158,52 +164,61 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
 
   const int r_lo = c * rows_per_chunk;
   const int r_hi = min(TB, r_lo + rows_per_chunk);
+  const int2* rec2 = reinterpret_cast<const int2*>(rec);
   for (int rb = r_lo + w * kRowsPerBatch; rb < r_hi; rb += kDwWaves * kRowsPerBatch) {
-    // every load of the batch is issued before any is used (indices clamped into range,
-    // results masked afterwards: a branch around a load would serialise the loads)
+    // every load of the batch is issued before any is used (indices clamped into range; rows
+    // past r_hi read sp[r_hi], so their entry ranges are empty)
     const int spv = spl[min(rb + min(l, kRowsPerBatch), r_hi)];
-    float tr[kRowsPerBatch];
+    float tr0[kRowsPerBatch], tr1[kRowsPerBatch];
 #pragma unroll
-    for (int k = 0; k < kRowsPerBatch; ++k) tr[k] = trace[(size_t)min(rb + k, r_hi - 1) * N_in + ic];
+    for (int k = 0; k < kRowsPerBatch; ++k) {
+      const size_t row = (size_t)min(rb + k, r_hi - 1) * N_in;
+      tr0[k] = trace[row + ic0];
+      tr1[k] = trace[row + ic1];
+    }
     __builtin_amdgcn_sched_barrier(0);
     const int base = rdlane(spv, 0);
     const int n = rdlane(spv, kRowsPerBatch) - base;
-    const int2* rec2 = reinterpret_cast<const int2*>(rec);
     const int2 ra = rec2[min((int64_t)base + l, nrec - 1)];  // lane s holds the batch's record s
     __builtin_amdgcn_sched_barrier(0);
     if (n <= kWave) {  // common case: the batch's records are all in one register
+      int lo = 0;
 #pragma unroll
       for (int k = 0; k < kRowsPerBatch; ++k) {
-        const double t = (rb + k < r_hi && has_i) ? (double)tr[k] : 0.0;
-        const int lo = rdlane(spv, k) - base;
+        const double t0 = (double)tr0[k], t1 = (double)tr1[k];
         const int hi = rdlane(spv, k + 1) - base;
         for (int s = lo; s < hi; ++s) {
           const int off = rdlane(ra.x, s);
-          const float G = __int_as_float(rdlane(ra.y, s));
-          atomicAdd(reinterpret_cast<double*>(accb + off), t * (double)G);
+          const double G = (double)__int_as_float(rdlane(ra.y, s));
+          double* a = reinterpret_cast<double*>(accb + off);
+          atomicAdd(a, t0 * G);
+          atomicAdd(a + kWave, t1 * G);
         }
+        lo = hi;
       }
     } else {  // dense batch: records read one by one (uniform addresses)
 #pragma unroll
       for (int k = 0; k < kRowsPerBatch; ++k) {
-        const double t = (rb + k < r_hi && has_i) ? (double)tr[k] : 0.0;
+        const double t0 = (double)tr0[k], t1 = (double)tr1[k];
         const int lo = rdlane(spv, k);
         const int hi = rdlane(spv, k + 1);
         for (int s = lo; s < hi; ++s) {
           const int2 x = rec2[s];
-          atomicAdd(reinterpret_cast<double*>(accb + x.x), t * (double)__int_as_float(x.y));
+          const double G = (double)__int_as_float(x.y);
+          double* a = reinterpret_cast<double*>(accb + x.x);
+          atomicAdd(a, t0 * G);
+          atomicAdd(a + kWave, t1 * G);
         }
       }
     }
   }
   __syncthreads();
-
   float* dst = out + (size_t)c * N_in * N_out;
   const int width = j1 - j0;
-  for (int k = tid; k < kWave * width; k += kDwThreads) {
+  for (int k = tid; k < kItile * width; k += kDwThreads) {
     const int ii = k / width;
     const int jj = k - ii * width;
-    if (it * kWave + ii < N_in) dst[(size_t)(it * kWave + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
+    if (it * kItile + ii < N_in) dst[(size_t)(it * kItile + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
   }
 }
 
@@ -275,6 +290,16 @@ __global__ void gin_carries(int T, int B, int N_out, float alpha, int P, int C, 
   }
 }
 
+// Buffer descriptor of one row of n floats (raw buffer, range-checked: reads past the row give 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const float* row, int n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(row), (short)0, n * (int)sizeof(float), kBufWord3);
+}
+
+// One float through a buffer descriptor (the builtin returns the raw 32 bits).
+__device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t rs, int byte_off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, byte_off, 0, 0));
+}
+
 // Sum over the wavefront of four values at once (one per entry u): two exchanges across
 // halves and across rows leave each 16-lane row holding entry u = row index summed over 4
 // lanes; four DPP steps then finish the sum inside the row. Returns the total of entry
@@ -296,12 +321,13 @@ __device__ __forceinline__ float wave_sum4(float a0, float a1, float a2, float a
 }
 
 // One wavefront per (chunk c, sample b). delta[b, 0:N_out] lives in registers: lane l holds
-// j = l + 64 m. The row pointers of all steps of the chunk are loaded once; at each step the
-// input-active entries are taken four at a time (4 * NJ W loads in flight) and reduced
-// together; then delta <- alpha delta + G[t], each active output added by the lane that owns
-// its column (a uniform register index).
+// j = l + 64 m. The row pointers of all steps of the chunk are loaded once, and each step's
+// entry indices (input and output side, one entry per lane) are requested one step ahead, so
+// that a step waits only for its W rows. The input-active entries are taken four at a time
+// (4 * NJ W loads in flight) and reduced together; then delta <- alpha delta + G[t], each
+// active output added by the lane that owns its column (a uniform register index).
 template <int NJ>
-__global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict__ W, int T, int B, int N_in,
+__global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk(const float* __restrict__ W, int T, int B, int N_in,
                                                          int N_out, float alpha, int P, int C,
                                                          const int32_t* __restrict__ orp,
                                                          const int32_t* __restrict__ oci,
@@ -332,8 +358,27 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
     oa = clamp_entry(orp[r], ocap);
     ob = clamp_entry(orp[r + 1], ocap);
   }
-  for (int t = t_hi - 1; t >= t_lo; --t) {
-    const int k = t - t_lo;
+  // entry l of step k's row (clamped into the row; only lanes below the row length are used)
+  auto in_idx = [&](int k) {
+    const int a = rdlane(ia, k), z = rdlane(ib, k);
+    return z > a ? ici[min(a + l, z - 1)] : -1;
+  };
+  auto out_col = [&](int k) {
+    const int a = rdlane(oa, k), z = rdlane(ob, k);
+    return z > a ? oci[min(a + l, z - 1)] : -1;
+  };
+  auto out_g = [&](int k) {
+    const int a = rdlane(oa, k), z = rdlane(ob, k);
+    const int e = min(a + l, max(z - 1, 0));
+    return z > a ? oeps[e] * (og ? og[e] : 1.0f) : 0.0f;
+  };
+  int k = t_hi - 1 - t_lo;
+  int vi = in_idx(k), vj = out_col(k);
+  float vg = out_g(k);
+  for (; k >= 0; --k) {
+    const int kn = max(k - 1, 0);
+    const int vi_n = in_idx(kn), vj_n = out_col(kn);
+    const float vg_n = out_g(kn);
     // eps_in at the input-active entries of row (t, b), with delta[t] = d
     const int i0 = rdlane(ia, k);
     const int i1 = rdlane(ib, k);
@@ -341,15 +386,18 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
       int iv[kGinBatch];
 #pragma unroll
       for (int u = 0; u < kGinBatch; ++u) {
-        const int x = ici[min(e + u, i1 - 1)];
-        iv[u] = (e + u < i1 && (unsigned)x < (unsigned)N_in) ? x : -1;
+        const int eu = e + u;
+        const int x = eu - i0 < kWave ? rdlane(vi, min(eu - i0, kWave - 1)) : ici[min(eu, i1 - 1)];
+        iv[u] = (eu < i1 && (unsigned)x < (unsigned)N_in) ? x : -1;
       }
+      // W row gathers through a buffer descriptor per row (base in scalar registers, column
+      // offsets as immediates, columns past N_out read as 0 by the range check)
       float wv[kGinBatch][NJ];
 #pragma unroll
       for (int u = 0; u < kGinBatch; ++u) {
-        const float* wr = W + (size_t)(iv[u] >= 0 ? iv[u] : 0) * N_out;
+        const __amdgpu_buffer_rsrc_t rs = row_rsrc(W + (size_t)(iv[u] >= 0 ? iv[u] : 0) * N_out, N_out);
 #pragma unroll
-        for (int m = 0; m < NJ; ++m) wv[u][m] = wr[min(l + kWave * m, N_out - 1)];
+        for (int m = 0; m < NJ; ++m) wv[u][m] = load_f32(rs, (l + kWave * m) * 4);
       }
       __builtin_amdgcn_sched_barrier(0);
       float acc[kGinBatch];
@@ -357,8 +405,7 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
       for (int u = 0; u < kGinBatch; ++u) {
         acc[u] = 0.0f;
 #pragma unroll
-        for (int m = 0; m < NJ; ++m)
-          if (l + kWave * m < N_out) acc[u] += wv[u][m] * d[m];
+        for (int m = 0; m < NJ; ++m) acc[u] += wv[u][m] * d[m];  // d = 0 past N_out
         acc[u] = iv[u] >= 0 ? acc[u] : 0.0f;
       }
       const float tot = wave_sum4(acc[0], acc[1], acc[2], acc[3]);
@@ -371,12 +418,13 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
     const int o0 = rdlane(oa, k);
     const int o1 = rdlane(ob, k);
     for (int e = o0; e < o1; e += kWave) {
-      const int ec = min(e + l, o1 - 1);
-      const int jj = oci[ec];
-      const float ee = oeps[ec];
-      const float gg = og ? og[ec] : 1.0f;
-      const int jv = (e + l < o1) ? jj : -1;
-      const float gv = ee * gg;
+      int jv = vj;
+      float gv = vg;
+      if (e > o0) {  // rows with more than 64 active outputs: the rest is read here
+        const int ec = min(e + l, o1 - 1);
+        jv = oci[ec];
+        gv = oeps[ec] * (og ? og[ec] : 1.0f);
+      }
       const int ns = min(kWave, o1 - e);
       for (int s = 0; s < ns; ++s) {
         const int j = rdlane(jv, s);
@@ -387,6 +435,9 @@ __global__ __launch_bounds__(kWalkThreads) void gin_walk(const float* __restrict
         }
       }
     }
+    vi = vi_n;
+    vj = vj_n;
+    vg = vg_n;
   }
 }
 
