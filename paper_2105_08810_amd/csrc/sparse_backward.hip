@@ -90,43 +90,98 @@ struct SlabRec {
   float G;
 };
 
-__global__ void slab_count(int TB, int n_slabs, int slab, const int32_t* __restrict__ row_ptr,
-                           const int32_t* __restrict__ col_idx, int64_t cap, int32_t* __restrict__ cnt) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= TB) return;
-  const int e0 = clamp_entry(row_ptr[r], cap);
-  const int e1 = clamp_entry(row_ptr[r + 1], cap);
-  int e = e0;
-  for (int sl = 0; sl < n_slabs; ++sl) {  // columns ascend: each slab's run follows the previous one
-    const int end = (sl + 1) * slab;
-    const int start = e;
-    while (e < e1 && col_idx[e] < end) ++e;
-    cnt[(size_t)sl * TB + r] = e - start;
+// A wavefront takes R consecutive rows (R * n_slabs <= 64): their entries are contiguous in the
+// CSR, and lane k of each 64-entry piece finds its entry's row from the batch's row pointers.
+// An entry's key is (row in batch, slab); with ascending columns the entries of one key are a
+// run of lanes, and a run's head is found with one ballot. Per-key totals live in a 64-int LDS
+// array of the wavefront (runs may continue into the next piece). Entries whose column is
+// outside [0, N_out) are neither counted nor placed.
+constexpr int kRowWaves = 4;
+
+struct EntryKey {
+  int key;    // row-in-batch * n_slabs + slab, or -1
+  int j;      // column
+  int h;      // lane of the run's first entry in this piece
+  bool tail;  // last lane of the run in this piece
+};
+
+__device__ __forceinline__ EntryKey entry_key(int ee, int E1, int rp, int nr, int N_out, int n_slabs, int slab,
+                                              const int32_t* __restrict__ col_idx) {
+  const int l = lane_id();
+  EntryKey x{-1, -1, 0, false};
+  if (ee < E1) {
+    x.j = col_idx[ee];
+    if ((unsigned)x.j < (unsigned)N_out) {
+      int k = 0;
+      for (int m = 1; m < nr; ++m) k += ee >= rdlane(rp, m);
+      x.key = k * n_slabs + x.j / slab;
+    }
   }
+  const int prev = __shfl_up(x.key, 1, kWave);
+  const int next = __shfl_down(x.key, 1, kWave);
+  const bool head = x.key >= 0 && (l == 0 || prev != x.key);
+  x.tail = x.key >= 0 && (l == kWave - 1 || next != x.key);
+  const uint64_t le = __ballot(head) & ((2ull << l) - 1ull);  // heads at or below this lane
+  x.h = le ? 63 - __clzll(le) : 0;
+  return x;
+}
+
+__global__ __launch_bounds__(kRowWaves * kWave) void slab_count(int TB, int N_out, int n_slabs, int slab, int R,
+                                                                const int32_t* __restrict__ row_ptr,
+                                                                const int32_t* __restrict__ col_idx, int64_t cap,
+                                                                int32_t* __restrict__ cnt) {
+  __shared__ int tot[kRowWaves][kWave];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  const int r0 = (blockIdx.x * kRowWaves + w) * R;
+  if (r0 >= TB) return;
+  const int nr = min(R, TB - r0);
+  int* tw = tot[w];
+  tw[l] = 0;
+  const int rp = l <= nr ? clamp_entry(row_ptr[r0 + l], cap) : 0;
+  const int E0 = rdlane(rp, 0);
+  const int E1 = rdlane(rp, nr);
+  for (int e = E0; e < E1; e += kWave) {
+    const EntryKey x = entry_key(e + l, E1, rp, nr, N_out, n_slabs, slab, col_idx);
+    if (x.tail) tw[x.key] += l - x.h + 1;
+  }
+  if (l < nr * n_slabs) cnt[(size_t)(l % n_slabs) * TB + r0 + l / n_slabs] = tw[l];
 }
 
 template <bool HAS_G>
-__global__ void slab_fill(int TB, int N_out, int slab, const int32_t* __restrict__ row_ptr,
-                          const int32_t* __restrict__ col_idx, const float* __restrict__ g,
-                          const float* __restrict__ eps, int64_t cap, const int32_t* __restrict__ sp,
-                          SlabRec* __restrict__ rec) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= TB) return;
-  const int e0 = clamp_entry(row_ptr[r], cap);
-  const int e1 = clamp_entry(row_ptr[r + 1], cap);
-  int cur = -1, pos = 0;
-  for (int e = e0; e < e1; ++e) {
-    const int j = col_idx[e];
-    if ((unsigned)j >= (unsigned)N_out) continue;
-    const int sl = j / slab;
-    if (sl != cur) {
-      cur = sl;
-      pos = sp[(size_t)sl * TB + r];
+__global__ __launch_bounds__(kRowWaves * kWave) void slab_fill(int TB, int N_out, int n_slabs, int slab, int R,
+                                                               const int32_t* __restrict__ row_ptr,
+                                                               const int32_t* __restrict__ col_idx,
+                                                               const float* __restrict__ g,
+                                                               const float* __restrict__ eps, int64_t cap,
+                                                               const int32_t* __restrict__ sp, int64_t nrec,
+                                                               SlabRec* __restrict__ rec) {
+  __shared__ int done[kRowWaves][kWave];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  const int r0 = (blockIdx.x * kRowWaves + w) * R;
+  if (r0 >= TB) return;
+  const int nr = min(R, TB - r0);
+  int* dw = done[w];
+  dw[l] = 0;
+  const int rp = l <= nr ? clamp_entry(row_ptr[r0 + l], cap) : 0;
+  const int E0 = rdlane(rp, 0);
+  const int E1 = rdlane(rp, nr);
+  // lane p: first slot of key p (row r0 + p / n_slabs in slab p % n_slabs)
+  const int first = l < nr * n_slabs ? sp[(size_t)(l % n_slabs) * TB + r0 + l / n_slabs] : 0;
+  for (int e = E0; e < E1; e += kWave) {
+    const int ee = e + l;
+    const EntryKey x = entry_key(ee, E1, rp, nr, N_out, n_slabs, slab, col_idx);
+    const int kq = x.key >= 0 ? x.key : 0;
+    const int pos = __shfl(first, kq, kWave) + dw[kq] + (l - x.h);
+    if (x.key >= 0 && pos < nrec) {
+      const int sl = kq % n_slabs;
+      SlabRec r;
+      r.off = (x.j - sl * slab) * kLd * (int)sizeof(double);
+      r.G = eps[ee] * (HAS_G ? g[ee] : 1.0f);
+      rec[pos] = r;
     }
-    SlabRec x;
-    x.off = (j - sl * slab) * kLd * (int)sizeof(double);
-    x.G = eps[e] * (HAS_G ? g[e] : 1.0f);
-    rec[pos++] = x;
+    if (x.tail) dw[x.key] += l - x.h + 1;
   }
 }
 
@@ -158,6 +213,7 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   const int j1 = min(N_out, j0 + slab);
   const int32_t* spl = sp + (size_t)sl * TB;
   char* accb = reinterpret_cast<char*>(acc) + l * (int)sizeof(double);
+  const int max_off = (slab - 1) * kLd * (int)sizeof(double);
 
   for (int k = tid; k < slab * kLd; k += kDwThreads) acc[k] = 0.0;
   __syncthreads();
@@ -188,7 +244,7 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
         const double t0 = (double)tr0[k], t1 = (double)tr1[k];
         const int hi = rdlane(spv, k + 1) - base;
         for (int s = lo; s < hi; ++s) {
-          const int off = rdlane(ra.x, s);
+          const int off = (int)min((unsigned)rdlane(ra.x, s), (unsigned)max_off);  // scalar clamp into the slab
           const double G = (double)__int_as_float(rdlane(ra.y, s));
           double* a = reinterpret_cast<double*>(accb + off);
           atomicAdd(a, t0 * G);
@@ -205,7 +261,7 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
         for (int s = lo; s < hi; ++s) {
           const int2 x = rec2[s];
           const double G = (double)__int_as_float(x.y);
-          double* a = reinterpret_cast<double*>(accb + x.x);
+          double* a = reinterpret_cast<double*>(accb + min(max(x.x, 0), max_off));
           atomicAdd(a, t0 * G);
           atomicAdd(a + kWave, t1 * G);
         }
@@ -338,8 +394,9 @@ __global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk(const
                                                          const float* __restrict__ D, float* __restrict__ eps_in) {
   const int w = threadIdx.x / kWave;
   const int l = lane_id();
-  const int q = blockIdx.x * kWalkWaves + w;
-  if (q >= C * B) return;
+  // grid-stride over (c, b): a grid smaller than C*B/4 blocks leaves room on every CU for
+  // other work (the dW kernel on another stream)
+  for (int q = blockIdx.x * kWalkWaves + w; q < C * B; q += gridDim.x * kWalkWaves) {
   const int c = q / B;
   const int b = q - c * B;
   float d[NJ];
@@ -439,6 +496,7 @@ __global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk(const
     vj = vj_n;
     vg = vg_n;
   }
+  }
 }
 
 template <int NJ>
@@ -532,8 +590,12 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
     hipLaunchKernelGGL(gin_carries, dim3((unsigned)((BN + 255) / 256)), dim3(256), 0, sa, T, B, N_out, alpha, wp.P,
                        wp.C, Lbuf);
     const int nj = (N_out + kWave - 1) / kWave;
+    // beside a dW that takes longer than the walk, the walk keeps to two blocks per CU so that a
+    // dW block fits next to it (per product, a dW entry costs about 1.5 times a walk entry)
+    const bool dw_longer = 3.0 * (double)out_cap * N_in >= 2.0 * (double)in_cap * N_out;
+    const dim3 walk_grid(sa != s && dw_longer ? std::min<unsigned>(wgrid.x, 2 * kAssumedCUs) : wgrid.x);
 #define SNN_WALK(NJ_)                                                                                         \
-  launch_walk<NJ_>(wgrid, 0, sa, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, \
+  launch_walk<NJ_>(walk_grid, 0, sa, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, \
                    eps_out, out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)
     if (nj <= 1) SNN_WALK(1);
     else if (nj <= 2) SNN_WALK(2);
@@ -545,16 +607,20 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
 #undef SNN_WALK
   }
   // slab-major records of the active entries, then the slab accumulation
-  const unsigned rgrid = (unsigned)((TB + 255) / 256);
-  hipLaunchKernelGGL(slab_count, dim3(rgrid), dim3(256), 0, s, TB, p.n_slabs, p.slab, out_row_ptr, out_col_idx,
+  const int R = std::max(1, std::min(8, kWave / p.n_slabs));  // rows per wavefront
+  const int nwaves = (TB + R - 1) / R;
+  const dim3 rgrid((unsigned)((nwaves + kRowWaves - 1) / kRowWaves));
+  const dim3 rblock(kRowWaves * kWave);
+  const int64_t nrec = std::max<int64_t>(out_cap, 1);
+  hipLaunchKernelGGL(slab_count, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr, out_col_idx,
                      out_cap, scnt);
   launch_exclusive_scan(scnt, nsp, sp, nullptr, stmp, s);
   if (out_g)
-    hipLaunchKernelGGL(slab_fill<true>, dim3(rgrid), dim3(256), 0, s, TB, N_out, p.slab, out_row_ptr, out_col_idx,
-                       out_g, eps_out, out_cap, sp, rec);
+    hipLaunchKernelGGL(slab_fill<true>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
+                       out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
   else
-    hipLaunchKernelGGL(slab_fill<false>, dim3(rgrid), dim3(256), 0, s, TB, N_out, p.slab, out_row_ptr, out_col_idx,
-                       out_g, eps_out, out_cap, sp, rec);
+    hipLaunchKernelGGL(slab_fill<false>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
+                       out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
   const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
   (void)hipFuncSetAttribute((const void*)dw_slab_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
   hipLaunchKernelGGL(dw_slab_kernel, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out, sp, rec,
