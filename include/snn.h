@@ -65,7 +65,9 @@ const char* snn_status_string(int status);
  * Arithmetic is float32 with every operation rounded separately (no fused multiply-add) and
  * the weighted input of a row summed over its spiking inputs in ascending input index starting
  * from +0.0, so V and s_out are a deterministic function of the inputs.
- * s_in[T-1] does not enter V. Supported: N_in <= 4096.
+ * s_in[T-1] does not enter V. V doubles as scratch during the call (the weighted inputs are
+ * parked in it before the recurrence overwrites them). Supported: N_out <= 4096; larger N_out
+ * returns SNN_ERR_UNSUPPORTED.
  */
 snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
                            float alpha, float theta, float* V, uint8_t* s_out, float* trace_in,

@@ -2,15 +2,15 @@
 // V[0] = 0, the strict Heaviside of Eq. (spike_fn), and the input trace that Eq. (w_grad)
 // reuses (the filtered input of Eq. (lif_unrolled)).
 //
-// One block owns one batch sample b and up to 256 output neurons j (one per thread); the
-// j-blocks of a sample are placed on the same XCD so they share its L2 for the spike rows.
-// Time is walked in chunks of P steps:
-//   1. each wavefront turns some of the chunk's spike rows S_in[t,b,:] into an ascending list
-//      of spiking inputs in LDS (wave ballot per byte lane + mbcnt prefix);
-//   2. every thread sums W[i,j] over each list in ascending i for all P rows at once (the P
-//      independent gathers keep many W loads in flight; W rows are served by L2);
-//   3. the membrane recurrence runs P steps in registers and writes V and S_out;
-//   4. the block updates its share of the input trace and writes it.
+// Two kernels, so that no block walks the whole time axis with gathers on its critical path:
+//   lif_gather  one wavefront per row (t, b), t < T-1: the ascending list of spiking inputs of
+//               S_in[t,b,:] (ballots over 1024-input segments, list in LDS), then
+//               I[t,b,:] = sum over that list of W[i,:], summed in ascending i. The row-parallel
+//               sums have no dependence on time, so every row's W gathers can be in flight at
+//               once. I[t,b,:] is parked in the slot of V[t+1,b,:].
+//   lif_scan    one thread per (b, j): the membrane recurrence over t, reading I from V[t+1]
+//               and overwriting it with V[t+1]; S_out[t] = V[t] > theta. And one thread per
+//               (b, four inputs): the input trace over t. Loads run 16 steps ahead.
 // Float32 with separately rounded operations (__fmul_rn / __fadd_rn) and the ascending
 // summation order make V a deterministic function of the inputs.
 #include "common.h"
@@ -18,11 +18,11 @@
 namespace snn {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kJT = 256;         // output neurons per block
-constexpr int kPMax = 16;        // time steps per chunk
-constexpr int kTraceGroups = 4;  // float4 trace groups per thread -> 4096 inputs per block
-constexpr int kListBytes = 32768;
+constexpr int kGatherWaves = 4;        // wavefronts (rows) per gather block
+constexpr int kPiece = 4 * kWave;      // inputs per ballot piece (4 bytes per lane)
+constexpr int kSegPieces = 4;          // pieces whose spike bytes are loaded together
+constexpr int kScanThreads = 256;
+constexpr int kScanAhead = 16;         // time steps loaded ahead in the scans
 
 template <bool ALIGNED>
 __device__ __forceinline__ uint32_t load4(const uint8_t* p, int i, int n) {
@@ -34,128 +34,178 @@ __device__ __forceinline__ uint32_t load4(const uint8_t* p, int i, int n) {
   return x;
 }
 
-template <bool ALIGNED>
-__global__ __launch_bounds__(kThreads) void lif_forward_kernel(const uint8_t* __restrict__ s_in,
-                                                               const float* __restrict__ W, int T, int B, int N_in,
-                                                               int N_out, float alpha, float theta,
-                                                               float* __restrict__ V, uint8_t* __restrict__ s_out,
-                                                               float* __restrict__ trace, int P, int n_jblk,
-                                                               int tr_span) {
-  extern __shared__ uint16_t lists[];  // [P][N_in]
-  __shared__ int counts[kPMax];
+// NQ float4 column groups per lane: lane l holds columns 4 (l + 64 m) .. +3, m < NQ.
+// The row's spike bytes are read kSegPieces pieces at a time (all loads issued first), their
+// spiking inputs listed in LDS in ascending order, and the list's W rows summed in batches.
+template <bool ALIGNED, bool VEC, int NQ>
+__global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t* __restrict__ s_in,
+                                                                   const float* __restrict__ W, int T, int B,
+                                                                   int N_in, int N_out, float* __restrict__ V) {
+  constexpr int kBatch = NQ >= 16 ? 1 : (NQ >= 8 ? 2 : 4);  // W rows in flight: kBatch * NQ float4 loads
+  __shared__ uint16_t seg_list[kGatherWaves][kSegPieces * kPiece];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  const long r = (long)blockIdx.x * kGatherWaves + w;  // row r = t * B + b, t < T - 1
+  if (r >= (long)(T - 1) * B) return;
+  const uint8_t* row = s_in + (size_t)r * N_in;
+  uint16_t* lst = seg_list[w];
+  float acc[NQ][4];
+#pragma unroll
+  for (int m = 0; m < NQ; ++m)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[m][q] = 0.0f;
 
-  int id = blockIdx.x;
-  const int G = gridDim.x;
-  if ((G & 7) == 0) id = (id & 7) * (G >> 3) + (id >> 3);  // consecutive ids share an XCD
-  const int b = id / n_jblk;
-  const int jb = id - b * n_jblk;
-  const int tid = threadIdx.x;
-  const int w = tid / kWave;
-  const int l = tid % kWave;
-  const int j = jb * kJT + tid;
-  const bool has_j = j < N_out;
-
-  const size_t step_in = (size_t)B * N_in;
-  const size_t step_out = (size_t)B * N_out;
-  const int tr_lo = jb * tr_span;
-  const int tr_hi = min(N_in, tr_lo + tr_span);
-  float tr[kTraceGroups][4];
+  for (int s0 = 0; s0 < N_in; s0 += kSegPieces * kPiece) {
+    uint32_t x[kSegPieces];
 #pragma unroll
-  for (int k = 0; k < kTraceGroups; ++k)
+    for (int c = 0; c < kSegPieces; ++c) x[c] = load4<ALIGNED>(row, s0 + c * kPiece + 4 * l, N_in);
+    // ascending list of the segment's spiking inputs (offsets inside the segment)
+    int base = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) tr[k][q] = 0.0f;
-
-  float v = 0.0f;
-  if (has_j) V[(size_t)b * N_out + j] = 0.0f;
-  if (trace) {
-#pragma unroll
-    for (int k = 0; k < kTraceGroups; ++k) {
-      const int i = tr_lo + 4 * (tid + kThreads * k);
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (i + q < tr_hi) trace[(size_t)b * N_in + i + q] = 0.0f;
+    for (int c = 0; c < kSegPieces; ++c) {
+      const bool a0 = (x[c] & 0xffu) != 0, a1 = (x[c] & 0xff00u) != 0, a2 = (x[c] & 0xff0000u) != 0,
+                 a3 = (x[c] & 0xff000000u) != 0;
+      const uint64_t m0 = __ballot(a0), m1 = __ballot(a1), m2 = __ballot(a2), m3 = __ballot(a3);
+      int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+      const int o = c * kPiece + 4 * l;
+      if (a0) lst[pos++] = (uint16_t)o;
+      if (a1) lst[pos++] = (uint16_t)(o + 1);
+      if (a2) lst[pos++] = (uint16_t)(o + 2);
+      if (a3) lst[pos++] = (uint16_t)(o + 3);
+      base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
     }
-  }
-
-  for (int t0 = 0; t0 < T - 1; t0 += P) {
-    const int np = min(P, T - 1 - t0);
-    // 1. ascending lists of spiking inputs, one row per wavefront at a time
-    for (int p = w; p < np; p += kThreads / kWave) {
-      const uint8_t* row = s_in + (size_t)(t0 + p) * step_in + (size_t)b * N_in;
-      uint16_t* lst = lists + p * N_in;
-      int base = 0;
-      for (int i0 = 0; i0 < N_in; i0 += 4 * kWave) {
-        const int i = i0 + 4 * l;
-        const uint32_t x = load4<ALIGNED>(row, i, N_in);
-        const bool a0 = (x & 0xffu) != 0, a1 = (x & 0xff00u) != 0, a2 = (x & 0xff0000u) != 0,
-                   a3 = (x & 0xff000000u) != 0;
-        const uint64_t m0 = __ballot(a0), m1 = __ballot(a1), m2 = __ballot(a2), m3 = __ballot(a3);
-        int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
-        if (a0) lst[pos++] = (uint16_t)i;
-        if (a1) lst[pos++] = (uint16_t)(i + 1);
-        if (a2) lst[pos++] = (uint16_t)(i + 2);
-        if (a3) lst[pos++] = (uint16_t)(i + 3);
-        base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
-      }
-      if (l == 0) counts[p] = base;
-    }
-    __syncthreads();
-
-    // 2-3. weighted inputs of the chunk, then the membrane recurrence
-    if (has_j) {
-      float acc[kPMax];
-      int cnt[kPMax];
-      int kmax = 0;
+    const int n = base;
+    __builtin_amdgcn_wave_barrier();
+    // sums in ascending i, kBatch W rows in flight; positions past the list are clamped to its
+    // last entry and their sums skipped by a select
+    for (int k = 0; k < n; k += kBatch) {
+      float4 wv[kBatch][NQ];
 #pragma unroll
-      for (int p = 0; p < kPMax; ++p) {
-        acc[p] = 0.0f;
-        cnt[p] = p < np ? counts[p] : 0;
-        kmax = max(kmax, cnt[p]);
-      }
-      const float* Wj = W + j;
-      for (int k = 0; k < kmax; ++k) {
+      for (int u = 0; u < kBatch; ++u) {
+        const int ii = s0 + (int)lst[min(k + u, n - 1)];
+        const float* wr = W + (size_t)ii * N_out;
 #pragma unroll
-        for (int p = 0; p < kPMax; ++p)
-          if (k < cnt[p]) acc[p] = __fadd_rn(acc[p], Wj[(size_t)lists[p * N_in + k] * N_out]);
+        for (int m = 0; m < NQ; ++m) {
+          const int j = 4 * (l + kWave * m);
+          if (VEC) {
+            wv[u][m] = j < N_out ? *reinterpret_cast<const float4*>(wr + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+          } else {
+            wv[u][m].x = j < N_out ? wr[j] : 0.0f;
+            wv[u][m].y = j + 1 < N_out ? wr[j + 1] : 0.0f;
+            wv[u][m].z = j + 2 < N_out ? wr[j + 2] : 0.0f;
+            wv[u][m].w = j + 3 < N_out ? wr[j + 3] : 0.0f;
+          }
+        }
       }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int p = 0; p < kPMax; ++p) {
-        if (p < np) {
-          const int t = t0 + p;
-          const bool s = v > theta;
-          s_out[(size_t)t * step_out + (size_t)b * N_out + j] = (uint8_t)s;
-          v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), acc[p]), s ? -1.0f : -0.0f);
-          V[(size_t)(t + 1) * step_out + (size_t)b * N_out + j] = v;
+      for (int u = 0; u < kBatch; ++u) {
+        const bool take = k + u < n;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m) {
+          acc[m][0] = take ? __fadd_rn(acc[m][0], wv[u][m].x) : acc[m][0];
+          acc[m][1] = take ? __fadd_rn(acc[m][1], wv[u][m].y) : acc[m][1];
+          acc[m][2] = take ? __fadd_rn(acc[m][2], wv[u][m].z) : acc[m][2];
+          acc[m][3] = take ? __fadd_rn(acc[m][3], wv[u][m].w) : acc[m][3];
         }
       }
     }
-
-    // 4. input trace of this block's share of the inputs
-    if (trace) {
+    __builtin_amdgcn_wave_barrier();  // the list is rewritten by the next segment
+  }
+  float* dst = V + (size_t)(r + B) * N_out;  // slot of V[t+1, b, :]
 #pragma unroll
-      for (int k = 0; k < kTraceGroups; ++k) {
-        const int i = tr_lo + 4 * (tid + kThreads * k);
-        if (i < tr_hi) {
-          for (int p = 0; p < np; ++p) {
-            const uint32_t x = load4<ALIGNED>(s_in + (size_t)(t0 + p) * step_in + (size_t)b * N_in, i, N_in);
+  for (int m = 0; m < NQ; ++m) {
+    const int j = 4 * (l + kWave * m);
+    if (VEC) {
+      if (j < N_out) *reinterpret_cast<float4*>(dst + j) = make_float4(acc[m][0], acc[m][1], acc[m][2], acc[m][3]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (j + q < N_out) dst[j + q] = acc[m][q];
+    }
+  }
+}
+
+// Blocks [0, nv) run the membrane recurrence of B * N_out neurons; blocks [nv, nv + nt) run the
+// trace of B * ceil(N_in / 4) input quads.
+template <bool ALIGNED>
+__global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restrict__ s_in, int T, int B, int N_in,
+                                                         int N_out, float alpha, float theta, float* __restrict__ V,
+                                                         uint8_t* __restrict__ s_out, float* __restrict__ trace,
+                                                         int nv) {
+  if ((int)blockIdx.x < nv) {
+    const size_t k = (size_t)blockIdx.x * kScanThreads + threadIdx.x;  // b * N_out + j
+    if (k >= (size_t)B * N_out) return;
+    const size_t step = (size_t)B * N_out;
+    float v = 0.0f;
+    V[k] = 0.0f;
+    for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
+      const int np = min(kScanAhead, T - 1 - t0);
+      float in[kScanAhead];
+#pragma unroll
+      for (int p = 0; p < kScanAhead; ++p) in[p] = V[(size_t)(t0 + min(p, np - 1) + 1) * step + k];
+#pragma unroll
+      for (int p = 0; p < kScanAhead; ++p) {
+        if (p < np) {
+          const int t = t0 + p;
+          const bool sp = v > theta;
+          s_out[(size_t)t * step + k] = (uint8_t)sp;
+          v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), in[p]), sp ? -1.0f : -0.0f);
+          V[(size_t)(t + 1) * step + k] = v;
+        }
+      }
+    }
+    s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
+  } else {
+    const int nq = (N_in + 3) / 4;
+    const size_t k = (size_t)(blockIdx.x - nv) * kScanThreads + threadIdx.x;  // b * nq + quad
+    if (k >= (size_t)B * nq) return;
+    const int b = (int)(k / nq);
+    const int i = 4 * (int)(k - (size_t)b * nq);
+    const size_t step = (size_t)B * N_in;
+    float* dst0 = trace + (size_t)b * N_in + i;
+    float tr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (i + q < N_in) dst0[q] = 0.0f;
+    const uint8_t* src0 = s_in + (size_t)b * N_in;
+    for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
+      const int np = min(kScanAhead, T - 1 - t0);
+      uint32_t x[kScanAhead];
+#pragma unroll
+      for (int p = 0; p < kScanAhead; ++p) x[p] = load4<ALIGNED>(src0 + (size_t)(t0 + min(p, np - 1)) * step, i, N_in);
+#pragma unroll
+      for (int p = 0; p < kScanAhead; ++p) {
+        if (p < np) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            tr[q] = __fadd_rn(__fmul_rn(alpha, tr[q]), ((x[p] >> (8 * q)) & 0xffu) ? 1.0f : 0.0f);
+          float* dst = dst0 + (size_t)(t0 + p + 1) * step;
+          if (ALIGNED) {
+            *reinterpret_cast<float4*>(dst) = make_float4(tr[0], tr[1], tr[2], tr[3]);
+          } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-              tr[k][q] = __fadd_rn(__fmul_rn(alpha, tr[k][q]), ((x >> (8 * q)) & 0xffu) ? 1.0f : 0.0f);
-            float* dst = trace + (size_t)(t0 + p + 1) * step_in + (size_t)b * N_in + i;
-            if (ALIGNED && i + 3 < tr_hi) {
-              *reinterpret_cast<float4*>(dst) = make_float4(tr[k][0], tr[k][1], tr[k][2], tr[k][3]);
-            } else {
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                if (i + q < tr_hi) dst[q] = tr[k][q];
-            }
+              if (i + q < N_in) dst[q] = tr[q];
           }
         }
       }
     }
-    __syncthreads();
   }
-  if (has_j) s_out[(size_t)(T - 1) * step_out + (size_t)b * N_out + j] = (uint8_t)(v > theta);
+}
+
+template <bool ALIGNED, bool VEC>
+void launch_gather(int NQ, dim3 grid, hipStream_t s, const uint8_t* s_in, const float* W, int T, int B, int N_in,
+                   int N_out, float* V) {
+#define SNN_G(Q)                                                                                              \
+  hipLaunchKernelGGL((lif_gather<ALIGNED, VEC, Q>), grid, dim3(kGatherWaves * kWave), 0, s, s_in, W, T, B, N_in, \
+                     N_out, V)
+  if (NQ <= 1) SNN_G(1);
+  else if (NQ <= 2) SNN_G(2);
+  else if (NQ <= 4) SNN_G(4);
+  else if (NQ <= 8) SNN_G(8);
+  else SNN_G(16);
+#undef SNN_G
 }
 
 }  // namespace
@@ -170,22 +220,29 @@ extern "C" snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T
   if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out)) return SNN_ERR_INVALID_ARG;
   if (too_big(T, B, N_in) || too_big(T, B, N_out)) return SNN_ERR_INVALID_ARG;
   if (bad_alpha(alpha) || isnan(theta)) return SNN_ERR_INVALID_ARG;
-  if (N_in > kTraceGroups * kThreads * 4) return SNN_ERR_UNSUPPORTED;
+  if (N_out > 16 * 4 * kWave) return SNN_ERR_UNSUPPORTED;
 
-  const int n_jblk = (N_out + kJT - 1) / kJT;
-  int tr_span = (N_in + n_jblk - 1) / n_jblk;
-  tr_span = (tr_span + 3) & ~3;
-  const int P = max(1, min(kPMax, kListBytes / (int)(N_in * sizeof(uint16_t))));
-  const size_t lds = (size_t)P * N_in * sizeof(uint16_t);
-  const bool aligned = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0 &&
-                       (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0;
-  const dim3 grid((unsigned)B * n_jblk);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (aligned)
-    hipLaunchKernelGGL(lif_forward_kernel<true>, grid, dim3(kThreads), lds, s, s_in, W, T, B, N_in, N_out, alpha,
-                       theta, V, s_out, trace_in, P, n_jblk, tr_span);
+  const bool al = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0;
+  const bool vec = (N_out % 4) == 0 && (reinterpret_cast<uintptr_t>(W) % 16) == 0 &&
+                   (reinterpret_cast<uintptr_t>(V) % 16) == 0;
+  const int NQ = (N_out + 4 * kWave - 1) / (4 * kWave);
+  const long rows = (long)(T - 1) * B;
+  if (rows > 0) {
+    const dim3 g((unsigned)((rows + kGatherWaves - 1) / kGatherWaves));
+    if (al && vec) launch_gather<true, true>(NQ, g, s, s_in, W, T, B, N_in, N_out, V);
+    else if (al) launch_gather<true, false>(NQ, g, s, s_in, W, T, B, N_in, N_out, V);
+    else if (vec) launch_gather<false, true>(NQ, g, s, s_in, W, T, B, N_in, N_out, V);
+    else launch_gather<false, false>(NQ, g, s, s_in, W, T, B, N_in, N_out, V);
+  }
+  const int nv = (int)(((size_t)B * N_out + kScanThreads - 1) / kScanThreads);
+  const int nt = trace_in ? (int)(((size_t)B * ((N_in + 3) / 4) + kScanThreads - 1) / kScanThreads) : 0;
+  const bool tal = al && (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0;
+  if (tal)
+    hipLaunchKernelGGL(lif_scan<true>, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out,
+                       alpha, theta, V, s_out, trace_in, nv);
   else
-    hipLaunchKernelGGL(lif_forward_kernel<false>, grid, dim3(kThreads), lds, s, s_in, W, T, B, N_in, N_out, alpha,
-                       theta, V, s_out, trace_in, P, n_jblk, tr_span);
+    hipLaunchKernelGGL(lif_scan<false>, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out,
+                       alpha, theta, V, s_out, trace_in, nv);
   return launch_status();
 }

@@ -57,7 +57,7 @@ def test_forward_rejects(lib, kw):
 
 
 def test_forward_unsupported_width(lib):
-    assert _fwd(lib, N_in=5000) == snn.SNN_ERR_UNSUPPORTED
+    assert _fwd(lib, N_out=5000) == snn.SNN_ERR_UNSUPPORTED
 
 
 def _cmp(lib, **kw):
