@@ -2,15 +2,22 @@
 
 One step = the whole path over one batch of the workload: LIF forward of every layer and
 the readout, readout loss, active-set compaction of every LIF layer, the sparse backward
-chain, and the dense matrix-core baseline chain. HIP events on the launch stream time each
-part; the headline is the sparse backward (compaction + snn_sparse_backward of every LIF
-layer; the readout's own backward and the loss are outside both chains).
+chain, and the dense matrix-core baseline chain. HIP events time each part; the headline is
+the sparse backward (compaction + sparse backward of every LIF layer; the readout's own
+backward and the loss are outside both chains, as are the forward passes).
+
+In each LIF layer the spike gradient (snn_sparse_grad_in) runs on an auxiliary stream beside
+dW (snn_sparse_dw) on the main stream; the layer's time is taken on the main stream from the
+fork to the join. dW is the dominant kernel: events on the main stream bracket each of its
+calls, and the roofline object is computed from those durations.
 
 Prints ONE JSON line. `value` = active neuron-steps per second of the sparse backward
 (sum over LIF layers of the active entries, divided by its time); the dense time and the
 speedup are in the same line. Inputs are resident in HBM before timing starts.
 
     python bench.py [--steps K] [--warmup W] [--workload stress] [--b-th 0.2] [--no-cpu]
+    python bench.py --sweep            one JSON line per B_th of the workload's sweep
+    python bench.py --copy-probe MB    device copies of known size (counter calibration)
 """
 from __future__ import annotations
 
@@ -28,8 +35,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-FP32_PEAK_TFLOPS = 157.3
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_backward_stress.json")
+# float64 LDS read-modify-write adds: 256 CUs x 2.4 GHz x 128 B/clk of LDS, 16 B per lane
+# update (8 read, 8 written) -> 4.915e12 lane updates/s; 2 flops each (multiply, add)
+LDS_F64_RMW_TFLOPS = 2 * 256 * 2.4e9 * 128 / 16 / 1e12
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_dw_stress.json")
 CSRC = os.path.join(ROOT, "paper_2105_08810_amd", "csrc")
 
 
@@ -43,20 +52,21 @@ def csrc_digest() -> str:
 
 
 def algorithmic(T, B, n_in, n_out, nnz_out, r_out, nnz_in=None):
-    """Gathered bytes and flops of one layer's sparse backward.
+    """Gathered bytes and flops of one layer's sparse backward, split into (dW, spike gradient).
 
-    bytes: trace rows with at least one active output, the output CSR (index, g, eps), the
-    row pointers and the dW write; with a spike gradient also W once, the input CSR index and
-    the eps_in write, and its row pointers. flops: 2 per multiply-add of the sparse dW and
-    grad_in sums plus the delta recurrence.
+    dW: trace rows with at least one active output, the output CSR (index, g, eps), the row
+    pointers and the dW write; 2 flops per multiply-add. Spike gradient: W once, the input
+    CSR index, the eps_in write and its row pointers; 2 flops per multiply-add plus the delta
+    recurrence.
     """
     TB = T * B
-    by = 4 * n_in * r_out + 12 * nnz_out + 4 * (TB + 1) + 4 * n_in * n_out
-    fl = 2 * nnz_out * n_in
+    by_dw = 4 * n_in * r_out + 12 * nnz_out + 4 * (TB + 1) + 4 * n_in * n_out
+    fl_dw = 2 * nnz_out * n_in
+    by_gi = fl_gi = 0
     if nnz_in is not None:
-        by += 4 * n_in * n_out + 8 * nnz_in + 4 * (TB + 1)
-        fl += 2 * nnz_in * n_out + 2 * TB * n_out
-    return by, fl
+        by_gi = 4 * n_in * n_out + 8 * nnz_in + 4 * (TB + 1)
+        fl_gi = 2 * nnz_in * n_out + 2 * TB * n_out
+    return by_dw, fl_dw, by_gi, fl_gi
 
 
 def cpu_baseline(cfg, b_th, n_samples):
@@ -85,158 +95,244 @@ def cpu_baseline(cfg, b_th, n_samples):
             "host_cpus": len(os.sched_getaffinity(0)), "blas": blas}
 
 
+def copy_probe(mb):
+    """Device-to-device copies of a known size (for scaling the HBM byte counters)."""
+    import torch
+    n = mb * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "copies": 5}))
+
+
+class Runner:
+    """Device state of one workload and the timed step."""
+
+    def __init__(self, cfg, args):
+        import torch
+        from paper_2105_08810_amd import pipeline, snn
+        from synth import make_inputs
+        self.torch, self.snn = torch, snn
+        self.cfg, self.args = cfg, args
+        inp = make_inputs(cfg)
+        self.net = net = pipeline.from_inputs(inp, "cuda:0").allocate()
+        self.T, self.B, self.L = net.T, net.B, net.L
+        self.sizes = list(cfg.sizes)
+        net.forward()
+        self.main = torch.cuda.current_stream()
+        self.aux = self.main if args.serial else torch.cuda.Stream()  # default priority
+        T, B, L, sizes = self.T, self.B, self.L, self.sizes
+        self.ws_dn = None if args.no_dense else snn.workspace(
+            max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
+        self.ws_gi = snn.workspace(max(snn.snn_sparse_grad_in_workspace(T, B, sizes[l + 1]) for l in range(L + 1)))
+        self.ro = net.readout(dense=not args.no_dense)
+        self.ws_ro = snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[L], sizes[L + 1],
+                                                                     self.ro[0].capacity))
+
+    def prepare(self, b_th):
+        """Size compaction outputs and workspaces for one band (the first compaction counts)."""
+        snn, T, B, L, sizes = self.snn, self.T, self.B, self.L, self.sizes
+        self.b_th = b_th
+        csrs = self.net.compact(b_th)
+        self.caps = [c.capacity for c in csrs]
+        self.ws_dw = [snn.workspace(snn.snn_sparse_dw_workspace(T, B, sizes[l], sizes[l + 1], self.caps[l]))
+                      for l in range(L)]
+        self.dW = [self.torch.empty((sizes[l], sizes[l + 1]), dtype=self.torch.float32, device="cuda:0")
+                   for l in range(L)]
+        self.eps = [self.torch.empty(self.caps[l], dtype=self.torch.float32, device="cuda:0") for l in range(L)]
+        # the walk keeps to two blocks per CU when the dW beside it is the longer job
+        self.share = [False] + [3.0 * self.caps[l] * sizes[l] >= 2.0 * self.caps[l - 1] * sizes[l + 1]
+                                for l in range(1, L)]
+
+    def step(self, ev, dense=True):
+        """One pass of the whole path. ev: dict of event lists, recorded in order."""
+        torch, snn, net = self.torch, self.snn, self.net
+        T, B, L = self.T, self.B, self.L
+        main, aux = self.main, self.aux
+        E = lambda k: ev[k]  # noqa: E731
+        E("fwd0").record(main)
+        net.forward()
+        E("fwd1").record(main)
+        r = net.readout(dense=dense and not self.args.no_dense)
+        E("cmp0").record(main)
+        cs = net.compact(self.b_th, self.caps)
+        E("cmp1").record(main)
+        _, eps = snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1], inp=cs[L - 1],
+                                     ws=self.ws_ro, aux_stream=None if self.args.serial else aux)
+        E("ro1").record(main)
+        for l in range(L - 1, -1, -1):
+            i = L - 1 - l  # top layer first
+            ev["lay0"][i].record(main)
+            if l > 0:
+                if aux is not main:
+                    aux.wait_stream(main)
+                ev["gi0"][i].record(aux)
+                snn.sparse_grad_in(net.Ws[l], net.alphas[l], T, B, cs[l], eps, cs[l - 1],
+                                   share_cu=self.share[l] and aux is not main,
+                                   ws=self.ws_gi, stream=aux, eps_in=self.eps[l - 1])
+                ev["gi1"][i].record(aux)
+            ev["dw0"][i].record(main)
+            snn.sparse_dw(net.trace[l], cs[l], eps, net.Ws[l].shape[1], ws=self.ws_dw[l], stream=main,
+                          dW=self.dW[l])
+            ev["dw1"][i].record(main)
+            if l > 0:
+                if aux is not main:
+                    main.wait_stream(aux)
+                eps = self.eps[l - 1]
+            ev["lay1"][i].record(main)
+        if dense and not self.args.no_dense:
+            _, e = snn.dense_backward_ref(net.W_out, net.trace_out, net.V_out, r[3], net.alpha_out, math.inf,
+                                          math.inf, net.beta, grad_in=True, ws=self.ws_dn)
+            E("dn0").record(main)
+            for l in range(L - 1, -1, -1):
+                _, e = snn.dense_backward_ref(net.Ws[l], net.trace[l], net.V[l], e, net.alphas[l], net.theta,
+                                              self.b_th, net.beta, grad_in=l > 0, ws=self.ws_dn)
+            E("dn1").record(main)
+        return cs
+
+    def events(self):
+        mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
+        ev = {k: mk() for k in ("fwd0", "fwd1", "cmp0", "cmp1", "ro1", "dn0", "dn1")}
+        for k in ("lay0", "lay1", "gi0", "gi1", "dw0", "dw1"):
+            ev[k] = [mk() for _ in range(self.L)]
+        return ev
+
+    def run(self, steps, warmup, dense=True):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step(self.events(), dense)
+        torch.cuda.synchronize()
+        evs = [self.events() for _ in range(steps)]
+        t0 = time.perf_counter()
+        for k in range(steps):
+            cs = self.step(evs[k], dense)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return evs, cs, wall
+
+    def summarize(self, evs, cs, wall, dense=True):
+        T, B, L, sizes = self.T, self.B, self.L, self.sizes
+        cfg = self.cfg
+
+        def span(a, b, i=None):
+            if i is None:
+                return np.array([e[a].elapsed_time(e[b]) for e in evs])
+            return np.array([e[a][i].elapsed_time(e[b][i]) for e in evs])
+
+        med = lambda a: float(np.median(a))  # noqa: E731
+        t_fwd = span("fwd0", "fwd1")
+        t_layers = [np.array([e["lay0"][i].elapsed_time(e["lay1"][i]) for e in evs]) for i in range(L)]
+        t_dw = [span("dw0", "dw1", i) for i in range(L)]
+        t_gi = [np.array([e["gi0"][i].elapsed_time(e["gi1"][i]) for e in evs]) for i in range(L - 1)]
+        t_cmp = span("cmp0", "cmp1")
+        t_sparse = t_cmp + sum(t_layers)
+        t_step = np.array([e["fwd0"].elapsed_time(e["dn1" if dense and not self.args.no_dense else "ro1"])
+                           for e in evs])
+
+        nnz = [c.nnz() for c in cs]
+        r_out = [int((c.row_ptr[1:] > c.row_ptr[:-1]).sum().item()) for c in cs]
+        per = [algorithmic(T, B, sizes[l], sizes[l + 1], nnz[l], r_out[l], nnz[l - 1] if l > 0 else None)
+               for l in range(L)]
+        dw_ms = [med(t) for t in reversed(t_dw)]  # layer order
+        dw_flops = sum(p[1] for p in per)
+        dw_bytes = sum(p[0] for p in per)
+        dw_s = sum(dw_ms) * 1e-3
+        achieved = dw_flops / dw_s / 1e12
+        value = sum(nnz) / (med(t_sparse) * 1e-3)
+        traffic = None
+        if os.path.exists(TRAFFIC_FILE):
+            with open(TRAFFIC_FILE) as f:
+                tr = json.load(f)
+            if tr.get("csrc_digest") == csrc_digest() and tr.get("workload") == f"{cfg.name}:{self.b_th}":
+                traffic = tr.get("hbm_bytes_per_launch")
+        out = {
+            "metric": "sparse backward ms/batch + active neuron-steps/s, speedup vs dense BPTT",
+            "value": value,
+            "unit": "active neuron-steps/s",
+            "n_gpus": 1,
+            "steps": len(evs),
+            "warmup": self.args.warmup,
+            "ms_per_step": med(t_step),
+            "higher_is_better": True,
+            "scaling": "weak",
+            "vs_baseline": None,
+            "dtype": "f32",
+            "data": "synthetic",
+            "config": {"workload": f"{cfg.name}: {cfg.description}; B_th={self.b_th}", "T": T, "B": B,
+                       "sizes": sizes, "b_th": self.b_th, "alpha": float(cfg.alpha), "beta": cfg.beta},
+            "sparse_backward_ms": med(t_sparse),
+            "sparse_backward_ms_iqr": [float(np.percentile(t_sparse, 25)), float(np.percentile(t_sparse, 75))],
+            "compaction_ms": med(t_cmp),
+            "sparse_layer_ms": [med(t) for t in reversed(t_layers)],
+            "sparse_dw_ms": dw_ms,
+            "sparse_grad_in_ms": [med(t) for t in reversed(t_gi)],
+            "dense_backward_ms": med(span("dn0", "dn1")) if dense and not self.args.no_dense else None,
+            "forward_ms": med(t_fwd),
+            "active_fraction": [n / (T * B * sizes[l + 1]) for l, n in enumerate(nnz)],
+            "nnz": nnz,
+            "roofline": {
+                "bound": "alu", "achieved": achieved, "peak": LDS_F64_RMW_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / LDS_F64_RMW_TFLOPS, "traffic": traffic,
+                "kernel": "snn_sparse_dw (slab records + dw_slab_kernel + chunk reduction), LIF layers",
+                "resource": "float64 LDS read-modify-write adds (multiply on the VALU)",
+                "algorithmic_flops": dw_flops, "algorithmic_bytes": dw_bytes, "launch_ms": dw_ms,
+                "hbm_achieved_gbs": dw_bytes / dw_s / 1e9, "hbm_frac": dw_bytes / dw_s / 1e9 / HBM_PEAK_GBS,
+            },
+            "wall_s_timed": wall,
+        }
+        if out["dense_backward_ms"] is not None:
+            out["speedup_vs_dense"] = out["dense_backward_ms"] / out["sparse_backward_ms"]
+            out["overall_speedup_fwd_plus_bwd"] = (out["forward_ms"] + out["dense_backward_ms"]) / (
+                out["forward_ms"] + out["sparse_backward_ms"])
+        return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="stress")
     ap.add_argument("--b-th", type=float, default=None)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=16)
     ap.add_argument("--no-dense", action="store_true")
-    ap.add_argument("--serial", action="store_true", help="no auxiliary stream in the sparse backward")
+    ap.add_argument("--serial", action="store_true", help="everything on one stream")
+    ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the path is single-device here (multi-GPU is design only)",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
 
-    import torch
-    from paper_2105_08810_amd import pipeline, snn
-    from synth import CONFIGS, make_inputs
-
+    from paper_2105_08810_amd import snn
+    from synth import CONFIGS
     snn.lib()
     cfg = CONFIGS[args.workload]
-    b_th = cfg.b_th if args.b_th is None else args.b_th
-    inp = make_inputs(cfg)
-    net = pipeline.from_inputs(inp, "cuda:0").allocate()
-    T, B, L = net.T, net.B, net.L
-    sizes = list(cfg.sizes)
-
-    # size everything once (the first compaction counts; inputs are fixed so nnz is too)
-    net.forward()
-    ro = net.readout(dense=not args.no_dense)
-    csrs = net.compact(b_th)
-    caps = [c.capacity for c in csrs]
-    ws_sp = [snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[l], sizes[l + 1], caps[l]))
-             for l in range(L)]
-    ws_ro = snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[L], sizes[L + 1], ro[0].capacity))
-    ws_dn = None if args.no_dense else snn.workspace(
-        max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
-    stream = torch.cuda.current_stream()
-    aux = None if args.serial else torch.cuda.Stream()  # default priority
-
-    def step(ev):
-        ev[0].record(stream)
-        net.forward()
-        ev[1].record(stream)
-        r = net.readout(dense=not args.no_dense)
-        ev[2].record(stream)
-        cs = net.compact(b_th, caps)
-        ev[3].record(stream)
-        dW_out, eps = snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1], inp=cs[L - 1],
-                                          ws=ws_ro, aux_stream=aux)
-        ev[4].record(stream)
-        for l in range(L - 1, -1, -1):
-            ev[5 + 2 * (L - 1 - l)].record(stream)
-            _, eps = snn.sparse_backward(net.Ws[l], net.trace[l], net.alphas[l], cs[l], eps,
-                                         inp=cs[l - 1] if l > 0 else None, ws=ws_sp[l], aux_stream=aux)
-            ev[6 + 2 * (L - 1 - l)].record(stream)
-        k = 5 + 2 * L
-        if not args.no_dense:
-            _, e = snn.dense_backward_ref(net.W_out, net.trace_out, net.V_out, r[3], net.alpha_out, math.inf,
-                                          math.inf, net.beta, grad_in=True, ws=ws_dn)
-            ev[k].record(stream)
-            for l in range(L - 1, -1, -1):
-                _, e = snn.dense_backward_ref(net.Ws[l], net.trace[l], net.V[l], e, net.alphas[l], net.theta, b_th,
-                                              net.beta, grad_in=l > 0, ws=ws_dn)
-            ev[k + 1].record(stream)
-        else:
-            ev[k].record(stream)
-            ev[k + 1].record(stream)
-        return cs
-
-    n_ev = 7 + 2 * L
-    for _ in range(args.warmup):
-        step([torch.cuda.Event(enable_timing=True) for _ in range(n_ev)])
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
-    t_wall0 = time.perf_counter()
-    for k in range(args.steps):
-        cs = step(evs[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall0
-
-    def span(a, b):
-        return np.array([e[a].elapsed_time(e[b]) for e in evs])  # ms
-
-    t_fwd = span(0, 1)
-    t_cmp = span(2, 3)
-    t_layers = [span(5 + 2 * i, 6 + 2 * i) for i in range(L)]  # top layer first
-    t_sparse = t_cmp + sum(t_layers)
-    t_dense = span(5 + 2 * L, 6 + 2 * L)
-    t_step = span(0, 6 + 2 * L)
-
-    # active entries and algorithmic bytes (bookkeeping outside the timed steps)
-    nnz = [c.nnz() for c in cs]
-    r_out = [int((c.row_ptr[1:] > c.row_ptr[:-1]).sum().item()) for c in cs]
-    by_l, fl_l = [], []
-    for l in range(L):
-        by, fl = algorithmic(T, B, sizes[l], sizes[l + 1], nnz[l], r_out[l], nnz[l - 1] if l > 0 else None)
-        by_l.append(by)
-        fl_l.append(fl)
-    med = lambda a: float(np.median(a))  # noqa: E731
-    t_bwd_kernels = sum(med(t) for t in t_layers)  # snn_sparse_backward of all LIF layers
-    gb = sum(by_l)
-    achieved = gb / (t_bwd_kernels * 1e-3) / 1e9
-    flops = sum(fl_l)
-    value = sum(nnz) / (med(t_sparse) * 1e-3)
-
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
-            tr = json.load(f)
-        if tr.get("csrc_digest") == csrc_digest() and tr.get("workload") == f"{cfg.name}:{b_th}":
-            traffic = tr.get("bytes_per_step")
-
-    out = {
-        "metric": "sparse backward ms/batch + active neuron-steps/s, speedup vs dense BPTT",
-        "value": value,
-        "unit": "active neuron-steps/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": med(t_step),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {cfg.description}; B_th={b_th}", "T": T, "B": B,
-                   "sizes": sizes, "b_th": b_th, "alpha": float(cfg.alpha), "beta": cfg.beta},
-        "sparse_backward_ms": med(t_sparse),
-        "sparse_backward_ms_iqr": [float(np.percentile(t_sparse, 25)), float(np.percentile(t_sparse, 75))],
-        "compaction_ms": med(t_cmp),
-        "sparse_layer_ms": [med(t) for t in reversed(t_layers)],
-        "dense_backward_ms": None if args.no_dense else med(t_dense),
-        "speedup_vs_dense": None if args.no_dense else med(t_dense) / med(t_sparse),
-        "forward_ms": med(t_fwd),
-        "overall_speedup_fwd_plus_bwd": None if args.no_dense else (med(t_fwd) + med(t_dense)) / (
-            med(t_fwd) + med(t_sparse)),
-        "active_fraction": [n / (T * B * sizes[l + 1]) for l, n in enumerate(nnz)],
-        "nnz": nnz,
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "snn_sparse_backward, all LIF layers per step",
-                     "algorithmic_bytes": gb, "algorithmic_flops": flops,
-                     "alu_frac": flops / (t_bwd_kernels * 1e-3) / 1e12 / FP32_PEAK_TFLOPS,
-                     "launch_ms": t_bwd_kernels},
-        "wall_s_timed": wall,
-    }
-    if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(cfg, b_th, args.cpu_samples)
-    print(json.dumps(out))
+    run = Runner(cfg, args)
+    points = cfg.sweep if args.sweep else (cfg.b_th if args.b_th is None else args.b_th,)
+    dense_ms = None
+    for k, b_th in enumerate(points):
+        run.prepare(b_th)
+        dense = not args.no_dense and (k == 0 or not args.sweep)  # the dense chain's cost does not depend on B_th
+        evs, cs, wall = run.run(args.steps, args.warmup, dense)
+        out = run.summarize(evs, cs, wall, dense)
+        if dense:
+            dense_ms = out["dense_backward_ms"]
+        elif dense_ms is not None:
+            out["dense_backward_ms"] = dense_ms
+            out["speedup_vs_dense"] = dense_ms / out["sparse_backward_ms"]
+            out["overall_speedup_fwd_plus_bwd"] = (out["forward_ms"] + dense_ms) / (
+                out["forward_ms"] + out["sparse_backward_ms"])
+        if not args.no_cpu and not args.sweep:
+            out["cpu_baseline"] = cpu_baseline(cfg, b_th, args.cpu_samples)
+        print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

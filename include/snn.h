@@ -123,6 +123,34 @@ snn_status snn_sparse_backward(const float* W, const float* trace_in, int T, int
                                void* stream, void* aux_stream);
 
 /*
+ * The two halves of snn_sparse_backward as calls of their own, for callers that schedule them
+ * on different streams (the combined call does this itself when given aux_stream). Arguments
+ * mean the same as in snn_sparse_backward; the results are the same as its results.
+ *
+ * snn_sparse_dw: dW of one layer (sparse form of Eq. (w_grad)), overwriting dW [N_in,N_out].
+ *   Needs no W. Workspace from snn_sparse_dw_workspace (depends on out_cap).
+ * snn_sparse_grad_in: the spike gradient eps_in at the input layer's active entries (sparse
+ *   form of Eq. (s_grad) with Proposition 1's recurrence). in_row_ptr is required; nothing is
+ *   written when in_cap = 0. share_cu != 0 keeps the walk to two blocks per compute unit, so
+ *   that a kernel launched beside it on another stream (dW) finds room; 0 uses the whole GPU.
+ *   Workspace from snn_sparse_grad_in_workspace.
+ * The two calls use separate workspaces and may run concurrently.
+ */
+size_t snn_sparse_dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap);
+snn_status snn_sparse_dw(const float* trace_in, int T, int B, int N_in, int N_out,
+                         const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
+                         const float* eps_out, int64_t out_cap, float* dW, void* workspace,
+                         size_t workspace_bytes, void* stream);
+size_t snn_sparse_grad_in_workspace(int T, int B, int N_out);
+snn_status snn_sparse_grad_in(const float* W, int T, int B, int N_in, int N_out, float alpha,
+                              const int32_t* out_row_ptr, const int32_t* out_col_idx,
+                              const float* out_g, const float* eps_out, int64_t out_cap,
+                              const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap,
+                              float* eps_in, int share_cu, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+
+/*
  * Dense surrogate BPTT of one layer on matrix cores: the baseline the sparse rule is
  * measured against (Table 1, "Original").
  *   W, trace_in as above; V [T,B,N_out] (read); eps_out [T,B,N_out] dense loss gradient

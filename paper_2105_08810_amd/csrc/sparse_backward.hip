@@ -513,15 +513,14 @@ void launch_walk(dim3 grid, size_t lds, hipStream_t s, const float* W, int T, in
 
 using namespace snn;
 
-extern "C" size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
-  if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out) || out_cap < 0) return 0;
-  if (too_big(T, B, N_in) || too_big(T, B, N_out)) return 0;
+namespace snn {
+namespace {
+
+size_t dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
   const DwPlan p = plan_dw(T, B, N_in, N_out);
-  const WalkPlan wp = plan_walk(T);
+  const int nsp = p.n_slabs * T * B;
   Carve c(nullptr);
   if (p.n_chunks > 1) c.take<float>((size_t)p.n_chunks * N_in * N_out);
-  c.take<float>((size_t)wp.C * B * N_out);
-  const int nsp = p.n_slabs * T * B;
   c.take<int32_t>((size_t)nsp + 1);
   c.take<int32_t>((size_t)nsp);
   c.take<int32_t>(scan_temp_elems(nsp));
@@ -529,84 +528,42 @@ extern "C" size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_ou
   return c.off;
 }
 
-extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in, int T, int B, int N_in, int N_out,
-                                          float alpha, const int32_t* out_row_ptr, const int32_t* out_col_idx,
-                                          const float* out_g, const float* eps_out, int64_t out_cap,
-                                          const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap,
-                                          float* eps_in, float* dW, void* workspace, size_t workspace_bytes,
-                                          void* stream, void* aux_stream) {
-  if (!W || !trace_in || !out_row_ptr || !dW) return SNN_ERR_INVALID_ARG;
-  if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out)) return SNN_ERR_INVALID_ARG;
-  if (too_big(T, B, N_in) || too_big(T, B, N_out)) return SNN_ERR_INVALID_ARG;
-  if (bad_alpha(alpha) || out_cap < 0 || in_cap < 0) return SNN_ERR_INVALID_ARG;
-  if (out_cap > 0 && (!out_col_idx || !eps_out)) return SNN_ERR_INVALID_ARG;
-  const bool grad_in = in_row_ptr != nullptr;
-  if (grad_in && in_cap > 0 && (!in_col_idx || !eps_in)) return SNN_ERR_INVALID_ARG;
-  if (!grad_in && (in_col_idx || eps_in)) return SNN_ERR_INVALID_ARG;
-  const size_t need = snn_sparse_backward_workspace(T, B, N_in, N_out, out_cap);
-  if (need > 0 && (!workspace || workspace_bytes < need)) return SNN_ERR_INVALID_ARG;
-  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+size_t gin_workspace(int T, int B, int N_out) {
+  const WalkPlan wp = plan_walk(T);
+  Carve c(nullptr);
+  c.take<float>((size_t)wp.C * B * N_out);
+  return c.off;
+}
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
+bool dims_ok(int T, int B, int N_in, int N_out) {
+  return !(bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out) || too_big(T, B, N_in) ||
+           too_big(T, B, N_out));
+}
+
+void fill_zero_async(float* p, size_t n, hipStream_t s) {
+  if (n == 0) return;
+  hipLaunchKernelGGL(fill_zero, dim3((unsigned)std::min<size_t>((n + 255) / 256, 4096)), dim3(256), 0, s, p, n);
+}
+
+// dW of one layer: group-major records of the active entries, the slab accumulation, the
+// reduction over row chunks. Arguments already validated.
+void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const int32_t* out_row_ptr,
+                const int32_t* out_col_idx, const float* out_g, const float* eps_out, int64_t out_cap, float* dW,
+                void* workspace, hipStream_t s) {
+  if (out_cap == 0) {  // no active output entry: dW = 0 and no entry array is read
+    fill_zero_async(dW, (size_t)N_in * N_out, s);
+    return;
+  }
   const int TB = T * B;
   const DwPlan p = plan_dw(T, B, N_in, N_out);
-  const WalkPlan wp = plan_walk(T);
   Carve ws(workspace);
   float* part = p.n_chunks > 1 ? ws.take<float>((size_t)p.n_chunks * N_in * N_out) : dW;
-  float* Lbuf = ws.take<float>((size_t)wp.C * B * N_out);
   const int nsp = p.n_slabs * TB;
   int32_t* sp = ws.take<int32_t>((size_t)nsp + 1);
   int32_t* scnt = ws.take<int32_t>((size_t)nsp);
   int32_t* stmp = ws.take<int32_t>(scan_temp_elems(nsp));
   SlabRec* rec = ws.take<SlabRec>((size_t)std::max<int64_t>(out_cap, 1));
 
-  if (out_cap == 0) {  // no active output entry: dW = 0 and eps_in = 0; no entry array is read
-    hipLaunchKernelGGL(fill_zero, dim3((unsigned)std::min<size_t>(((size_t)N_in * N_out + 255) / 256, 4096)),
-                       dim3(256), 0, s, dW, (size_t)N_in * N_out);
-    if (grad_in && in_cap > 0)
-      hipLaunchKernelGGL(fill_zero, dim3((unsigned)std::min<int64_t>((in_cap + 255) / 256, 4096)), dim3(256), 0, s,
-                         eps_in, (size_t)in_cap);
-    return launch_status();
-  }
-  // The spike gradient (L2-gather bound) and dW (LDS-atomic bound) use different parts of a
-  // CU; with an auxiliary stream they run side by side. aux waits for what is already on s,
-  // and s waits for aux before anything enqueued after this call.
-  hipStream_t sa = s;
-  hipEvent_t ev_in = nullptr, ev_out = nullptr;
-  const bool split = aux_stream && aux_stream != stream && grad_in && in_cap > 0;
-  if (split && hipEventCreateWithFlags(&ev_in, hipEventDisableTiming) == hipSuccess &&
-      hipEventCreateWithFlags(&ev_out, hipEventDisableTiming) == hipSuccess &&
-      hipEventRecord(ev_in, s) == hipSuccess &&
-      hipStreamWaitEvent(static_cast<hipStream_t>(aux_stream), ev_in, 0) == hipSuccess) {
-    sa = static_cast<hipStream_t>(aux_stream);
-  }
-  if (grad_in && in_cap > 0) {
-    const int pairs = wp.C * B;
-    const dim3 wgrid((pairs + kWalkWaves - 1) / kWalkWaves);
-    const size_t lds = (size_t)kWalkWaves * N_out * sizeof(float);  // chunk sums only
-    hipLaunchKernelGGL(gin_chunk_sums, wgrid, dim3(kWalkThreads), lds, sa, T, B, N_out, alpha, wp.P, wp.C,
-                       out_row_ptr, out_col_idx, out_g, eps_out, out_cap, Lbuf);
-    const size_t BN = (size_t)B * N_out;
-    hipLaunchKernelGGL(gin_carries, dim3((unsigned)((BN + 255) / 256)), dim3(256), 0, sa, T, B, N_out, alpha, wp.P,
-                       wp.C, Lbuf);
-    const int nj = (N_out + kWave - 1) / kWave;
-    // beside a dW that takes longer than the walk, the walk keeps to two blocks per CU so that a
-    // dW block fits next to it (per product, a dW entry costs about 1.5 times a walk entry)
-    const bool dw_longer = 3.0 * (double)out_cap * N_in >= 2.0 * (double)in_cap * N_out;
-    const dim3 walk_grid(sa != s && dw_longer ? std::min<unsigned>(wgrid.x, 2 * kAssumedCUs) : wgrid.x);
-#define SNN_WALK(NJ_)                                                                                         \
-  launch_walk<NJ_>(walk_grid, 0, sa, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, \
-                   eps_out, out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)
-    if (nj <= 1) SNN_WALK(1);
-    else if (nj <= 2) SNN_WALK(2);
-    else if (nj <= 4) SNN_WALK(4);
-    else if (nj <= 8) SNN_WALK(8);
-    else if (nj <= 16) SNN_WALK(16);
-    else if (nj <= 32) SNN_WALK(32);
-    else SNN_WALK(64);
-#undef SNN_WALK
-  }
-  // slab-major records of the active entries, then the slab accumulation
   const int R = std::max(1, std::min(8, kWave / p.n_slabs));  // rows per wavefront
   const int nwaves = (TB + R - 1) / R;
   const dim3 rgrid((unsigned)((nwaves + kRowWaves - 1) / kRowWaves));
@@ -623,14 +580,143 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
                        out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
   const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
   (void)hipFuncSetAttribute((const void*)dw_slab_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
-  hipLaunchKernelGGL(dw_slab_kernel, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out, sp, rec,
-                     out_cap, part, p.rows_per_chunk, p.n_itiles, p.n_slabs, p.slab);
+  hipLaunchKernelGGL(dw_slab_kernel, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out, sp, rec, nrec,
+                     part, p.rows_per_chunk, p.n_itiles, p.n_slabs, p.slab);
   if (p.n_chunks > 1) {
     const size_t n = (size_t)N_in * N_out;
     const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
     hipLaunchKernelGGL(reduce_chunks, dim3(blocks), dim3(256), 0, s, part, p.n_chunks, n, dW);
   }
+}
 
+// Spike gradient of one layer: chunk sums, carries, the walk. share_cu keeps the walk to two
+// blocks per CU so that a kernel running beside it (dW) finds room. Arguments already validated.
+void enqueue_grad_in(const float* W, int T, int B, int N_in, int N_out, float alpha, const int32_t* out_row_ptr,
+                     const int32_t* out_col_idx, const float* out_g, const float* eps_out, int64_t out_cap,
+                     const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap, float* eps_in,
+                     bool share_cu, void* workspace, hipStream_t s) {
+  if (in_cap == 0) return;
+  if (out_cap == 0) {  // no active output entry: delta = 0 everywhere
+    fill_zero_async(eps_in, (size_t)in_cap, s);
+    return;
+  }
+  const WalkPlan wp = plan_walk(T);
+  Carve ws(workspace);
+  float* Lbuf = ws.take<float>((size_t)wp.C * B * N_out);
+  const int pairs = wp.C * B;
+  const dim3 wgrid((pairs + kWalkWaves - 1) / kWalkWaves);
+  const size_t lds = (size_t)kWalkWaves * N_out * sizeof(float);  // chunk sums only
+  hipLaunchKernelGGL(gin_chunk_sums, wgrid, dim3(kWalkThreads), lds, s, T, B, N_out, alpha, wp.P, wp.C, out_row_ptr,
+                     out_col_idx, out_g, eps_out, out_cap, Lbuf);
+  const size_t BN = (size_t)B * N_out;
+  hipLaunchKernelGGL(gin_carries, dim3((unsigned)((BN + 255) / 256)), dim3(256), 0, s, T, B, N_out, alpha, wp.P, wp.C,
+                     Lbuf);
+  const int nj = (N_out + kWave - 1) / kWave;
+  const dim3 walk_grid(share_cu ? std::min<unsigned>(wgrid.x, 2 * kAssumedCUs) : wgrid.x);
+#define SNN_WALK(NJ_)                                                                                             \
+  launch_walk<NJ_>(walk_grid, 0, s, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, eps_out, \
+                   out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)
+  if (nj <= 1) SNN_WALK(1);
+  else if (nj <= 2) SNN_WALK(2);
+  else if (nj <= 4) SNN_WALK(4);
+  else if (nj <= 8) SNN_WALK(8);
+  else if (nj <= 16) SNN_WALK(16);
+  else if (nj <= 32) SNN_WALK(32);
+  else SNN_WALK(64);
+#undef SNN_WALK
+}
+
+// common checks of the output-side CSR and its gradient
+bool out_csr_ok(const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* eps_out, int64_t out_cap) {
+  if (!out_row_ptr || out_cap < 0) return false;
+  return out_cap == 0 || (out_col_idx && eps_out);
+}
+
+}  // namespace
+}  // namespace snn
+
+extern "C" size_t snn_sparse_dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
+  if (!dims_ok(T, B, N_in, N_out) || out_cap < 0) return 0;
+  return dw_workspace(T, B, N_in, N_out, out_cap);
+}
+
+extern "C" snn_status snn_sparse_dw(const float* trace_in, int T, int B, int N_in, int N_out,
+                                    const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
+                                    const float* eps_out, int64_t out_cap, float* dW, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  if (!trace_in || !dW || !dims_ok(T, B, N_in, N_out)) return SNN_ERR_INVALID_ARG;
+  if (!out_csr_ok(out_row_ptr, out_col_idx, eps_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < dw_workspace(T, B, N_in, N_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+  enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, workspace,
+             static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" size_t snn_sparse_grad_in_workspace(int T, int B, int N_out) {
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N_out) || too_big(T, B, N_out)) return 0;
+  return gin_workspace(T, B, N_out);
+}
+
+extern "C" snn_status snn_sparse_grad_in(const float* W, int T, int B, int N_in, int N_out, float alpha,
+                                         const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
+                                         const float* eps_out, int64_t out_cap, const int32_t* in_row_ptr,
+                                         const int32_t* in_col_idx, int64_t in_cap, float* eps_in, int share_cu,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!W || !dims_ok(T, B, N_in, N_out) || bad_alpha(alpha)) return SNN_ERR_INVALID_ARG;
+  if (!out_csr_ok(out_row_ptr, out_col_idx, eps_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (!in_row_ptr || in_cap < 0 || (in_cap > 0 && (!in_col_idx || !eps_in))) return SNN_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < gin_workspace(T, B, N_out)) return SNN_ERR_INVALID_ARG;
+  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+  enqueue_grad_in(W, T, B, N_in, N_out, alpha, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, in_row_ptr,
+                  in_col_idx, in_cap, eps_in, share_cu != 0, workspace, static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
+  if (!dims_ok(T, B, N_in, N_out) || out_cap < 0) return 0;
+  return align256(dw_workspace(T, B, N_in, N_out, out_cap)) + gin_workspace(T, B, N_out);
+}
+
+extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in, int T, int B, int N_in, int N_out,
+                                          float alpha, const int32_t* out_row_ptr, const int32_t* out_col_idx,
+                                          const float* out_g, const float* eps_out, int64_t out_cap,
+                                          const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap,
+                                          float* eps_in, float* dW, void* workspace, size_t workspace_bytes,
+                                          void* stream, void* aux_stream) {
+  if (!W || !trace_in || !dW || !dims_ok(T, B, N_in, N_out)) return SNN_ERR_INVALID_ARG;
+  if (bad_alpha(alpha) || in_cap < 0) return SNN_ERR_INVALID_ARG;
+  if (!out_csr_ok(out_row_ptr, out_col_idx, eps_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  const bool grad_in = in_row_ptr != nullptr;
+  if (grad_in && in_cap > 0 && (!in_col_idx || !eps_in)) return SNN_ERR_INVALID_ARG;
+  if (!grad_in && (in_col_idx || eps_in)) return SNN_ERR_INVALID_ARG;
+  const size_t need = snn_sparse_backward_workspace(T, B, N_in, N_out, out_cap);
+  if (!workspace || workspace_bytes < need) return SNN_ERR_INVALID_ARG;
+  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* dw_ws = static_cast<char*>(workspace);
+  char* gin_ws = dw_ws + align256(dw_workspace(T, B, N_in, N_out, out_cap));
+  const bool do_gin = grad_in && in_cap > 0;
+  // The spike gradient (L1/L2-gather bound) and dW (LDS-atomic bound) lean on different parts of
+  // a CU; with an auxiliary stream they run side by side. aux waits for what is already on s,
+  // and s waits for aux before anything enqueued after this call.
+  hipStream_t sa = s;
+  hipEvent_t ev_in = nullptr, ev_out = nullptr;
+  if (do_gin && aux_stream && aux_stream != stream &&
+      hipEventCreateWithFlags(&ev_in, hipEventDisableTiming) == hipSuccess &&
+      hipEventCreateWithFlags(&ev_out, hipEventDisableTiming) == hipSuccess && hipEventRecord(ev_in, s) == hipSuccess &&
+      hipStreamWaitEvent(static_cast<hipStream_t>(aux_stream), ev_in, 0) == hipSuccess) {
+    sa = static_cast<hipStream_t>(aux_stream);
+  }
+  if (do_gin) {
+    // beside a dW that takes longer than the walk, the walk leaves room for a dW block on every
+    // CU (per product, a dW entry costs about 1.5 times a walk entry)
+    const bool dw_longer = 3.0 * (double)out_cap * N_in >= 2.0 * (double)in_cap * N_out;
+    enqueue_grad_in(W, T, B, N_in, N_out, alpha, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, in_row_ptr,
+                    in_col_idx, in_cap, eps_in, sa != s && dw_longer, gin_ws, sa);
+  }
+  enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, dw_ws, s);
   if (sa != s) {
     if (hipEventRecord(ev_out, sa) != hipSuccess || hipStreamWaitEvent(s, ev_out, 0) != hipSuccess)
       (void)hipStreamSynchronize(sa);  // never leave aux work unordered with later work on s

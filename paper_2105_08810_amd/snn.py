@@ -35,6 +35,10 @@ _SIGNATURES = {
     "snn_sparse_backward_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_backward": (_I, [_P, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
                                  _P, _P]),
+    "snn_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
+    "snn_sparse_dw": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_sparse_grad_in_workspace": (_SZ, [_I, _I, _I]),
+    "snn_sparse_grad_in": (_I, [_P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _I, _P, _SZ, _P]),
     "snn_dense_backward_workspace": (_SZ, [_I, _I, _I, _I]),
     "snn_dense_backward_ref": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _F, _F, _F, _F, _P, _P, _P, _SZ, _P]),
     "snn_readout_ce_workspace": (_SZ, [_I, _I, _I, _I]),
@@ -134,6 +138,34 @@ def snn_sparse_backward(W, trace_in, T, B, N_in, N_out, alpha, out_row_ptr, out_
         None if aux_stream is None else aux_stream.cuda_stream))
 
 
+def snn_sparse_dw_workspace(T, B, N_in, N_out, out_cap) -> int:
+    return int(lib().snn_sparse_dw_workspace(T, B, N_in, N_out, int(out_cap)))
+
+
+def snn_sparse_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, ws,
+                  stream=None):
+    _check("snn_sparse_dw", lib().snn_sparse_dw(
+        _ptr(trace_in, torch.float32, "trace_in"), T, B, N_in, N_out, _ptr(out_row_ptr, torch.int32, "out_row_ptr"),
+        _ptr(out_col_idx, torch.int32, "out_col_idx"), _ptr(out_g, torch.float32, "out_g"),
+        _ptr(eps_out, torch.float32, "eps_out"), int(out_cap), _ptr(dW, torch.float32, "dW"),
+        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_sparse_grad_in_workspace(T, B, N_out) -> int:
+    return int(lib().snn_sparse_grad_in_workspace(T, B, N_out))
+
+
+def snn_sparse_grad_in(W, T, B, N_in, N_out, alpha, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, in_row_ptr,
+                       in_col_idx, in_cap, eps_in, share_cu, ws, stream=None):
+    _check("snn_sparse_grad_in", lib().snn_sparse_grad_in(
+        _ptr(W, torch.float32, "W"), T, B, N_in, N_out, float(alpha), _ptr(out_row_ptr, torch.int32, "out_row_ptr"),
+        _ptr(out_col_idx, torch.int32, "out_col_idx"), _ptr(out_g, torch.float32, "out_g"),
+        _ptr(eps_out, torch.float32, "eps_out"), int(out_cap), _ptr(in_row_ptr, torch.int32, "in_row_ptr"),
+        _ptr(in_col_idx, torch.int32, "in_col_idx"), int(in_cap), _ptr(eps_in, torch.float32, "eps_in"),
+        int(share_cu), _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
 def snn_dense_backward_workspace(T, B, N_in, N_out) -> int:
     return int(lib().snn_dense_backward_workspace(T, B, N_in, N_out))
 
@@ -229,6 +261,33 @@ def sparse_backward(W, trace_in, alpha, out: Csr, eps_out, inp: Optional[Csr] = 
                         out.capacity, None if inp is None else inp.row_ptr, None if inp is None else inp.col_idx,
                         0 if inp is None else inp.capacity, eps_in, dW, ws, aux_stream=aux_stream)
     return dW, eps_in
+
+
+def sparse_dw(trace_in, out: Csr, eps_out, N_out, ws=None, stream=None, dW=None):
+    """Run snn_sparse_dw (dW only). Returns dW [N_in, N_out]."""
+    T, B, N_in = trace_in.shape
+    dev = trace_in.device
+    if dW is None:
+        dW = torch.empty((N_in, N_out), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = workspace(snn_sparse_dw_workspace(T, B, N_in, N_out, out.capacity), dev)
+    snn_sparse_dw(trace_in, T, B, N_in, N_out, out.row_ptr, out.col_idx, out.g, eps_out, out.capacity, dW, ws,
+                  stream)
+    return dW
+
+
+def sparse_grad_in(W, alpha, T, B, out: Csr, eps_out, inp: Csr, share_cu=False, ws=None, stream=None,
+                   eps_in=None):
+    """Run snn_sparse_grad_in. Returns eps_in aligned with inp."""
+    N_in, N_out = W.shape
+    dev = W.device
+    if eps_in is None:
+        eps_in = torch.empty(inp.capacity, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = workspace(snn_sparse_grad_in_workspace(T, B, N_out), dev)
+    snn_sparse_grad_in(W, T, B, N_in, N_out, alpha, out.row_ptr, out.col_idx, out.g, eps_out, out.capacity,
+                       inp.row_ptr, inp.col_idx, inp.capacity, eps_in, share_cu, ws, stream)
+    return eps_in
 
 
 def dense_backward_ref(W, trace_in, V, eps_out, alpha, theta, b_th, beta, grad_in=True, ws=None):

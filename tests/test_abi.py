@@ -135,3 +135,45 @@ def test_readout_rejects(lib, kw):
     st = lib.snn_readout_ce(a["V"], a["labels"], a["T"], a["B"], a["C"], a["mode"], a["rp"], a["ci"], a["eps"],
                             a["loss"], a["dense"], a["ws"], a["ws_bytes"], None)
     assert st == snn.SNN_ERR_INVALID_ARG
+
+
+def _sdw(lib, **kw):
+    a = dict(tr=FAKE, T=10, B=4, N_in=32, N_out=16, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE, ocap=10, dW=FAKE, ws=FAKE,
+             ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.snn_sparse_dw(a["tr"], a["T"], a["B"], a["N_in"], a["N_out"], a["orp"], a["oci"], a["og"], a["oeps"],
+                             a["ocap"], a["dW"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(tr=None), dict(dW=None), dict(orp=None), dict(oci=None), dict(oeps=None),
+                                dict(ocap=-1), dict(ws=None), dict(ws_bytes=8), dict(T=0), dict(N_in=-2)])
+def test_sparse_dw_rejects(lib, kw):
+    assert _sdw(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_sparse_dw_unsupported_width(lib):
+    assert _sdw(lib, N_out=5000) == snn.SNN_ERR_UNSUPPORTED
+
+
+def _sgi(lib, **kw):
+    a = dict(W=FAKE, T=10, B=4, N_in=32, N_out=16, alpha=0.9, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE, ocap=10,
+             irp=FAKE, ici=FAKE, icap=10, eps_in=FAKE, share=1, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.snn_sparse_grad_in(a["W"], a["T"], a["B"], a["N_in"], a["N_out"], a["alpha"], a["orp"], a["oci"],
+                                  a["og"], a["oeps"], a["ocap"], a["irp"], a["ici"], a["icap"], a["eps_in"],
+                                  a["share"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(W=None), dict(alpha=0.0), dict(alpha=NAN), dict(orp=None), dict(oeps=None),
+                                dict(irp=None), dict(ici=None), dict(eps_in=None), dict(icap=-1), dict(ws=None),
+                                dict(ws_bytes=4), dict(B=0)])
+def test_sparse_grad_in_rejects(lib, kw):
+    assert _sgi(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_split_workspaces(lib):
+    dw = lib.snn_sparse_dw_workspace(500, 256, 1024, 1024, 10 ** 6)
+    gi = lib.snn_sparse_grad_in_workspace(500, 256, 1024)
+    assert dw > 0 and gi > 0
+    assert lib.snn_sparse_backward_workspace(500, 256, 1024, 1024, 10 ** 6) >= dw + gi
+    assert lib.snn_sparse_grad_in_workspace(0, 256, 1024) == 0

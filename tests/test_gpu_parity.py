@@ -263,3 +263,32 @@ def test_compaction_long_rows(name, batch, b_th):
         assert_env(_np(c.g[:n]).astype(F64), g, np.abs(g), f"g[{l}]", tol=2e-6)
         longest = max(longest, int(np.diff(rp).max()))
     assert longest > 64  # the re-read path ran
+
+
+@pytest.mark.parametrize("name,batch,b_th", [("latency", list(range(32)), 0.2), ("stress", list(range(8)), 0.2)])
+def test_split_calls_match_combined(name, batch, b_th):
+    """snn_sparse_dw and snn_sparse_grad_in, on two streams, give the combined call's results."""
+    print(f"\n[case] split calls {name} b_th={b_th}", flush=True)
+    inp = _case(name, batch)
+    g = _gpu(inp, b_th, dense=False)
+    net, csrs, ro = g["net"], g["csrs"], g["ro"]
+    T, B, L = net.T, net.B, net.L
+    aux = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    eps = g["eps"][L - 1]  # eps of the top hidden layer from the combined readout call
+    for l in range(L - 1, -1, -1):
+        W = net.Ws[l]
+        if l > 0:
+            aux.wait_stream(main)
+            with torch.cuda.stream(aux):
+                eps_in = snn.sparse_grad_in(W, net.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=True,
+                                            stream=aux)
+        dW = snn.sparse_dw(net.trace[l], csrs[l], eps, W.shape[1])
+        main.wait_stream(aux)
+        torch.cuda.synchronize()
+        ref_dW = g["dW"][l]
+        assert torch.allclose(dW, ref_dW, rtol=1e-6, atol=1e-7 * float(ref_dW.abs().max())), f"dW[{l}]"
+        if l > 0:
+            n = csrs[l - 1].nnz()
+            assert torch.equal(eps_in[:n], g["eps"][l - 1][:n]), f"eps[{l - 1}]"  # fixed order: bit-equal
+            eps = eps_in
