@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kRowWaves * kWave) void slab_fill(int TB, int N_out
   }
 }
 
-// Block (it, sl, c): inputs [128 it, 128 it + 128), outputs of slab sl, rows of chunk c. Lane l
+// Block (c, it, sl): inputs [128 it, 128 it + 128), outputs of slab sl, rows of chunk c. Lane l
 // holds inputs 128 it + l and 128 it + 64 + l, so one record read, conversion and address serve
 // two float64 LDS atomics (the second at an immediate offset): on this hardware the VALU work of
 // an atomic adds to its LDS time instead of overlapping it. Blocks of one chunk are numbered so
@@ -201,8 +201,8 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   if ((nb & 7) == 0) id = (id & 7) * (nb >> 3) + (id >> 3);
   const int tiles = n_itiles * n_slabs;
   const int c = id / tiles;
-  const int it = (id - c * tiles) % n_itiles;
-  const int sl = (id - c * tiles) / n_itiles;
+  const int sl = (id - c * tiles) % n_slabs;  // the slabs of one input tile run side by side and
+  const int it = (id - c * tiles) / n_slabs;  // read the same trace slices (L2 hits)
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int l = tid % kWave;
