@@ -316,7 +316,7 @@ def main():
     snn.lib()
     cfg = CONFIGS[args.workload]
     run = Runner(cfg, args)
-    points = cfg.sweep if args.sweep else (cfg.b_th if args.b_th is None else args.b_th,)
+    points = cfg.sweep() if args.sweep else (cfg.b_th if args.b_th is None else args.b_th,)
     dense_ms = None
     for k, b_th in enumerate(points):
         run.prepare(b_th)

@@ -88,7 +88,7 @@ CONFIGS = {
         description="700 channels, Poisson spikes under a smooth channel x time envelope (SHD-like), LIF 700->400, readout 400->20"),
     "stress": Config(
         "stress", 5, T=500, B=256, sizes=(1024, 1024, 1024, 1024, 100), tau_ratio_hidden=0.1, tau_ratio_out=0.1,
-        loss_mode="max", b_th=0.2, b_th_sweep=(0.02, 0.05, 0.1, 0.2, 0.35, 0.5, 0.8), kind="bernoulli", rate=0.02,
+        loss_mode="max", b_th=0.2, b_th_sweep=(0.02, 0.05, 0.1, 0.2, 0.35, 0.5, 0.8, 1.2), kind="bernoulli", rate=0.02,
         description="3 LIF layers 1024->1024, readout 1024->100, T=500, B=256, Bernoulli(0.02)"),
 }
 
