@@ -221,22 +221,36 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   const int r_lo = c * rows_per_chunk;
   const int r_hi = min(TB, r_lo + rows_per_chunk);
   const int2* rec2 = reinterpret_cast<const int2*>(rec);
-  for (int rb = r_lo + w * kRowsPerBatch; rb < r_hi; rb += kDwWaves * kRowsPerBatch) {
-    // every load of the batch is issued before any is used (indices clamped into range; rows
-    // past r_hi read sp[r_hi], so their entry ranges are empty)
-    const int spv = spl[min(rb + min(l, kRowsPerBatch), r_hi)];
-    float tr0[kRowsPerBatch], tr1[kRowsPerBatch];
+  // Software pipeline over batches of 8 rows: while a batch is processed, the next batch's
+  // trace values and records are in flight and the row pointers of the one after it. Rows past
+  // r_hi read sp[r_hi] (empty ranges); a row with no entry in this slab reads the chunk's first
+  // trace row instead of its own (a cache hit, never used).
+  auto load_sp = [&](int rb) { return spl[min(rb + min(l, kRowsPerBatch), r_hi)]; };
+  auto load_rest = [&](int rb, int spv, float* t0, float* t1, int2& ra) {
 #pragma unroll
     for (int k = 0; k < kRowsPerBatch; ++k) {
-      const size_t row = (size_t)min(rb + k, r_hi - 1) * N_in;
-      tr0[k] = trace[row + ic0];
-      tr1[k] = trace[row + ic1];
+      const bool any = rdlane(spv, k + 1) > rdlane(spv, k);
+      const size_t row = (size_t)(any ? min(rb + k, r_hi - 1) : r_lo) * N_in;
+      t0[k] = trace[row + ic0];
+      t1[k] = trace[row + ic1];
     }
+    ra = rec2[min((int64_t)rdlane(spv, 0) + l, nrec - 1)];  // lane s holds the batch's record s
+  };
+  constexpr int kStride = kDwWaves * kRowsPerBatch;
+  int rb = r_lo + w * kRowsPerBatch;
+  int spv = load_sp(rb);
+  float tr0[kRowsPerBatch], tr1[kRowsPerBatch];
+  int2 ra;
+  load_rest(rb, spv, tr0, tr1, ra);
+  int spv_n = load_sp(rb + kStride);
+  for (; rb < r_hi; rb += kStride) {
+    float tn0[kRowsPerBatch], tn1[kRowsPerBatch];
+    int2 ran;
+    load_rest(rb + kStride, spv_n, tn0, tn1, ran);
+    const int spv_nn = load_sp(rb + 2 * kStride);
     __builtin_amdgcn_sched_barrier(0);
     const int base = rdlane(spv, 0);
     const int n = rdlane(spv, kRowsPerBatch) - base;
-    const int2 ra = rec2[min((int64_t)base + l, nrec - 1)];  // lane s holds the batch's record s
-    __builtin_amdgcn_sched_barrier(0);
     if (n <= kWave) {  // common case: the batch's records are all in one register
       int lo = 0;
 #pragma unroll
@@ -266,6 +280,14 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
           atomicAdd(a + kWave, t1 * G);
         }
       }
+    }
+    spv = spv_n;
+    spv_n = spv_nn;
+    ra = ran;
+#pragma unroll
+    for (int k = 0; k < kRowsPerBatch; ++k) {
+      tr0[k] = tn0[k];
+      tr1[k] = tn1[k];
     }
   }
   __syncthreads();

@@ -292,3 +292,65 @@ def test_split_calls_match_combined(name, batch, b_th):
             n = csrs[l - 1].nnz()
             assert torch.equal(eps_in[:n], g["eps"][l - 1][:n]), f"eps[{l - 1}]"  # fixed order: bit-equal
             eps = eps_in
+
+
+def test_full_size_stress_sampled():
+    """The stress workload at full size (T=500, B=256, 3 x 1024) in the bench's launch
+    configuration (spike gradient on an auxiliary stream beside dW). Samples are independent in
+    the forward, compaction and spike gradient, so for sampled b the oracle run on sample b alone
+    (its loss gradient scaled by 1/B) is exact: V, spikes, traces and CSR rows bit-exact, eps of
+    every layer within the envelope. dW sums over all samples: checked against the dense matrix-core
+    path of the same truncated gradient (validated against the oracle on the smaller cases)."""
+    cfg = CONFIGS["stress"]
+    b_th = cfg.b_th
+    print(f"\n[case] full-size stress b_th={b_th}", flush=True)
+    inp = make_inputs(cfg)
+    net = pipeline.from_inputs(inp).forward()
+    ro = net.readout(dense=True)
+    csrs = net.compact(b_th)
+    T, B, L = net.T, net.B, net.L
+    main = torch.cuda.current_stream()
+    aux = torch.cuda.Stream()
+    _, eps = snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, ro[0], ro[1], inp=csrs[L - 1],
+                                 aux_stream=aux)
+    eps_l, dW = [None] * L, [None] * L
+    for l in range(L - 1, -1, -1):
+        eps_l[l] = eps
+        n_in, n_out = net.Ws[l].shape
+        if l > 0:
+            share = 3.0 * csrs[l].capacity * n_in >= 2.0 * csrs[l - 1].capacity * n_out
+            aux.wait_stream(main)
+            eps_in = snn.sparse_grad_in(net.Ws[l], net.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=share,
+                                        stream=aux)
+        dW[l] = snn.sparse_dw(net.trace[l], csrs[l], eps, n_out, stream=main)
+        if l > 0:
+            main.wait_stream(aux)
+            eps = eps_in
+    ddW, _, _ = net.dense_backward(b_th, ro)
+    torch.cuda.synchronize()
+
+    for b in (0, 137, 255):
+        sub = make_inputs(cfg, [b])
+        f = oracle.network_forward(sub.X, sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, np.float32(cfg.theta))
+        args = (sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, sub.labels, cfg.loss_mode, cfg.theta, b_th, cfg.beta)
+        r = oracle.network_backward(f, *args)
+        env = oracle.network_backward(f, *args, absolute=True)
+        for l in range(L):
+            assert_bits(_np(net.V[l][:, b]), f["V"][l][:, 0], f"V[{l}] b={b}")
+            assert_bits(_np(net.S[l][:, b]), f["S"][l][:, 0], f"S[{l}] b={b}")
+            assert_bits(_np(net.trace[l][:, b]), f["trace"][l][:, 0], f"trace[{l}] b={b}")
+            rp = _np(csrs[l].row_ptr).astype(np.int64)
+            rows = np.arange(T) * B + b
+            lo, hi = rp[rows], rp[rows + 1]
+            ref_rp, ref_ci, _ = oracle.active_csr(f["V"][l], cfg.theta, b_th, cfg.beta)
+            assert_bits(hi - lo, np.diff(ref_rp).astype(np.int64), f"row counts[{l}] b={b}")
+            idx = np.concatenate([np.arange(a, z) for a, z in zip(lo, hi)]).astype(np.int64)
+            col = _np(csrs[l].col_idx)[idx].astype(np.int64)
+            assert_bits(col, ref_ci.astype(np.int64), f"col_idx[{l}] b={b}")
+            t_of = np.repeat(np.arange(T), hi - lo)
+            got = _np(eps_l[l])[idx].astype(F64)
+            assert_env(got, r["eps"][l][t_of, 0, col] / B, env["eps"][l][t_of, 0, col] / B, f"eps[{l}] b={b}")
+    for l in range(L):
+        x, y = _np(dW[l]).astype(F64), _np(ddW[l]).astype(F64)
+        bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
+        assert not bad.any(), f"dW[{l}]: {int(bad.sum())} elements differ from the dense path"
