@@ -192,6 +192,23 @@ class Runner:
             E("dn1").record(main)
         return cs
 
+    def memory(self, nnz):
+        """Per LIF layer: bytes each backward chain allocates beyond the shared forward state, and
+        the memory saved, 100 (dense - sparse) / dense (Eq. (memory_saved))."""
+        snn, T, B, L, sizes = self.snn, self.T, self.B, self.L, self.sizes
+        TB = T * B
+        out = []
+        for l in range(L):
+            n_in, n_out = sizes[l], sizes[l + 1]
+            sparse = 4 * (TB + 1) + 12 * nnz[l] + 4 * n_in * n_out  # CSR (index, g), eps, dW
+            sparse += snn.snn_sparse_dw_workspace(T, B, n_in, n_out, nnz[l])
+            dense = 4 * TB * n_out + 4 * n_in * n_out + snn.snn_dense_backward_workspace(T, B, n_in, n_out)
+            if l > 0:
+                sparse += 4 * nnz[l - 1] + snn.snn_sparse_grad_in_workspace(T, B, n_out)
+                dense += 4 * TB * n_in
+            out.append((sparse, dense, 100.0 * (dense - sparse) / dense))
+        return out
+
     def events(self):
         mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
         ev = {k: mk() for k in ("fwd0", "fwd1", "cmp0", "cmp1", "ro1", "dn0", "dn1")}
@@ -241,6 +258,7 @@ class Runner:
         dw_s = sum(dw_ms) * 1e-3
         achieved = dw_flops / dw_s / 1e12
         value = sum(nnz) / (med(t_sparse) * 1e-3)
+        mem = self.memory(nnz)
         traffic = None
         if os.path.exists(TRAFFIC_FILE):
             with open(TRAFFIC_FILE) as f:
@@ -271,6 +289,8 @@ class Runner:
             "dense_backward_ms": med(span("dn0", "dn1")) if dense and not self.args.no_dense else None,
             "forward_ms": med(t_fwd),
             "active_fraction": [n / (T * B * sizes[l + 1]) for l, n in enumerate(nnz)],
+            "memory_saved_pct": [m[2] for m in mem],
+            "backward_bytes_sparse_dense": [[m[0], m[1]] for m in mem],
             "nnz": nnz,
             "roofline": {
                 "bound": "alu", "achieved": achieved, "peak": LDS_F64_RMW_TFLOPS, "unit": "TFLOP/s",

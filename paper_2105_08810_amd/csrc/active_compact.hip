@@ -20,6 +20,7 @@ namespace {
 constexpr int kRowsPerBlock = 4;  // one wavefront per row
 constexpr int kThreads = kRowsPerBlock * kWave;
 constexpr int kStage = 64;  // staged entries per row
+constexpr int kGroup = 4;   // 256-wide slices of a row loaded together
 
 struct Staged {
   int32_t j;
@@ -44,25 +45,33 @@ __global__ __launch_bounds__(kThreads) void compact_count(const float* __restric
   Staged* st = stage + (size_t)r * scap;
   int base = 0;
   if (VEC) {
-    // lane l holds elements 4l..4l+3 of each 256-wide slice; ascending order is (lane, q)
-    for (int j0 = 0; j0 < N; j0 += 4 * kWave) {
-      const int j = j0 + 4 * l;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (j < N) v = *reinterpret_cast<const float4*>(row + j);
-      const float vv[4] = {v.x, v.y, v.z, v.w};
-      bool a[4];
+    // lane l holds elements 4l..4l+3 of each 256-wide slice; ascending order is (lane, q). The
+    // slices of a 1024-wide group are loaded together before any is used.
+    for (int g0 = 0; g0 < N; g0 += kGroup * 4 * kWave) {
+      float4 v[kGroup];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) a[q] = (j < N) && is_active(vv[q], theta, bth);
-      const uint64_t m0 = __ballot(a[0]), m1 = __ballot(a[1]), m2 = __ballot(a[2]), m3 = __ballot(a[3]);
-      int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (a[q]) {
-          if (pos < scap) st[pos] = Staged{j + q, surrogate(vv[q], theta, beta)};
-          ++pos;
-        }
+      for (int c = 0; c < kGroup; ++c) {
+        const int j = g0 + c * 4 * kWave + 4 * l;
+        v[c] = j < N ? *reinterpret_cast<const float4*>(row + j) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
-      base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+#pragma unroll
+      for (int c = 0; c < kGroup; ++c) {
+        const int j = g0 + c * 4 * kWave + 4 * l;
+        const float vv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+        bool a[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a[q] = (j < N) && is_active(vv[q], theta, bth);
+        const uint64_t m0 = __ballot(a[0]), m1 = __ballot(a[1]), m2 = __ballot(a[2]), m3 = __ballot(a[3]);
+        int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (a[q]) {
+            if (pos < scap) st[pos] = Staged{j + q, surrogate(vv[q], theta, beta)};
+            ++pos;
+          }
+        }
+        base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+      }
     }
   } else {
     for (int j0 = 0; j0 < N; j0 += kWave) {

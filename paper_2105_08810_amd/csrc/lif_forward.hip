@@ -22,7 +22,7 @@ constexpr int kGatherWaves = 4;        // wavefronts (rows) per gather block
 constexpr int kPiece = 4 * kWave;      // inputs per ballot piece (4 bytes per lane)
 constexpr int kSegPieces = 4;          // pieces whose spike bytes are loaded together
 constexpr int kScanThreads = 256;
-constexpr int kScanAhead = 16;         // time steps loaded ahead in the scans
+constexpr int kScanAhead = 32;         // time steps loaded ahead in the scans
 
 template <bool ALIGNED>
 __device__ __forceinline__ uint32_t load4(const uint8_t* p, int i, int n) {
