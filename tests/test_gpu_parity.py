@@ -354,3 +354,21 @@ def test_full_size_stress_sampled():
         x, y = _np(dW[l]).astype(F64), _np(ddW[l]).astype(F64)
         bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
         assert not bad.any(), f"dW[{l}]: {int(bad.sum())} elements differ from the dense path"
+
+
+def _wide(hidden, n_in, n_ro, T=8, B=2):
+    sizes = (n_in, *hidden, n_ro)
+    cfg = Config(f"wide{'x'.join(map(str, hidden))}", 204, T=T, B=B, sizes=sizes, tau_ratio_hidden=0.1,
+                 tau_ratio_out=0.1, loss_mode="max", b_th=0.4, kind="bernoulli", rate=0.3)
+    rates = [0.3] + [0.2] * len(hidden)  # input rate, then about the hidden spike rate
+    sig = [1.2 / math.sqrt(r * n) for r, n in zip(rates, sizes[:-2])] + [1 / math.sqrt(sizes[-2])]
+    return make_inputs(cfg, sigmas=sig)
+
+
+@pytest.mark.parametrize("hidden,n_in,n_ro", [((2000, 4096), 48, 3), ((1500,), 40, 1100), ((700, 3000), 33, 7)])
+def test_parity_wide_layers(hidden, n_in, n_ro):
+    """Wide layers: the forward's 8- and 16-group gathers, the spike gradient's 32- and 64-group
+    walks (LIF to LIF with 4096 outputs, a 1100-class readout), unaligned widths."""
+    inp = _wide(hidden, n_in, n_ro)
+    print(f"\n[case] wide {n_in}->{hidden}->{n_ro}", flush=True)
+    check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
