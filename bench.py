@@ -135,6 +135,7 @@ class Runner:
         """Size compaction outputs and workspaces for one band (the first compaction counts)."""
         snn, T, B, L, sizes = self.snn, self.T, self.B, self.L, self.sizes
         self.b_th = b_th
+        self.net.forward(None if self.args.unfused else b_th)
         csrs = self.net.compact(b_th)
         self.caps = [c.capacity for c in csrs]
         self.ws_dw = [snn.workspace(snn.snn_sparse_dw_workspace(T, B, sizes[l], sizes[l + 1], self.caps[l]))
@@ -153,7 +154,7 @@ class Runner:
         main, aux = self.main, self.aux
         E = lambda k: ev[k]  # noqa: E731
         E("fwd0").record(main)
-        net.forward()
+        net.forward(None if self.args.unfused else self.b_th)
         E("fwd1").record(main)
         r = net.readout(dense=dense and not self.args.no_dense)
         E("cmp0").record(main)
@@ -245,7 +246,7 @@ class Runner:
         t_gi = [np.array([e["gi0"][i].elapsed_time(e["gi1"][i]) for e in evs]) for i in range(L - 1)]
         t_cmp = span("cmp0", "cmp1")
         t_sparse = t_cmp + sum(t_layers)
-        t_step = np.array([e["fwd0"].elapsed_time(e["dn1" if dense and not self.args.no_dense else "ro1"])
+        t_step = np.array([e["fwd0"].elapsed_time(e["dn1"] if dense and not self.args.no_dense else e["lay1"][L - 1])
                            for e in evs])
 
         nnz = [c.nnz() for c in cs]
@@ -279,7 +280,8 @@ class Runner:
             "dtype": "f32",
             "data": "synthetic",
             "config": {"workload": f"{cfg.name}: {cfg.description}; B_th={self.b_th}", "T": T, "B": B,
-                       "sizes": sizes, "b_th": self.b_th, "alpha": float(cfg.alpha), "beta": cfg.beta},
+                       "sizes": sizes, "b_th": self.b_th, "alpha": float(cfg.alpha), "beta": cfg.beta,
+                       "compaction": "from V" if self.args.unfused else "from the forward's active bitsets"},
             "sparse_backward_ms": med(t_sparse),
             "sparse_backward_ms_iqr": [float(np.percentile(t_sparse, 25)), float(np.percentile(t_sparse, 75))],
             "compaction_ms": med(t_cmp),
@@ -320,6 +322,8 @@ def main():
     ap.add_argument("--cpu-samples", type=int, default=16)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--serial", action="store_true", help="everything on one stream")
+    ap.add_argument("--unfused", action="store_true",
+                    help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
     args = ap.parse_args()

@@ -74,6 +74,20 @@ snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T, int B, in
                            void* stream);
 
 /*
+ * The forward with the active set of Definition 1 marked on the way (the band test runs on each
+ * V value while it is in a register, so compaction need not read V again).
+ *   b_th         backprop band; bit (t,b,j) is set iff |V[t,b,j] - theta| < b_th, in float32
+ *                exactly as snn_active_compact evaluates it
+ *   active_bits  uint64 bitset of snn_active_bits_words(T,B,N_out) words (written): bit (t, k),
+ *                k = b*N_out + j, is bit k % 64 of word t*W64 + k/64, W64 = ceil(B*N_out/64)
+ * Everything else as snn_lif_forward. NaN or negative b_th -> SNN_ERR_INVALID_ARG.
+ */
+size_t snn_active_bits_words(int T, int B, int N);
+snn_status snn_lif_forward_active(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
+                                  float alpha, float theta, float b_th, float* V, uint8_t* s_out,
+                                  float* trace_in, uint64_t* active_bits, void* stream);
+
+/*
  * Active-set compaction (Definition 1) with the truncated spike derivative (Definition 2).
  *   V        [T,B,N] float32 (read)
  *   active   |V - theta| < b_th in float32, strictly (b_th = +INFINITY: every finite V)
@@ -89,6 +103,18 @@ size_t snn_active_compact_workspace(int T, int B, int N);
 snn_status snn_active_compact(const float* V, int T, int B, int N, float theta, float b_th, float beta,
                               int32_t* row_ptr, int32_t* col_idx, float* g_act, int64_t capacity,
                               int64_t* nnz_dev, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Compaction from the bitset of snn_lif_forward_active: the same CSR as snn_active_compact with
+ * the band used for the bitset (row_ptr, col_idx ascending, g_act = 1/(beta|V-theta|+1)^2 read
+ * from V at the active entries only). V may be NULL when g_act is NULL. Capacity, nnz and
+ * overflow behave as in snn_active_compact.
+ */
+size_t snn_active_compact_bits_workspace(int T, int B, int N);
+snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, int T, int B, int N,
+                                   float theta, float beta, int32_t* row_ptr, int32_t* col_idx,
+                                   float* g_act, int64_t capacity, int64_t* nnz_dev, void* workspace,
+                                   size_t workspace_bytes, void* stream);
 
 /*
  * Sparse backward of one layer (Sec. 2.2: sparse dW and sparse spike gradient, Proposition 1).

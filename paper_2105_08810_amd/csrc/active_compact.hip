@@ -149,6 +149,119 @@ __global__ __launch_bounds__(kThreads) void compact_fill(const float* __restrict
   }
 }
 
+// ------------------------------------------------------------------ from a bitset
+// Bit (t, k), k = b * N + j, of word t * W64 + k / 64 (W64 = ceil(B N / 64)) marks an active
+// entry (as snn_lif_forward_active writes it). Window w of row (t, b) = row bits [64 w, 64 w + 64).
+__device__ __forceinline__ uint64_t row_window(const uint64_t* __restrict__ bits, size_t W64, int t, size_t bN,
+                                               int N, int w) {
+  const size_t bit0 = bN + (size_t)kWave * w;
+  const size_t wi = bit0 / kWave;
+  const int sh = (int)(bit0 % kWave);
+  const uint64_t* row = bits + (size_t)t * W64;
+  uint64_t x = row[wi] >> sh;
+  if (sh) x |= (wi + 1 < W64 ? row[wi + 1] : 0ull) << (kWave - sh);
+  const int rem = N - kWave * w;
+  if (rem < kWave) x &= (1ull << rem) - 1ull;
+  return x;
+}
+
+// A wavefront takes RPW = 64 / nw rows when a row has nw <= 64 windows (lane l: row l / nw of
+// the wavefront's rows, window l % nw), else one row with the windows walked 64 at a time.
+// Positions inside a row come from a wavefront-wide inclusive scan minus its value just before
+// the row's first lane.
+__global__ __launch_bounds__(kThreads) void bits_count(const uint64_t* __restrict__ bits, int T, int B, int N,
+                                                       int rpw, int32_t* __restrict__ counts) {
+  const int l = lane_id();
+  const int rows = T * B;
+  const int nw = (N + kWave - 1) / kWave;
+  const size_t W64 = ((size_t)B * N + kWave - 1) / kWave;
+  const int r0 = (blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave)) * rpw;
+  if (r0 >= rows) return;
+  if (rpw > 1) {
+    const int k = l / nw, w = l - k * nw;
+    const int r = r0 + k;
+    const bool ok = k < rpw && r < rows;
+    const int c = ok ? __popcll(row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w)) : 0;
+    const int incl = wave_incl_scan(c);
+    const int first = k * nw;  // lane of the row's first window
+    const int before = __shfl(incl, max(first - 1, 0), kWave);  // every lane takes part in the exchange
+    if (ok && w == nw - 1) counts[r] = incl - (first > 0 ? before : 0);
+    return;
+  }
+  const int r = r0;
+  int c = 0;
+  for (int w0 = 0; w0 < nw; w0 += kWave)
+    if (w0 + l < nw) c += __popcll(row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w0 + l));
+  c = wave_sum_int(c);
+  if (l == 0) counts[r] = c;
+}
+
+// Places a lane's set bits of one window at pos, pos + 1, ... (up to four V loads in flight).
+__device__ __forceinline__ void place_window(uint64_t x, int jbase, int64_t pos, const float* __restrict__ vrow,
+                                             float theta, float beta, int32_t* __restrict__ col_idx,
+                                             float* __restrict__ g_act, int64_t cap) {
+  while (__ballot(x != 0ull)) {
+    int jj[4];
+    float vv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      jj[u] = x ? jbase + (__ffsll((long long)x) - 1) : -1;
+      x &= x - 1ull;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) vv[u] = (g_act && jj[u] >= 0) ? vrow[jj[u]] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (jj[u] >= 0) {
+        if (pos < cap) {
+          col_idx[pos] = jj[u];
+          if (g_act) g_act[pos] = surrogate(vv[u], theta, beta);
+        }
+        ++pos;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void bits_fill(const uint64_t* __restrict__ bits, const float* __restrict__ V,
+                                                      int T, int B, int N, int rpw, float theta, float beta,
+                                                      const int32_t* __restrict__ row_ptr,
+                                                      int32_t* __restrict__ col_idx, float* __restrict__ g_act,
+                                                      int64_t cap) {
+  const int l = lane_id();
+  const int rows = T * B;
+  const int nw = (N + kWave - 1) / kWave;
+  const size_t W64 = ((size_t)B * N + kWave - 1) / kWave;
+  const int r0 = (blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave)) * rpw;
+  if (r0 >= rows) return;
+  if (rpw > 1) {
+    const int k = l / nw, w = l - k * nw;
+    const int r = r0 + k;
+    const bool ok = k < rpw && r < rows;
+    const uint64_t x = ok ? row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w) : 0ull;
+    const int64_t dst = ok ? row_ptr[r] : 0;
+    const int c = __popcll(x);
+    const int incl = wave_incl_scan(c);
+    const int first = k * nw;
+    const int prev = __shfl(incl, max(first - 1, 0), kWave);  // every lane takes part in the exchange
+    const int before = first > 0 ? prev : 0;
+    place_window(x, kWave * w, dst + (incl - c - before), V + (size_t)(ok ? r : 0) * N, theta, beta, col_idx, g_act,
+                 cap);
+    return;
+  }
+  const int r = r0;
+  const float* vrow = V + (size_t)r * N;
+  int64_t base = row_ptr[r];
+  for (int w0 = 0; w0 < nw; w0 += kWave) {
+    const int w = w0 + l;
+    const uint64_t x = w < nw ? row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w) : 0ull;
+    const int c = __popcll(x);
+    const int incl = wave_incl_scan(c);
+    place_window(x, kWave * w, base + incl - c, vrow, theta, beta, col_idx, g_act, cap);
+    base += __shfl(incl, kWave - 1, kWave);
+  }
+}
+
 }  // namespace
 }  // namespace snn
 
@@ -197,5 +310,41 @@ extern "C" snn_status snn_active_compact(const float* V, int T, int B, int N, fl
       hipLaunchKernelGGL(compact_fill<false>, grid, dim3(kThreads), 0, s, V, rows, N, theta, b_th, beta, row_ptr,
                          stage, scap, col_idx, g_act, capacity);
   }
+  return launch_status();
+}
+
+extern "C" size_t snn_active_compact_bits_workspace(int T, int B, int N) {
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return 0;
+  const int rows = T * B;
+  Carve c(nullptr);
+  c.take<int32_t>(rows);
+  c.take<int32_t>(scan_temp_elems(rows));
+  return c.off;
+}
+
+extern "C" snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, int T, int B, int N,
+                                              float theta, float beta, int32_t* row_ptr, int32_t* col_idx,
+                                              float* g_act, int64_t capacity, int64_t* nnz_dev, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  if (!active_bits || !row_ptr || !nnz_dev || !workspace) return SNN_ERR_INVALID_ARG;
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return SNN_ERR_INVALID_ARG;
+  if (isnan(theta) || isnan(beta) || beta < 0.0f) return SNN_ERR_INVALID_ARG;
+  if (capacity < 0 || (capacity > 0 && !col_idx) || (g_act && !V)) return SNN_ERR_INVALID_ARG;
+  if (workspace_bytes < snn_active_compact_bits_workspace(T, B, N)) return SNN_ERR_INVALID_ARG;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int rows = T * B;
+  Carve ws(workspace);
+  int32_t* counts = ws.take<int32_t>(rows);
+  int32_t* temp = ws.take<int32_t>(scan_temp_elems(rows));
+  const int nw = (N + kWave - 1) / kWave;
+  const int rpw = nw <= kWave ? kWave / nw : 1;  // rows per wavefront
+  const int waves = (rows + rpw - 1) / rpw;
+  const dim3 grid((waves + kRowsPerBlock - 1) / kRowsPerBlock);
+  hipLaunchKernelGGL(bits_count, grid, dim3(kThreads), 0, s, active_bits, T, B, N, rpw, counts);
+  launch_exclusive_scan(counts, rows, row_ptr, nnz_dev, temp, s);
+  if (capacity > 0)
+    hipLaunchKernelGGL(bits_fill, grid, dim3(kThreads), 0, s, active_bits, V, T, B, N, rpw, theta, beta, row_ptr,
+                       col_idx, g_act, capacity);
   return launch_status();
 }

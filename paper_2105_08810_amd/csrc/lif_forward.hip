@@ -128,34 +128,51 @@ __global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t
 
 // Blocks [0, nv) run the membrane recurrence of B * N_out neurons; blocks [nv, nv + nt) run the
 // trace of B * ceil(N_in / 4) input quads.
+// With bits != NULL the recurrence also marks the active set of Definition 1: bit (t, k) of the
+// bitset, k = b * N_out + j, is |V[t,b,j] - theta| < b_th in float32, word t * W64 + k / 64,
+// W64 = ceil(B * N_out / 64); one ballot per wavefront and step (its 64 k are one word).
+__device__ __forceinline__ void mark_active(uint64_t* bits, size_t word, bool valid, float v, float theta,
+                                            float b_th) {
+  const uint64_t m = __ballot(valid && fabsf(v - theta) < b_th);
+  if (lane_id() == 0) bits[word] = m;
+}
+
 template <bool ALIGNED>
 __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restrict__ s_in, int T, int B, int N_in,
-                                                         int N_out, float alpha, float theta, float* __restrict__ V,
-                                                         uint8_t* __restrict__ s_out, float* __restrict__ trace,
+                                                         int N_out, float alpha, float theta, float b_th,
+                                                         float* __restrict__ V, uint8_t* __restrict__ s_out,
+                                                         float* __restrict__ trace, uint64_t* __restrict__ bits,
                                                          int nv) {
   if ((int)blockIdx.x < nv) {
+    const size_t k0 = (size_t)blockIdx.x * kScanThreads + (threadIdx.x & ~(kWave - 1));
+    if (k0 >= (size_t)B * N_out) return;  // whole wavefront past the end
     const size_t k = (size_t)blockIdx.x * kScanThreads + threadIdx.x;  // b * N_out + j
-    if (k >= (size_t)B * N_out) return;
+    const bool valid = k < (size_t)B * N_out;
+    const size_t kc = valid ? k : k0;  // lanes past the end compute on a valid column, store nothing
     const size_t step = (size_t)B * N_out;
+    const size_t W64 = (step + kWave - 1) / kWave;
+    const size_t wword = k0 / kWave;
     float v = 0.0f;
-    V[k] = 0.0f;
+    if (valid) V[k] = 0.0f;
+    if (bits) mark_active(bits, wword, valid, v, theta, b_th);
     for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
       const int np = min(kScanAhead, T - 1 - t0);
       float in[kScanAhead];
 #pragma unroll
-      for (int p = 0; p < kScanAhead; ++p) in[p] = V[(size_t)(t0 + min(p, np - 1) + 1) * step + k];
+      for (int p = 0; p < kScanAhead; ++p) in[p] = V[(size_t)(t0 + min(p, np - 1) + 1) * step + kc];
 #pragma unroll
       for (int p = 0; p < kScanAhead; ++p) {
         if (p < np) {
           const int t = t0 + p;
           const bool sp = v > theta;
-          s_out[(size_t)t * step + k] = (uint8_t)sp;
+          if (valid) s_out[(size_t)t * step + k] = (uint8_t)sp;
           v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), in[p]), sp ? -1.0f : -0.0f);
-          V[(size_t)(t + 1) * step + k] = v;
+          if (valid) V[(size_t)(t + 1) * step + k] = v;
+          if (bits) mark_active(bits, (size_t)(t + 1) * W64 + wword, valid, v, theta, b_th);
         }
       }
     }
-    s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
+    if (valid) s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
   } else {
     const int nq = (N_in + 3) / 4;
     const size_t k = (size_t)(blockIdx.x - nv) * kScanThreads + threadIdx.x;  // b * nq + quad
@@ -213,13 +230,16 @@ void launch_gather(int NQ, dim3 grid, hipStream_t s, const uint8_t* s_in, const 
 
 using namespace snn;
 
-extern "C" snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
-                                      float alpha, float theta, float* V, uint8_t* s_out, float* trace_in,
-                                      void* stream) {
+namespace {
+
+snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out, float alpha,
+                            float theta, float b_th, float* V, uint8_t* s_out, float* trace_in, uint64_t* bits,
+                            void* stream) {
   if (!s_in || !W || !V || !s_out) return SNN_ERR_INVALID_ARG;
   if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out)) return SNN_ERR_INVALID_ARG;
   if (too_big(T, B, N_in) || too_big(T, B, N_out)) return SNN_ERR_INVALID_ARG;
   if (bad_alpha(alpha) || isnan(theta)) return SNN_ERR_INVALID_ARG;
+  if (bits && (isnan(b_th) || b_th < 0.0f)) return SNN_ERR_INVALID_ARG;
   if (N_out > 16 * 4 * kWave) return SNN_ERR_UNSUPPORTED;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -240,9 +260,29 @@ extern "C" snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T
   const bool tal = al && (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0;
   if (tal)
     hipLaunchKernelGGL(lif_scan<true>, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out,
-                       alpha, theta, V, s_out, trace_in, nv);
+                       alpha, theta, b_th, V, s_out, trace_in, bits, nv);
   else
     hipLaunchKernelGGL(lif_scan<false>, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out,
-                       alpha, theta, V, s_out, trace_in, nv);
+                       alpha, theta, b_th, V, s_out, trace_in, bits, nv);
   return launch_status();
+}
+
+}  // namespace
+
+extern "C" snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
+                                      float alpha, float theta, float* V, uint8_t* s_out, float* trace_in,
+                                      void* stream) {
+  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, 0.0f, V, s_out, trace_in, nullptr, stream);
+}
+
+extern "C" size_t snn_active_bits_words(int T, int B, int N) {
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return 0;
+  return (size_t)T * (((size_t)B * N + kWave - 1) / kWave);
+}
+
+extern "C" snn_status snn_lif_forward_active(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
+                                             float alpha, float theta, float b_th, float* V, uint8_t* s_out,
+                                             float* trace_in, uint64_t* active_bits, void* stream) {
+  if (!active_bits) return SNN_ERR_INVALID_ARG;
+  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, active_bits, stream);
 }

@@ -35,6 +35,8 @@ class Network:
     V_out: Optional[torch.Tensor] = None
     S_out: Optional[torch.Tensor] = None
     trace_out: Optional[torch.Tensor] = None
+    bits: List[torch.Tensor] = field(default_factory=list)  # active bitsets of the LIF layers
+    bits_bth: Optional[float] = None
 
     @property
     def T(self):
@@ -62,14 +64,24 @@ class Network:
         self.trace_out = torch.empty((T, B, sizes[-1]), dtype=torch.float32, device=dev)
         return self
 
-    def forward(self):
+    def forward(self, b_th: Optional[float] = None):
+        """Forward of every layer. With b_th, the LIF layers also mark their active sets (bitsets
+        that compact() then turns into CSR without reading V again)."""
         if not self.V:
             self.allocate()
         x = self.X
         T, B = self.T, self.B
+        if b_th is not None and not self.bits:
+            self.bits = [torch.empty(snn.snn_active_bits_words(T, B, W.shape[1]), dtype=torch.int64,
+                                     device=self.X.device) for W in self.Ws]
+        self.bits_bth = b_th
         for l, W in enumerate(self.Ws):
-            snn.snn_lif_forward(x, W, T, B, W.shape[0], W.shape[1], self.alphas[l], self.theta, self.V[l],
-                                self.S[l], self.trace[l])
+            if b_th is None:
+                snn.snn_lif_forward(x, W, T, B, W.shape[0], W.shape[1], self.alphas[l], self.theta, self.V[l],
+                                    self.S[l], self.trace[l])
+            else:
+                snn.snn_lif_forward_active(x, W, T, B, W.shape[0], W.shape[1], self.alphas[l], self.theta, b_th,
+                                           self.V[l], self.S[l], self.trace[l], self.bits[l])
             x = self.S[l]
         snn.snn_lif_forward(x, self.W_out, T, B, self.W_out.shape[0], self.W_out.shape[1], self.alpha_out, INF,
                             self.V_out, self.S_out, self.trace_out)
@@ -80,7 +92,12 @@ class Network:
         return snn.readout_ce(self.V_out, self.labels, self.loss_mode, dense=dense)
 
     def compact(self, b_th, capacities: Optional[List[int]] = None) -> List[snn.Csr]:
+        """CSR of every LIF layer's active set: from the forward's bitsets when they were marked
+        with this b_th, else from V."""
         caps = capacities or [None] * self.L
+        if self.bits and self.bits_bth == b_th:
+            return [snn.active_compact_bits(self.bits[l], self.V[l], self.theta, self.beta, caps[l])
+                    for l in range(self.L)]
         return [snn.active_compact(self.V[l], self.theta, b_th, self.beta, caps[l]) for l in range(self.L)]
 
     def sparse_backward(self, csrs: List[snn.Csr], ro=None, aux_stream=None, workspaces=None):

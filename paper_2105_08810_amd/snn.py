@@ -35,6 +35,10 @@ _SIGNATURES = {
     "snn_sparse_backward_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_backward": (_I, [_P, _P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _P, _P, _SZ,
                                  _P, _P]),
+    "snn_active_bits_words": (_SZ, [_I, _I, _I]),
+    "snn_lif_forward_active": (_I, [_P, _P, _I, _I, _I, _I, _F, _F, _F, _P, _P, _P, _P, _P]),
+    "snn_active_compact_bits_workspace": (_SZ, [_I, _I, _I]),
+    "snn_active_compact_bits": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_dw": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_sparse_grad_in_workspace": (_SZ, [_I, _I, _I]),
@@ -107,6 +111,31 @@ def snn_lif_forward(s_in, W, T, B, N_in, N_out, alpha, theta, V, s_out, trace_in
         _ptr(s_in, torch.uint8, "s_in"), _ptr(W, torch.float32, "W"), T, B, N_in, N_out, float(alpha), float(theta),
         _ptr(V, torch.float32, "V"), _ptr(s_out, torch.uint8, "s_out"), _ptr(trace_in, torch.float32, "trace_in"),
         _stream(stream)))
+
+
+def snn_active_bits_words(T, B, N) -> int:
+    return int(lib().snn_active_bits_words(T, B, N))
+
+
+def snn_lif_forward_active(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, active_bits,
+                           stream=None):
+    _check("snn_lif_forward_active", lib().snn_lif_forward_active(
+        _ptr(s_in, torch.uint8, "s_in"), _ptr(W, torch.float32, "W"), T, B, N_in, N_out, float(alpha), float(theta),
+        float(b_th), _ptr(V, torch.float32, "V"), _ptr(s_out, torch.uint8, "s_out"),
+        _ptr(trace_in, torch.float32, "trace_in"), _ptr(active_bits, torch.int64, "active_bits"), _stream(stream)))
+
+
+def snn_active_compact_bits_workspace(T, B, N) -> int:
+    return int(lib().snn_active_compact_bits_workspace(T, B, N))
+
+
+def snn_active_compact_bits(active_bits, V, T, B, N, theta, beta, row_ptr, col_idx, g_act, capacity, nnz_dev, ws,
+                            stream=None):
+    _check("snn_active_compact_bits", lib().snn_active_compact_bits(
+        _ptr(active_bits, torch.int64, "active_bits"), _ptr(V, torch.float32, "V"), T, B, N, float(theta),
+        float(beta), _ptr(row_ptr, torch.int32, "row_ptr"), _ptr(col_idx, torch.int32, "col_idx"),
+        _ptr(g_act, torch.float32, "g_act"), int(capacity), _ptr(nnz_dev, torch.int64, "nnz"),
+        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def snn_active_compact_workspace(T, B, N) -> int:
@@ -228,6 +257,24 @@ def active_compact(V: torch.Tensor, theta, b_th, beta, capacity: Optional[int] =
     col = torch.empty(cap, dtype=torch.int32, device=dev)
     g = torch.empty(cap, dtype=torch.float32, device=dev) if with_g else None
     snn_active_compact(V, T, B, N, theta, b_th, beta, row_ptr, col, g, cap, nnz, ws)
+    return Csr(row_ptr, col, g, nnz, cap)
+
+
+def active_compact_bits(bits: torch.Tensor, V: torch.Tensor, theta, beta, capacity: Optional[int] = None,
+                        with_g=True) -> Csr:
+    """Allocate and run snn_active_compact_bits. Without a capacity it first counts (one host sync)."""
+    T, B, N = V.shape
+    dev = V.device
+    ws = workspace(snn_active_compact_bits_workspace(T, B, N), dev)
+    row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device=dev)
+    nnz = torch.empty(1, dtype=torch.int64, device=dev)
+    if capacity is None:
+        snn_active_compact_bits(bits, V, T, B, N, theta, beta, row_ptr, None, None, 0, nnz, ws)
+        capacity = int(nnz.item())
+    cap = max(int(capacity), 1)
+    col = torch.empty(cap, dtype=torch.int32, device=dev)
+    g = torch.empty(cap, dtype=torch.float32, device=dev) if with_g else None
+    snn_active_compact_bits(bits, V, T, B, N, theta, beta, row_ptr, col, g, cap, nnz, ws)
     return Csr(row_ptr, col, g, nnz, cap)
 
 

@@ -177,3 +177,37 @@ def test_split_workspaces(lib):
     assert dw > 0 and gi > 0
     assert lib.snn_sparse_backward_workspace(500, 256, 1024, 1024, 10 ** 6) >= dw + gi
     assert lib.snn_sparse_grad_in_workspace(0, 256, 1024) == 0
+
+
+def test_fused_forward_rejects(lib):
+    f = lambda **kw: lib.snn_lif_forward_active(  # noqa: E731
+        kw.get("s", FAKE), FAKE, 10, 4, 32, 16, 0.9, 1.0, kw.get("b", 0.2), FAKE, FAKE, FAKE, kw.get("bits", FAKE),
+        None)
+    assert f(bits=None) == snn.SNN_ERR_INVALID_ARG
+    assert f(b=NAN) == snn.SNN_ERR_INVALID_ARG
+    assert f(b=-0.5) == snn.SNN_ERR_INVALID_ARG
+    assert f(s=None) == snn.SNN_ERR_INVALID_ARG
+    assert lib.snn_active_bits_words(10, 4, 16) == 10  # ceil(4 * 16 / 64) words per step
+    assert lib.snn_active_bits_words(3, 5, 100) == 3 * 8
+    assert lib.snn_active_bits_words(0, 5, 100) == 0
+
+
+def _cb(lib, **kw):
+    a = dict(bits=FAKE, V=FAKE, T=10, B=4, N=16, theta=1.0, beta=100.0, rp=FAKE, ci=FAKE, g=FAKE, cap=100, nnz=FAKE,
+             ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return lib.snn_active_compact_bits(a["bits"], a["V"], a["T"], a["B"], a["N"], a["theta"], a["beta"], a["rp"],
+                                       a["ci"], a["g"], a["cap"], a["nnz"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(bits=None), dict(rp=None), dict(nnz=None), dict(ws=None), dict(ws_bytes=4),
+                                dict(cap=-1), dict(ci=None), dict(V=None), dict(beta=NAN), dict(N=0)])
+def test_compact_bits_rejects(lib, kw):
+    assert _cb(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_compact_bits_v_optional_without_g(lib):
+    # V may be NULL when no g is asked for: validation passes that point and fails on the
+    # (deliberately) missing workspace instead
+    assert _cb(lib, V=None, g=None, ws=None) == snn.SNN_ERR_INVALID_ARG
+    assert lib.snn_active_compact_bits_workspace(10, 4, 16) > 0

@@ -372,3 +372,48 @@ def test_parity_wide_layers(hidden, n_in, n_ro):
     inp = _wide(hidden, n_in, n_ro)
     print(f"\n[case] wide {n_in}->{hidden}->{n_ro}", flush=True)
     check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
+
+
+@pytest.mark.parametrize("name,b_th", [("tiny", 0.2), ("tiny", math.inf), ("latency", 0.2), ("event", 0.05),
+                                       ("audio", 0.2), ("ragged", 0.3), ("ragged_sum", 0.25), ("wide", 0.4),
+                                       ("stress8", 0.02), ("stress8", 0.8)])
+def test_fused_active_bits(name, b_th):
+    """Active sets marked by the forward, compacted from the bitsets: CSR bit-exact against the
+    oracle and g bit-equal to the compaction that reads V; V and spikes unchanged."""
+    inp = {"ragged": _ragged, "ragged_sum": _ragged_sum, "wide": lambda: _wide((700, 3000), 33, 7),
+           "stress8": lambda: _case("stress", list(range(8)))}.get(name, lambda: _case(name))()
+    cfg = inp.cfg
+    print(f"\n[case] fused bits {cfg.name} b_th={b_th}", flush=True)
+    f = oracle.network_forward(inp.X, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, np.float32(cfg.theta))
+    net = pipeline.from_inputs(inp).forward(b_th)
+    fused = net.compact(b_th)
+    plain = [snn.active_compact(net.V[l], net.theta, b_th, net.beta) for l in range(net.L)]
+    torch.cuda.synchronize()
+    for l in range(net.L):
+        assert_bits(_np(net.V[l]), f["V"][l], f"V[{l}]")
+        rp, ci, g = oracle.active_csr(f["V"][l], cfg.theta, b_th, cfg.beta)
+        n = fused[l].nnz()
+        assert n == int(rp[-1])
+        assert_bits(_np(fused[l].row_ptr).astype(np.int64), rp.astype(np.int64), f"row_ptr[{l}]")
+        assert_bits(_np(fused[l].col_idx[:n]).astype(np.int64), ci.astype(np.int64), f"col_idx[{l}]")
+        assert torch.equal(fused[l].g[:n], plain[l].g[:n]), f"g[{l}]"
+
+
+def test_fused_bits_capacity_overflow():
+    inp = _case("latency", list(range(16)))
+    net = pipeline.from_inputs(inp).forward(0.2)
+    V, bits = net.V[0], net.bits[0]
+    T, B, N = V.shape
+    full = snn.active_compact_bits(bits, V, 1.0, 100.0)
+    nnz = full.nnz()
+    cap = nnz // 3
+    col = torch.full((cap + 64,), -7, dtype=torch.int32, device="cuda")
+    gg = torch.full((cap + 64,), -7.0, dtype=torch.float32, device="cuda")
+    row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device="cuda")
+    nnz_dev = torch.empty(1, dtype=torch.int64, device="cuda")
+    ws = snn.workspace(snn.snn_active_compact_bits_workspace(T, B, N))
+    snn.snn_active_compact_bits(bits, V, T, B, N, 1.0, 100.0, row_ptr, col, gg, cap, nnz_dev, ws)
+    torch.cuda.synchronize()
+    assert int(nnz_dev.item()) == nnz
+    assert torch.equal(col[:cap], full.col_idx[:cap]) and torch.equal(gg[:cap], full.g[:cap])
+    assert bool((col[cap:] == -7).all()) and bool((gg[cap:] == -7.0).all())
