@@ -42,12 +42,15 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_dw_stress.json")
 CSRC = os.path.join(ROOT, "paper_2105_08810_amd", "csrc")
 
 
+DW_SOURCES = ("common.h", "runtime.hip", "sparse_backward.hip")  # the sources of the dW call's kernels
+
+
 def csrc_digest() -> str:
+    """Digest of the dW call's sources: a traffic record is used only while they are unchanged."""
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(name.encode() + f.read())
+    for name in DW_SOURCES:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
 
 

@@ -49,7 +49,7 @@ DwPlan plan_dw(int T, int B, int N_in, int N_out) {
   p.lds = (size_t)p.slab * kLd * sizeof(double);
   p.n_itiles = (N_in + kItile - 1) / kItile;
   const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(2, (160 * 1024) / p.lds));
-  const int target = kAssumedCUs * per_cu * 2;  // two rounds: the last one evens out
+  const int target = kAssumedCUs * per_cu * 8;  // short chunks: the slab blocks of a tile stay close (L2 reuse)
   const int tiles = p.n_itiles * p.n_slabs;
   int nc = (target + tiles - 1) / tiles;
   nc = std::min(nc, std::max(1, TB / (4 * N_out)));  // partial slabs stay small next to the trace
