@@ -132,7 +132,10 @@ snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, 
  *   dW         [N_in,N_out] float32 (overwritten).
  *   out_cap / in_cap are the allocated lengths of the entry arrays; entries at or beyond them
  *   are ignored, so a CSR whose compaction overflowed its capacity is read safely (and gives
- *   a truncated result). The workspace size depends on out_cap (a slab-major copy of the
+ *   a truncated result). The CSRs are expected as the compaction writes them: row_ptr
+ *   non-decreasing, columns strictly ascending inside a row. Entries with a column outside
+ *   [0, N) are skipped; for other malformed input the results are unspecified, but every memory
+ *   access stays inside the arrays and workspace given (indices are clamped). The workspace size depends on out_cap (a slab-major copy of the
  *   active entries is built in it).
  *   aux_stream (may be NULL): a second hipStream_t. When given, the spike-gradient part runs on
  *   it beside the dW part on `stream`; the call makes aux_stream wait for the work already on
