@@ -273,7 +273,7 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
         const int lo = rdlane(spv, k);
         const int hi = rdlane(spv, k + 1);
         for (int s = lo; s < hi; ++s) {
-          const int2 x = rec2[s];
+          const int2 x = rec2[min((int64_t)s, nrec - 1)];  // clamped: malformed input cannot read past the records
           const double G = (double)__int_as_float(x.y);
           double* a = reinterpret_cast<double*>(accb + min(max(x.x, 0), max_off));
           atomicAdd(a, t0 * G);
