@@ -23,11 +23,17 @@ What it computes, and where the paper defines it:
   O1 literal sums, O2 memoised delta + BLAS (production), O3 event driven
   (Proposition 1 skip recurrence with the App. C schedule), plus operation
   counts (Table 1, App. B).
+* regularize.py -- the activity penalties of App. E and their gradient w.r.t.
+  spike counts.
+* adam.py     -- the Adam update (App. E's optimiser; Kingma and Ba, Algorithm 1).
+* train.py    -- a whole training step (loss with penalties, gradient, Adam) and
+  the sparse vs full-surrogate gradient difference of App. H.
 * smooth.py   -- a smoothed-surrogate model whose exact gradient is the
   truncated-surrogate BPTT gradient; finite differences of it pin O2.
 
 Parity status: every function here is pinned by tests in tests/test_oracle_*.py
-(closed forms, finite differences, autograd, limits, the App. C example).
+(closed forms, finite differences, autograd, limits, the App. C example,
+torch.optim.Adam).
 The paper's experimental numbers themselves are parity unpinned: they need the
 datasets, trained weights or the authors' GPUs.
 """
@@ -38,3 +44,6 @@ from .backward import (  # noqa: F401
     delta_recurrence, layer_backward, network_backward, layer_backward_literal,
     layer_backward_events, skip_delta, csr_values,
 )
+from .regularize import spike_counts, activity_penalty, activity_grad  # noqa: F401
+from .adam import adam_update  # noqa: F401
+from .train import training_gradients, train_step, gradient_difference  # noqa: F401

@@ -66,7 +66,7 @@ def csr_values(dense: np.ndarray, row_ptr: np.ndarray, col_idx: np.ndarray) -> n
 
 
 def network_backward(fwd: dict, Ws, W_out, alphas, alpha_out, labels, mode: str,
-                     theta, b_th, beta, absolute: bool = False):
+                     theta, b_th, beta, absolute: bool = False, reg=None):
     """Gradients of the whole network (O2), top down.
 
     fwd: output of forward.network_forward. With absolute=True every weight is
@@ -74,6 +74,9 @@ def network_backward(fwd: dict, Ws, W_out, alphas, alpha_out, labels, mode: str,
     which yields the magnitude envelope used to state tolerances: every sum and
     difference of the chain taken with its terms in absolute value (traces, alpha
     and g are non-negative already).
+    reg: optional list of [B, N_l] arrays, the derivative of an extra loss term
+    w.r.t. the spike count of each neuron of LIF layer l (regularize.activity_grad);
+    it joins eps[l] at every time step (in absolute value for the envelope).
     Returns dict with
       loss, dLda, readout (the readout_grad dict),
       dW_out, dW[l],
@@ -92,6 +95,9 @@ def network_backward(fwd: dict, Ws, W_out, alphas, alpha_out, labels, mode: str,
     gs = [None] * L
     for l in range(L - 1, -1, -1):
         V = fwd["V"][l]
+        if reg is not None and reg[l] is not None:
+            c = np.asarray(reg[l], F64)[None]
+            eps = eps + (np.abs(c) if absolute else c)
         mask = active_mask(V, theta, b_th)
         g = surrogate(V, theta, beta)
         G = eps * g * mask

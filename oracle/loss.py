@@ -9,7 +9,7 @@ Readings adopted:
   (V_out[0] = 0) takes part;
 * the cross-entropy is the usual negative log-likelihood, mean over the batch
   (the appendix prints it without the minus sign);
-* the activity regularisers of App. E are not part of this path.
+* the activity regularisers of App. E live in regularize.py.
 """
 from __future__ import annotations
 

@@ -19,6 +19,7 @@ from __future__ import annotations
 import numpy as np
 
 from .loss import cross_entropy
+from .regularize import activity_penalty
 
 
 def hard_forward64(X, Ws, W_out, alphas, alpha_out, theta=1.0):
@@ -52,16 +53,21 @@ def s_tilde(v, theta, b_th, beta):
     return np.sign(d) * (1.0 / beta) * (1.0 - 1.0 / (1.0 + beta * a))
 
 
-def smoothed_losses(X, Ws, W_out, alphas, alpha_out, labels, mode, theta, b_th, beta, base, tstar=None):
+def smoothed_losses(X, Ws, W_out, alphas, alpha_out, labels, mode, theta, b_th, beta, base, tstar=None,
+                    reg=None):
     """Loss of M for a stack of P weight sets.
 
     Ws[l] and W_out may be [N_in, N_out] or [P, N_in, N_out]; base is the
     hard_forward64 dict at W0. For mode 'max' the arg-max times tstar [B, C] of
     the base point are used (the max is smooth where the arg-max is unique).
+    reg = (lam_low, nu_low, lam_up, nu_up) adds the activity penalties of every LIF
+    layer, evaluated on the smoothed counts sum_t X_j[t] (a continuous function of W
+    that equals the spike count at W0).
     Returns losses [P].
     """
     x = np.asarray(X != 0, np.float64)[None]  # [1, T, B, N]
     T = x.shape[1]
+    extra = 0.0
     layers = list(zip(Ws, alphas))
     for l, (W, a) in enumerate(layers):
         W = np.asarray(W, np.float64)
@@ -75,6 +81,9 @@ def smoothed_losses(X, Ws, W_out, alphas, alpha_out, labels, mode, theta, b_th, 
         for t in range(T - 1):
             V[:, t + 1] = a * V[:, t] + np.matmul(x[:, t], W) - Sb[:, t]
         x = Sb + s_tilde(V, theta, b_th, beta) - s_tilde(Vb, theta, b_th, beta)
+        if reg is not None:
+            zeta = x.sum(axis=1)  # [P, B, N]
+            extra = extra + activity_penalty(zeta, *reg).mean(axis=-1)
     Wo = np.asarray(W_out, np.float64)
     if Wo.ndim == 2:
         Wo = Wo[None]
@@ -89,4 +98,5 @@ def smoothed_losses(X, Ws, W_out, alphas, alpha_out, labels, mode, theta, b_th, 
         logits = Vo[:, tstar, bb, cc]
     else:
         logits = Vo.sum(axis=1)
-    return np.array([cross_entropy(logits[p], labels)[0] for p in range(P)])
+    ce = np.array([cross_entropy(logits[p], labels)[0] for p in range(P)])
+    return ce + extra
