@@ -18,6 +18,7 @@ speedup are in the same line. Inputs are resident in HBM before timing starts.
     python bench.py [--steps K] [--warmup W] [--workload stress] [--b-th 0.2] [--no-cpu]
     python bench.py --sweep            one JSON line per B_th of the workload's sweep
     python bench.py --copy-probe MB    device copies of known size (counter calibration)
+    python bench.py --train            training runs, sparse vs full-surrogate gradient (App. E, H)
 """
 from __future__ import annotations
 
@@ -108,6 +109,106 @@ def copy_probe(mb):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "copies": 5}))
+
+
+def _grad_difference(a, b):
+    """App. H statistics of a sparse gradient a against the full-surrogate gradient b (host arrays):
+    max |a - b| / max |b|, the largest per-weight relative difference among weights with
+    |b| >= 1% of max |b|, the relative Frobenius norm of a - b, and the cosine of a and b."""
+    a = np.asarray(a, np.float64).ravel()
+    b = np.asarray(b, np.float64).ravel()
+    d = np.abs(a - b)
+    sc = np.abs(b).max()
+    big = np.abs(b) >= 0.01 * sc
+    nb, na = np.linalg.norm(b), np.linalg.norm(a)
+    return {"max_abs_over_max": float(d.max() / sc) if sc > 0 else 0.0,
+            "max_rel_big": float((d[big] / np.abs(b[big])).max()) if big.any() else 0.0,
+            "frobenius_rel": float(np.linalg.norm(a - b) / nb) if nb > 0 else 0.0,
+            "cosine": float(a @ b / (na * nb)) if na > 0 and nb > 0 else 0.0}
+
+
+def train_experiment(args):
+    """Training runs (App. E): the sparse gradient (B_th of the workload) and full-surrogate BPTT
+    (dense chain, B_th = inf) from the same initial weights over the same batches, with the
+    activity penalties and Adam. Prints one JSON line with the loss and test-accuracy
+    trajectories, the active fraction per layer, the time per training step of both, and the
+    App. H gradient-difference statistics at the initial and at the final sparse weights."""
+    import torch
+    from paper_2105_08810_amd import pipeline, snn
+    from synth import CONFIGS, make_inputs
+    from synth.inputs import make_labels, make_spikes
+    snn.lib()
+    cfg = CONFIGS[args.train_workload]
+    B, T, P = cfg.B, cfg.T, args.train_batches
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    Xs = [torch.from_numpy(make_spikes(cfg, range(k * B, (k + 1) * B))).to(dev) for k in range(P)]
+    Ys = [torch.from_numpy(make_labels(cfg, range(k * B, (k + 1) * B))).to(dev) for k in range(P)]
+    held = 10 ** 6  # held-out samples come from far above the training indices
+    Xt = [torch.from_numpy(make_spikes(cfg, range(held + k * B, held + (k + 1) * B))).to(dev) for k in range(2)]
+    Yt = [torch.from_numpy(make_labels(cfg, range(held + k * B, held + (k + 1) * B))).to(dev) for k in range(2)]
+    gen_s = time.time() - t0
+    inp0 = make_inputs(cfg, range(B))
+    pen = pipeline.Penalty(nu_up=args.nu_up)
+    aux = torch.cuda.Stream()
+
+    def grads_at(net, k, sparse):
+        net.X, net.labels = Xs[k], Ys[k]
+        opt = pipeline.Adam(net.params(), lr=0.0)
+        out = net.train_step(opt, cfg.b_th if sparse else math.inf, pen, sparse=sparse, aux_stream=aux)
+        return [g.cpu().numpy() for g in out["grads"]]
+
+    def diff(net):
+        gs, gf = grads_at(net, 0, True), grads_at(net, 0, False)
+        return [_grad_difference(a, b) for a, b in zip(gs, gf)]
+
+    def accuracy(net):
+        hits = 0
+        for X, Y in zip(Xt, Yt):
+            net.X = X
+            net.forward()
+            logits = net.V_out.max(dim=0).values if net.loss_mode == 0 else net.V_out.sum(dim=0)
+            hits += int((logits.argmax(dim=1).to(torch.int32) == Y).sum().item())
+        return hits / (len(Xt) * B)
+
+    result = {"mode": "train", "workload": cfg.name, "description": cfg.description, "steps": args.train_steps,
+              "batches_in_training_set": P, "lr": args.lr, "betas": [0.9, 0.999],
+              "penalty": vars(pen), "b_th_sparse": cfg.b_th, "data": "synthetic", "input_gen_s": gen_s}
+    nets = {}
+    for name, sparse in (("sparse", True), ("full_surrogate", False)):
+        net = pipeline.from_inputs(inp0, "cuda:0").allocate()
+        if name == "sparse":
+            result["grad_difference_init"] = diff(net)
+        opt = pipeline.Adam(net.params(), lr=args.lr)
+        b_th = cfg.b_th if sparse else math.inf
+        ce, pn, nnz, ms, acc = [], [], [], [], [acc0 := accuracy(net)]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for step in range(args.train_steps):
+            k = step % P
+            net.X, net.labels = Xs[k], Ys[k]
+            e0.record()
+            out = net.train_step(opt, b_th, pen, sparse=sparse, aux_stream=aux)
+            e1.record()
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+            ce.append(float(out["ce"].item()))
+            pn.append(float(out["penalty"].item()))
+            if sparse:
+                nnz.append([int(c.item()) for c in out["nnz"]])
+            if k == P - 1:
+                acc.append(accuracy(net))
+        nets[name] = net
+        r = {"ce": ce, "penalty": pn, "test_accuracy_per_epoch": acc, "train_step_ms_median": float(np.median(ms)),
+             "train_step_ms_iqr": [float(np.percentile(ms, 25)), float(np.percentile(ms, 75))],
+             "initial_test_accuracy": acc0}
+        if sparse:
+            sizes = cfg.sizes[1:-1]
+            r["active_fraction_per_layer"] = [[n / (T * B * sizes[l]) for l, n in enumerate(row)] for row in nnz]
+        result[name] = r
+    result["grad_difference_end_sparse_weights"] = diff(nets["sparse"])
+    result["train_step_speedup"] = result["full_surrogate"]["train_step_ms_median"] / result["sparse"][
+        "train_step_ms_median"]
+    print(json.dumps(result), flush=True)
 
 
 class Runner:
@@ -329,6 +430,13 @@ def main():
                     help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
+    ap.add_argument("--train", action="store_true",
+                    help="training runs, sparse vs full surrogate (App. E); prints one JSON line")
+    ap.add_argument("--train-workload", default="latency_train")
+    ap.add_argument("--train-steps", type=int, default=600)
+    ap.add_argument("--train-batches", type=int, default=20, help="batches in the synthetic training set")
+    ap.add_argument("--lr", type=float, default=2e-4)
+    ap.add_argument("--nu-up", type=float, default=1.0)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the path is single-device here (multi-GPU is design only)",
@@ -336,6 +444,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.train:
+        train_experiment(args)
         return
 
     from paper_2105_08810_amd import snn

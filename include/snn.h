@@ -212,6 +212,54 @@ snn_status snn_readout_ce(const float* V_out, const int32_t* labels, int T, int 
                           int32_t* row_ptr, int32_t* col_idx, float* eps, float* loss, float* eps_dense,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Activity penalties of App. E on one LIF layer's spikes (training step, outside the measured
+ * backward). With zeta[b,i] = number of nonzero S[t,b,i] over t and, per sample,
+ *   R_low[b] = (lam_low/N) sum_i max(0, nu_low - zeta[b,i])^2,
+ *   R_up[b]  = lam_up max(0, (1/N) sum_i zeta[b,i] - nu_up)
+ * (the appendix prints both negated, as terms to maximise; these are the penalties minimised),
+ * the loss gains (1/B) sum_b (R_low[b] + R_up[b]).
+ *   S        [T,B,N] uint8 spikes of the layer (read)
+ *   zeta     int32 [B,N] (written unless NULL): the spike counts
+ *   coef     float32 [B,N] (written): d loss / d zeta[b,i] =
+ *            (-2 lam_low/N max(0, nu_low - zeta) + [mean_i zeta[b,i] > nu_up] lam_up/N) / B,
+ *            which is also d loss / d S[t,b,i] at every t (slope 0 at the hinges)
+ *   penalty  float32 [1] device (written unless NULL): (1/B) sum_b (R_low[b] + R_up[b])
+ * lam_low, lam_up must be finite and >= 0, nu_low, nu_up finite; otherwise SNN_ERR_INVALID_ARG.
+ * Sums are formed in float64 in a fixed order: outputs are deterministic.
+ */
+size_t snn_activity_reg_workspace(int T, int B, int N);
+snn_status snn_activity_reg(const uint8_t* S, int T, int B, int N, float lam_low, float nu_low, float lam_up,
+                            float nu_up, int32_t* zeta, float* coef, float* penalty, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * Adds the penalties' gradient to a layer's spike gradient (App. E; the count is a sum over t,
+ * so coef[b,i] joins the gradient w.r.t. S[t,b,i] at every t).
+ *   coef     float32 [B,N] from snn_activity_reg (read)
+ *   row_ptr, col_idx, capacity: the layer's active-set CSR (rows r = t*B + b); then eps is
+ *            float32 [capacity], the spike gradient at those entries (snn_sparse_backward's
+ *            eps_in), and eps[e] += coef[b, col_idx[e]] for e < min(row_ptr[T*B], capacity).
+ *            Columns outside [0, N) are skipped.
+ *   row_ptr NULL: eps is the dense [T,B,N] gradient and eps[t,b,i] += coef[b,i] everywhere.
+ * No workspace; nothing is allocated.
+ */
+snn_status snn_activity_reg_grad(const float* coef, int T, int B, int N, const int32_t* row_ptr,
+                                 const int32_t* col_idx, int64_t capacity, float* eps, void* stream);
+
+/*
+ * One Adam step on a float32 tensor of n elements (App. E's optimiser; Kingma and Ba,
+ * Algorithm 1), in place:
+ *   m = beta1 m + (1-beta1) grad;  v = beta2 v + (1-beta2) grad^2;
+ *   W -= lr/(1-beta1^step) * m / (sqrt(v/(1-beta2^step)) + eps)
+ * step counts from 1; m and v start at zero. The bias corrections are formed in float64 on
+ * the host, the rest in float32. All four arrays are device float32 [n]; grad is read only.
+ * SNN_ERR_INVALID_ARG for step < 1, n <= 0, lr < 0, betas outside [0, 1), eps <= 0, or
+ * non-finite hyper-parameters.
+ */
+snn_status snn_adam_step(float* W, const float* grad, float* m, float* v, int64_t n, float lr, float beta1,
+                         float beta2, float eps, int step, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,6 +25,7 @@ SOURCES = [
     "sparse_backward.hip",
     "dense_backward.hip",
     "readout_ce.hip",
+    "train_step.hip",
 ]
 # The forward and the compaction decide spikes and active sets, which must be bit-exact:
 # no contraction of a*b+c into fused multiply-adds there.

@@ -7,6 +7,7 @@ layers then an infinite-threshold readout with a cross-entropy loss (App. E).
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass, field
 from typing import List, Optional
 
@@ -100,9 +101,15 @@ class Network:
                     for l in range(self.L)]
         return [snn.active_compact(self.V[l], self.theta, b_th, self.beta, caps[l]) for l in range(self.L)]
 
-    def sparse_backward(self, csrs: List[snn.Csr], ro=None, aux_stream=None, workspaces=None):
+    def activity(self, reg: "Penalty", want_zeta=False):
+        """Activity penalties of every LIF layer (App. E) on the forward's spikes.
+        Returns a list of (coef [B, N_l], penalty [1], zeta or None), all on the device."""
+        return [snn.activity_reg(S, reg.lam_low, reg.nu_low, reg.lam_up, reg.nu_up, want_zeta) for S in self.S]
+
+    def sparse_backward(self, csrs: List[snn.Csr], ro=None, aux_stream=None, workspaces=None, reg_coefs=None):
         """Readout backward, then every LIF layer top down. Returns (dW list, dW_out, eps list)
-        where eps[l] is the gradient w.r.t. layer l's spikes at its active entries."""
+        where eps[l] is the gradient w.r.t. layer l's spikes at its active entries. reg_coefs[l]
+        ([B, N_l], from activity()) joins layer l's spike gradient before its backward."""
         if ro is None:
             ro = self.readout()
         ro_csr, ro_eps = ro[0], ro[1]
@@ -112,13 +119,16 @@ class Network:
         dWs: List[Optional[torch.Tensor]] = [None] * self.L
         epss: List[Optional[torch.Tensor]] = [None] * self.L
         for l in range(self.L - 1, -1, -1):
+            if reg_coefs is not None:
+                snn.activity_reg_grad(reg_coefs[l], self.T, eps, csrs[l])
             epss[l] = eps
             dWs[l], eps = snn.sparse_backward(self.Ws[l], self.trace[l], self.alphas[l], csrs[l], eps,
                                               inp=csrs[l - 1] if l > 0 else None, ws=ws[l], aux_stream=aux_stream)
         return dWs, dW_out, epss
 
-    def dense_backward(self, b_th, ro=None):
-        """The dense baseline chain. Returns (dW list, dW_out, eps_dense list)."""
+    def dense_backward(self, b_th, ro=None, reg_coefs=None):
+        """The dense baseline chain (b_th = inf: full-surrogate BPTT). Returns (dW list, dW_out,
+        eps_dense list); reg_coefs as in sparse_backward."""
         if ro is None or ro[3] is None:
             ro = self.readout(dense=True)
         dW_out, eps = snn.dense_backward_ref(self.W_out, self.trace_out, self.V_out, ro[3], self.alpha_out, INF,
@@ -126,10 +136,65 @@ class Network:
         dWs: List[Optional[torch.Tensor]] = [None] * self.L
         epss: List[Optional[torch.Tensor]] = [None] * self.L
         for l in range(self.L - 1, -1, -1):
+            if reg_coefs is not None:
+                snn.activity_reg_grad(reg_coefs[l], self.T, eps)
             epss[l] = eps
             dWs[l], eps = snn.dense_backward_ref(self.Ws[l], self.trace[l], self.V[l], eps, self.alphas[l],
                                                  self.theta, b_th, self.beta, grad_in=l > 0)
         return dWs, dW_out, epss
+
+
+    def params(self) -> List[torch.Tensor]:
+        return list(self.Ws) + [self.W_out]
+
+    def train_step(self, opt: "Adam", b_th: float, reg: Optional["Penalty"] = None, sparse: bool = True,
+                   aux_stream=None):
+        """One training step (App. E): forward, cross-entropy plus activity penalties, the sparse
+        (or, with sparse=False, the dense) backward with truncation band b_th, and an Adam step on
+        every weight matrix in place. b_th = inf with sparse=False is full-surrogate BPTT.
+        Returns a dict of device tensors: ce [1], penalty [1] (all layers), grads (list), nnz."""
+        self.forward(b_th if sparse and math.isfinite(b_th) else None)
+        acts = self.activity(reg) if reg is not None else None
+        coefs = [a[0] for a in acts] if acts else None
+        if sparse:
+            ro = self.readout()
+            csrs = self.compact(b_th)
+            dWs, dW_out, _ = self.sparse_backward(csrs, ro, aux_stream=aux_stream, reg_coefs=coefs)
+            nnz = [c.nnz_dev for c in csrs]
+        else:
+            ro = self.readout(dense=True)
+            dWs, dW_out, _ = self.dense_backward(b_th, ro, reg_coefs=coefs)
+            nnz = None
+        grads = list(dWs) + [dW_out]
+        opt.step(grads)
+        pen = sum(a[1] for a in acts) if acts else torch.zeros(1, device=self.X.device)
+        return {"ce": ro[2], "penalty": pen, "grads": grads, "nnz": nnz}
+
+
+@dataclass
+class Penalty:
+    """Activity penalty weights and bounds of App. E (its parameter table: F-MNIST / N-MNIST
+    values by default; SHD uses nu_up = 10)."""
+    lam_low: float = 100.0
+    nu_low: float = 0.001
+    lam_up: float = 0.06
+    nu_up: float = 1.0
+
+
+class Adam:
+    """Adam state for a list of float32 device tensors, updated in place by snn_adam_step."""
+
+    def __init__(self, params: List[torch.Tensor], lr: float, betas=(0.9, 0.999), eps: float = 1e-8):
+        self.params = params
+        self.lr, self.betas, self.eps = float(lr), tuple(betas), float(eps)
+        self.m = [torch.zeros_like(p) for p in params]
+        self.v = [torch.zeros_like(p) for p in params]
+        self.k = 0
+
+    def step(self, grads: List[torch.Tensor]):
+        self.k += 1
+        for p, g, m, v in zip(self.params, grads, self.m, self.v):
+            snn.adam_step(p, g, m, v, self.k, self.lr, self.betas, self.eps)
 
 
 def from_inputs(inp, device="cuda") -> Network:

@@ -47,6 +47,10 @@ _SIGNATURES = {
     "snn_dense_backward_ref": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _F, _F, _F, _F, _P, _P, _P, _SZ, _P]),
     "snn_readout_ce_workspace": (_SZ, [_I, _I, _I, _I]),
     "snn_readout_ce": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "snn_activity_reg_workspace": (_SZ, [_I, _I, _I]),
+    "snn_activity_reg": (_I, [_P, _I, _I, _I, _F, _F, _F, _F, _P, _P, _P, _P, _SZ, _P]),
+    "snn_activity_reg_grad": (_I, [_P, _I, _I, _I, _P, _P, _I64, _P, _P]),
+    "snn_adam_step": (_I, [_P, _P, _P, _P, _I64, _F, _F, _F, _F, _I, _P]),
 }
 
 _lib = None
@@ -220,6 +224,30 @@ def snn_readout_ce(V_out, labels, T, B, C, mode, row_ptr, col_idx, eps, loss, ep
         _ptr(eps_dense, torch.float32, "eps_dense"), _ptr(ws, None, "workspace"), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def snn_activity_reg_workspace(T, B, N) -> int:
+    return int(lib().snn_activity_reg_workspace(T, B, N))
+
+
+def snn_activity_reg(S, T, B, N, lam_low, nu_low, lam_up, nu_up, zeta, coef, penalty, ws, stream=None):
+    _check("snn_activity_reg", lib().snn_activity_reg(
+        _ptr(S, torch.uint8, "S"), T, B, N, float(lam_low), float(nu_low), float(lam_up), float(nu_up),
+        _ptr(zeta, torch.int32, "zeta"), _ptr(coef, torch.float32, "coef"), _ptr(penalty, torch.float32, "penalty"),
+        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_activity_reg_grad(coef, T, B, N, row_ptr, col_idx, capacity, eps, stream=None):
+    _check("snn_activity_reg_grad", lib().snn_activity_reg_grad(
+        _ptr(coef, torch.float32, "coef"), T, B, N, _ptr(row_ptr, torch.int32, "row_ptr"),
+        _ptr(col_idx, torch.int32, "col_idx"), int(capacity), _ptr(eps, torch.float32, "eps"), _stream(stream)))
+
+
+def snn_adam_step(W, grad, m, v, n, lr, beta1, beta2, eps, step, stream=None):
+    _check("snn_adam_step", lib().snn_adam_step(
+        _ptr(W, torch.float32, "W"), _ptr(grad, torch.float32, "grad"), _ptr(m, torch.float32, "m"),
+        _ptr(v, torch.float32, "v"), int(n), float(lr), float(beta1), float(beta2), float(eps), int(step),
+        _stream(stream)))
+
+
 # ------------------------------------------------------------------ allocation helpers
 
 def lif_forward(s_in: torch.Tensor, W: torch.Tensor, alpha, theta, want_trace=True):
@@ -348,6 +376,38 @@ def dense_backward_ref(W, trace_in, V, eps_out, alpha, theta, b_th, beta, grad_i
         ws = workspace(snn_dense_backward_workspace(T, B, N_in, N_out), dev)
     snn_dense_backward_ref(W, trace_in, V, eps_out, T, B, N_in, N_out, alpha, theta, b_th, beta, gi, dW, ws)
     return dW, gi
+
+
+def activity_reg(S: torch.Tensor, lam_low, nu_low, lam_up, nu_up, want_zeta=False, ws=None, stream=None):
+    """Allocate and run snn_activity_reg on S [T, B, N]. Returns (coef [B, N], penalty [1], zeta or None)."""
+    T, B, N = S.shape
+    dev = S.device
+    coef = torch.empty((B, N), dtype=torch.float32, device=dev)
+    pen = torch.empty(1, dtype=torch.float32, device=dev)
+    zeta = torch.empty((B, N), dtype=torch.int32, device=dev) if want_zeta else None
+    if ws is None:
+        ws = workspace(snn_activity_reg_workspace(T, B, N), dev)
+    snn_activity_reg(S, T, B, N, lam_low, nu_low, lam_up, nu_up, zeta, coef, pen, ws, stream)
+    return coef, pen, zeta
+
+
+def activity_reg_grad(coef: torch.Tensor, T: int, eps: torch.Tensor, csr: Optional["Csr"] = None, stream=None):
+    """Run snn_activity_reg_grad: eps at csr's entries (or dense [T, B, N] when csr is None) += coef."""
+    B, N = coef.shape
+    if csr is None:
+        snn_activity_reg_grad(coef, T, B, N, None, None, 0, eps, stream)
+    else:
+        snn_activity_reg_grad(coef, T, B, N, csr.row_ptr, csr.col_idx, min(csr.capacity, eps.numel()), eps, stream)
+    return eps
+
+
+def adam_step(W, grad, m, v, step, lr, betas=(0.9, 0.999), eps=1e-8, stream=None):
+    """Run snn_adam_step on W in place (m and v are its float32 moment buffers)."""
+    n = W.numel()
+    if grad.numel() != n or m.numel() != n or v.numel() != n:
+        raise ValueError("adam_step: W, grad, m and v must have the same size")
+    snn_adam_step(W, grad, m, v, n, lr, betas[0], betas[1], eps, step, stream)
+    return W
 
 
 INF = math.inf

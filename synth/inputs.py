@@ -90,6 +90,11 @@ CONFIGS = {
         "stress", 5, T=500, B=256, sizes=(1024, 1024, 1024, 1024, 100), tau_ratio_hidden=0.1, tau_ratio_out=0.1,
         loss_mode="max", b_th=0.2, b_th_sweep=(0.02, 0.05, 0.1, 0.2, 0.35, 0.5, 0.8, 1.2), kind="bernoulli", rate=0.02,
         description="3 LIF layers 1024->1024, readout 1024->100, T=500, B=256, Bernoulli(0.02)"),
+    "latency_train": Config(
+        "latency_train", 6, T=100, B=256, sizes=(784, 200, 200, 10), tau_ratio_hidden=0.1, tau_ratio_out=0.1,
+        loss_mode="max", b_th=0.2, kind="classlatency",
+        description="class-conditional latency code (F-MNIST-like training task): 28x28 class templates plus "
+                    "noise, one spike per input at most; LIF 784->200->200, readout 200->10"),
 }
 
 
@@ -176,11 +181,59 @@ def _spikes_audio(cfg: Config, b: int) -> np.ndarray:
     return (r.poisson(lam.T) >= 1).astype(np.uint8)
 
 
+# Class-conditional latency code for training runs. Each class has a 28x28 template (a few
+# Gaussian blobs); a sample adds pixel noise to its class's template and each pixel x above
+# LAT_THETA fires once at step floor(LAT_TAU_EFF ln(x / (x - LAT_THETA))) if that is < T
+# (brighter pixels fire earlier; tau_eff = 20 steps and theta = 0.2 as in App. E's table).
+LAT_TAU_EFF = 20.0
+LAT_THETA = 0.2
+CLASS_BLOBS = 3
+CLASS_NOISE = 0.25
+_TEMPLATES = {}
+
+
+def class_templates(cfg: Config) -> np.ndarray:
+    """[C, N_in] float64 intensities in [0, 1] (N_in a square)."""
+    if cfg.name not in _TEMPLATES:
+        r = rng_for(cfg.cfg_id, 40)
+        side = int(round(math.sqrt(cfg.sizes[0])))
+        assert side * side == cfg.sizes[0]
+        ys, xs = np.mgrid[0:side, 0:side].astype(np.float64)
+        out = np.zeros((cfg.sizes[-1], side * side))
+        for c in range(cfg.sizes[-1]):
+            img = np.zeros((side, side))
+            for _ in range(CLASS_BLOBS):
+                cy, cx = r.uniform(4, side - 4, 2)
+                sd = r.uniform(2.5, 5.0)
+                a = r.uniform(0.6, 1.0)
+                img += a * np.exp(-((ys - cy) ** 2 + (xs - cx) ** 2) / (2 * sd * sd))
+            out[c] = np.clip(img, 0.0, 1.0).ravel()
+        _TEMPLATES[cfg.name] = out
+    return _TEMPLATES[cfg.name]
+
+
+def label_of(cfg: Config, sample: int) -> int:
+    """Class of one sample of a class-conditional workload (any sample index >= 0)."""
+    return int(rng_for(cfg.cfg_id, 30, sample).integers(0, cfg.sizes[-1]))
+
+
+def _spikes_classlatency(cfg: Config, b: int) -> np.ndarray:
+    r = rng_for(cfg.cfg_id, 0, b)
+    x = np.clip(class_templates(cfg)[label_of(cfg, b)] + CLASS_NOISE * r.standard_normal(cfg.sizes[0]), 0.0, 1.0)
+    out = np.zeros((cfg.T, cfg.sizes[0]), np.uint8)
+    idx = np.nonzero(x > LAT_THETA)[0]
+    t = np.floor(LAT_TAU_EFF * np.log(x[idx] / (x[idx] - LAT_THETA))).astype(np.int64)
+    keep = t < cfg.T
+    out[t[keep], idx[keep]] = 1
+    return out
+
+
 _SPIKE_KINDS = {
     "bernoulli": _spikes_bernoulli,
     "latency": _spikes_latency,
     "event": _spikes_event,
     "audio": _spikes_audio,
+    "classlatency": _spikes_classlatency,
 }
 
 
@@ -232,6 +285,9 @@ def make_weights(cfg: Config, sigmas: Optional[List[float]] = None) -> List[np.n
 
 
 def make_labels(cfg: Config, batch: Optional[Sequence[int]] = None) -> np.ndarray:
+    if cfg.kind == "classlatency":
+        bs = range(cfg.B) if batch is None else batch
+        return np.array([label_of(cfg, int(b)) for b in bs], np.int32)
     y = rng_for(cfg.cfg_id, 30).integers(0, cfg.sizes[-1], size=cfg.B).astype(np.int32)
     return y if batch is None else y[np.asarray(batch)]
 

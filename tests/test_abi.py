@@ -211,3 +211,44 @@ def test_compact_bits_v_optional_without_g(lib):
     # (deliberately) missing workspace instead
     assert _cb(lib, V=None, g=None, ws=None) == snn.SNN_ERR_INVALID_ARG
     assert lib.snn_active_compact_bits_workspace(10, 4, 16) > 0
+
+
+def _reg(lib, **kw):
+    a = dict(S=FAKE, T=10, B=4, N=16, ll=100.0, nl=0.001, lu=0.06, nu=1.0, zeta=FAKE, coef=FAKE, pen=FAKE, ws=FAKE,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    return lib.snn_activity_reg(a["S"], a["T"], a["B"], a["N"], a["ll"], a["nl"], a["lu"], a["nu"], a["zeta"],
+                                a["coef"], a["pen"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(S=None), dict(coef=None), dict(ws=None), dict(ws_bytes=16), dict(T=0),
+                                dict(N=-1), dict(ll=-1.0), dict(lu=NAN), dict(ll=INF), dict(nl=NAN), dict(nu=INF),
+                                dict(T=70000, B=70000)])
+def test_activity_reg_rejects(lib, kw):
+    assert _reg(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_activity_reg_workspace(lib):
+    # 2048 target blocks over 65536 quads of 256 threads: 8 chunks of 63 steps at T=500, B=256, N=1024
+    assert lib.snn_activity_reg_workspace(500, 256, 1024) >= 8 * 256 * 1024 * 4 + 256 * 8
+    assert lib.snn_activity_reg_workspace(0, 4, 16) == 0
+    assert lib.snn_activity_reg_workspace(20, 4, 32) >= 20 * 4 * 32 * 4
+
+
+@pytest.mark.parametrize("kw", [dict(coef=None), dict(eps=None), dict(T=0), dict(B=-1),
+                                dict(rp=FAKE, ci=None), dict(rp=FAKE, cap=-1)])
+def test_activity_reg_grad_rejects(lib, kw):
+    a = dict(coef=FAKE, T=10, B=4, N=16, rp=None, ci=FAKE, cap=10, eps=FAKE)
+    a.update(kw)
+    assert lib.snn_activity_reg_grad(a["coef"], a["T"], a["B"], a["N"], a["rp"], a["ci"], a["cap"], a["eps"],
+                                     None) == snn.SNN_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(W=None), dict(g=None), dict(m=None), dict(v=None), dict(n=0), dict(step=0),
+                                dict(lr=-1e-3), dict(lr=NAN), dict(b1=1.0), dict(b2=-0.1), dict(b2=NAN),
+                                dict(eps=0.0), dict(eps=INF)])
+def test_adam_rejects(lib, kw):
+    a = dict(W=FAKE, g=FAKE, m=FAKE, v=FAKE, n=100, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, step=1)
+    a.update(kw)
+    assert lib.snn_adam_step(a["W"], a["g"], a["m"], a["v"], a["n"], a["lr"], a["b1"], a["b2"], a["eps"], a["step"],
+                             None) == snn.SNN_ERR_INVALID_ARG
