@@ -36,6 +36,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F32_TFLOPS = 157.3  # dense fp32 matrix-core peak
+CPU_TARGET_S = 10.0  # seconds of oracle work timed for the CPU baseline
 # float64 LDS read-modify-write adds: 256 CUs x 2.4 GHz x 128 B/clk of LDS, 16 B per lane
 # update (8 read, 8 written) -> 4.915e12 lane updates/s; 2 flops each (multiply, add)
 LDS_F64_RMW_TFLOPS = 2 * 256 * 2.4e9 * 128 / 16 / 1e12
@@ -82,20 +84,26 @@ def cpu_baseline(cfg, b_th, n_samples):
         blas = [(d.get("internal_api"), d.get("num_threads")) for d in threadpool_info()]
     except Exception:  # pragma: no cover
         blas = []
+    n_samples = min(n_samples, cfg.B)
     inp = make_inputs(cfg, list(range(n_samples)))
     f = oracle.network_forward(inp.X, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, np.float32(cfg.theta))
-    t0 = time.perf_counter()
-    nnz = 0
-    for V in f["V"]:
-        rp, _, _ = oracle.active_csr(V, cfg.theta, b_th, cfg.beta)
-        nnz += int(rp[-1])
-    oracle.network_backward(f, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, inp.labels, cfg.loss_mode,
-                            cfg.theta, b_th, cfg.beta)
-    dt = time.perf_counter() - t0
+    # the timed unit is repeated until about CPU_TARGET_S of work has been measured
+    reps, dt, nnz = 0, 0.0, 0
+    while reps == 0 or (dt < CPU_TARGET_S and reps < 200):
+        t0 = time.perf_counter()
+        n = 0
+        for V in f["V"]:
+            rp, _, _ = oracle.active_csr(V, cfg.theta, b_th, cfg.beta)
+            n += int(rp[-1])
+        oracle.network_backward(f, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, inp.labels, cfg.loss_mode,
+                                cfg.theta, b_th, cfg.beta)
+        dt += time.perf_counter() - t0
+        nnz += n
+        reps += 1
     threads = max([n for _, n in blas if n] or [1])
     return {"value": nnz / dt, "unit": "active neuron-steps/s", "cores": threads, "kind": "oracle",
             "sample": f"{cfg.name} workload, batch samples 0..{n_samples - 1} of {cfg.B}, B_th={b_th}: "
-                      f"compaction + fp64 backward of all layers, {dt:.2f} s, {nnz} active entries",
+                      f"compaction + fp64 backward of all layers, {reps} runs, {dt:.2f} s, {nnz} active entries",
             "host_cpus": len(os.sched_getaffinity(0)), "blas": blas}
 
 
@@ -128,11 +136,13 @@ def _grad_difference(a, b):
 
 
 def train_experiment(args):
-    """Training runs (App. E): the sparse gradient (B_th of the workload) and full-surrogate BPTT
-    (dense chain, B_th = inf) from the same initial weights over the same batches, with the
-    activity penalties and Adam. Prints one JSON line with the loss and test-accuracy
+    """Training runs (App. E): the sparse gradient (the workload's B_th, or each band of
+    --train-bth) and full-surrogate BPTT (dense chain, B_th = inf) from the same initial weights
+    over the same batches, with the activity penalties and Adam. Prints one JSON line with the loss and test-accuracy
     trajectories, the active fraction per layer, the time per training step of both, and the
-    App. H gradient-difference statistics at the initial and at the final sparse weights."""
+    App. H gradient-difference statistics at the initial and at the final sparse weights.
+    The step time is host wall time from the call to the end of the step's work (it includes
+    the host reads of each layer's active-set size); the phases are HIP events."""
     import torch
     from paper_2105_08810_amd import pipeline, snn
     from synth import CONFIGS, make_inputs
@@ -152,14 +162,15 @@ def train_experiment(args):
     pen = pipeline.Penalty(nu_up=args.nu_up)
     aux = torch.cuda.Stream()
 
-    def grads_at(net, k, sparse):
+    def grads_at(net, k, b_th):
+        """Gradients at the net's weights on batch k: sparse with band b_th, or full surrogate (inf)."""
         net.X, net.labels = Xs[k], Ys[k]
         opt = pipeline.Adam(net.params(), lr=0.0)
-        out = net.train_step(opt, cfg.b_th if sparse else math.inf, pen, sparse=sparse, aux_stream=aux)
+        out = net.train_step(opt, b_th, pen, sparse=math.isfinite(b_th), aux_stream=aux)
         return [g.cpu().numpy() for g in out["grads"]]
 
-    def diff(net):
-        gs, gf = grads_at(net, 0, True), grads_at(net, 0, False)
+    def diff(net, b_th):
+        gs, gf = grads_at(net, 0, b_th), grads_at(net, 0, math.inf)
         return [_grad_difference(a, b) for a, b in zip(gs, gf)]
 
     def accuracy(net):
@@ -171,42 +182,49 @@ def train_experiment(args):
             hits += int((logits.argmax(dim=1).to(torch.int32) == Y).sum().item())
         return hits / (len(Xt) * B)
 
+    bths = [float(x) for x in args.train_bth.split(",")] if args.train_bth else [cfg.b_th]
     result = {"mode": "train", "workload": cfg.name, "description": cfg.description, "steps": args.train_steps,
               "batches_in_training_set": P, "lr": args.lr, "betas": [0.9, 0.999],
-              "penalty": vars(pen), "b_th_sparse": cfg.b_th, "data": "synthetic", "input_gen_s": gen_s}
+              "penalty": vars(pen), "b_th_sparse": bths, "data": "synthetic", "input_gen_s": gen_s}
+    runs = [(f"sparse_bth_{b:g}", True, b) for b in bths] + [("full_surrogate", False, math.inf)]
     nets = {}
-    for name, sparse in (("sparse", True), ("full_surrogate", False)):
+    for name, sparse, b_th in runs:
         net = pipeline.from_inputs(inp0, "cuda:0").allocate()
-        if name == "sparse":
-            result["grad_difference_init"] = diff(net)
+        if name == runs[0][0]:
+            result["grad_difference_init"] = diff(net, b_th)
         opt = pipeline.Adam(net.params(), lr=args.lr)
-        b_th = cfg.b_th if sparse else math.inf
-        ce, pn, nnz, ms, acc = [], [], [], [], [acc0 := accuracy(net)]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        acc0 = accuracy(net)
+        ce, pn, nnz, ms, acc, phases = [], [], [], [], [acc0], []
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
         for step in range(args.train_steps):
             k = step % P
             net.X, net.labels = Xs[k], Ys[k]
-            e0.record()
-            out = net.train_step(opt, b_th, pen, sparse=sparse, aux_stream=aux)
-            e1.record()
-            e1.synchronize()
-            ms.append(e0.elapsed_time(e1))
+            w0 = time.perf_counter()
+            out = net.train_step(opt, b_th, pen, sparse=sparse, aux_stream=aux, events=ev)
+            ev[5].synchronize()
+            ms.append((time.perf_counter() - w0) * 1e3)
+            phases.append([ev[i].elapsed_time(ev[i + 1]) for i in range(5)])
             ce.append(float(out["ce"].item()))
             pn.append(float(out["penalty"].item()))
             if sparse:
                 nnz.append([int(c.item()) for c in out["nnz"]])
             if k == P - 1:
                 acc.append(accuracy(net))
-        nets[name] = net
-        r = {"ce": ce, "penalty": pn, "test_accuracy_per_epoch": acc, "train_step_ms_median": float(np.median(ms)),
+        nets[name] = (net, b_th)
+        ph = np.median(np.array(phases), axis=0)
+        r = {"b_th": b_th if math.isfinite(b_th) else "inf", "ce": ce, "penalty": pn,
+             "test_accuracy_per_epoch": acc, "train_step_ms_median": float(np.median(ms)),
              "train_step_ms_iqr": [float(np.percentile(ms, 25)), float(np.percentile(ms, 75))],
+             "phase_ms_median": dict(zip(("forward", "loss_and_penalties", "compaction", "backward", "adam"),
+                                         map(float, ph))),
              "initial_test_accuracy": acc0}
         if sparse:
             sizes = cfg.sizes[1:-1]
             r["active_fraction_per_layer"] = [[n / (T * B * sizes[l]) for l, n in enumerate(row)] for row in nnz]
         result[name] = r
-    result["grad_difference_end_sparse_weights"] = diff(nets["sparse"])
-    result["train_step_speedup"] = result["full_surrogate"]["train_step_ms_median"] / result["sparse"][
+    first_net, first_bth = nets[runs[0][0]]
+    result["grad_difference_end_sparse_weights"] = diff(first_net, first_bth)
+    result["train_step_speedup"] = result["full_surrogate"]["train_step_ms_median"] / result[runs[0][0]][
         "train_step_ms_median"]
     print(json.dumps(result), flush=True)
 
@@ -218,8 +236,9 @@ class Runner:
         import torch
         from paper_2105_08810_amd import pipeline, snn
         from synth import make_inputs
-        self.torch, self.snn = torch, snn
+        self.torch, self.snn, self.pipeline = torch, snn, pipeline
         self.cfg, self.args = cfg, args
+        self.graphs = {}
         inp = make_inputs(cfg)
         self.net = net = pipeline.from_inputs(inp, "cuda:0").allocate()
         self.T, self.B, self.L = net.T, net.B, net.L
@@ -239,6 +258,7 @@ class Runner:
         """Size compaction outputs and workspaces for one band (the first compaction counts)."""
         snn, T, B, L, sizes = self.snn, self.T, self.B, self.L, self.sizes
         self.b_th = b_th
+        self.graphs = {}  # captured for this band on first use
         self.net.forward(None if self.args.unfused else b_th)
         csrs = self.net.compact(b_th)
         self.caps = [c.capacity for c in csrs]
@@ -251,21 +271,36 @@ class Runner:
         self.share = [False] + [3.0 * self.caps[l] * sizes[l] >= 2.0 * self.caps[l - 1] * sizes[l + 1]
                                 for l in range(1, L)]
 
+    def region(self, key, stream, fn):
+        """Run fn's library calls on stream: directly, or (with --graph) as a HIP graph captured on
+        first use and replayed after that. Returns what fn returns (static under a graph)."""
+        torch = self.torch
+        if not self.args.graph:
+            with torch.cuda.stream(stream):
+                return fn()
+        if key not in self.graphs:
+            self.graphs[key] = self.pipeline.Graphed(fn, stream)
+        return self.graphs[key](stream)
+
     def step(self, ev, dense=True):
-        """One pass of the whole path. ev: dict of event lists, recorded in order."""
-        torch, snn, net = self.torch, self.snn, self.net
+        """One pass of the whole path. ev: dict of event lists, recorded in order (outside any graph)."""
+        snn, net = self.snn, self.net
         T, B, L = self.T, self.B, self.L
         main, aux = self.main, self.aux
+        R = self.region
         E = lambda k: ev[k]  # noqa: E731
+        with_dense = dense and not self.args.no_dense
         E("fwd0").record(main)
-        net.forward(None if self.args.unfused else self.b_th)
+        R("fwd", main, lambda: net.forward(None if self.args.unfused else self.b_th))
         E("fwd1").record(main)
-        r = net.readout(dense=dense and not self.args.no_dense)
+        r = R("readout" + ("d" if with_dense else ""), main, lambda: net.readout(dense=with_dense))
         E("cmp0").record(main)
-        cs = net.compact(self.b_th, self.caps)
+        cs = R("compact", main, lambda: net.compact(self.b_th, self.caps))
         E("cmp1").record(main)
-        _, eps = snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1], inp=cs[L - 1],
-                                     ws=self.ws_ro, aux_stream=None if self.args.serial else aux)
+        use_aux = not (self.args.serial or self.args.graph)
+        eps = R("ro_bwd", main, lambda: snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1],
+                                                             inp=cs[L - 1], ws=self.ws_ro,
+                                                             aux_stream=aux if use_aux else None)[1])
         E("ro1").record(main)
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
@@ -274,26 +309,34 @@ class Runner:
                 if aux is not main:
                     aux.wait_stream(main)
                 ev["gi0"][i].record(aux)
-                snn.sparse_grad_in(net.Ws[l], net.alphas[l], T, B, cs[l], eps, cs[l - 1],
-                                   share_cu=self.share[l] and aux is not main,
-                                   ws=self.ws_gi, stream=aux, eps_in=self.eps[l - 1])
+                R(f"gi{l}", aux, lambda l=l, eps=eps: snn.sparse_grad_in(
+                    net.Ws[l], net.alphas[l], T, B, cs[l], eps, cs[l - 1], share_cu=self.share[l] and aux is not main,
+                    ws=self.ws_gi, eps_in=self.eps[l - 1]))
                 ev["gi1"][i].record(aux)
             ev["dw0"][i].record(main)
-            snn.sparse_dw(net.trace[l], cs[l], eps, net.Ws[l].shape[1], ws=self.ws_dw[l], stream=main,
-                          dW=self.dW[l])
+            R(f"dw{l}", main, lambda l=l, eps=eps: snn.sparse_dw(net.trace[l], cs[l], eps, net.Ws[l].shape[1],
+                                                                ws=self.ws_dw[l], dW=self.dW[l]))
             ev["dw1"][i].record(main)
             if l > 0:
                 if aux is not main:
                     main.wait_stream(aux)
                 eps = self.eps[l - 1]
             ev["lay1"][i].record(main)
-        if dense and not self.args.no_dense:
-            _, e = snn.dense_backward_ref(net.W_out, net.trace_out, net.V_out, r[3], net.alpha_out, math.inf,
-                                          math.inf, net.beta, grad_in=True, ws=self.ws_dn)
+        if with_dense:
+            def dense_chain():
+                _, e = snn.dense_backward_ref(net.W_out, net.trace_out, net.V_out, r[3], net.alpha_out, math.inf,
+                                              math.inf, net.beta, grad_in=True, ws=self.ws_dn)
+                return e
+            e_top = R("dense_ro", main, dense_chain)
+
+            def dense_layers():
+                e = e_top
+                for l in range(L - 1, -1, -1):
+                    _, e = snn.dense_backward_ref(net.Ws[l], net.trace[l], net.V[l], e, net.alphas[l], net.theta,
+                                                  self.b_th, net.beta, grad_in=l > 0, ws=self.ws_dn)
+                return e
             E("dn0").record(main)
-            for l in range(L - 1, -1, -1):
-                _, e = snn.dense_backward_ref(net.Ws[l], net.trace[l], net.V[l], e, net.alphas[l], net.theta,
-                                              self.b_th, net.beta, grad_in=l > 0, ws=self.ws_dn)
+            R("dense", main, dense_layers)
             E("dn1").record(main)
         return cs
 
@@ -364,6 +407,14 @@ class Runner:
         achieved = dw_flops / dw_s / 1e12
         value = sum(nnz) / (med(t_sparse) * 1e-3)
         mem = self.memory(nnz)
+        # whole sparse backward on its gathered bytes (compaction: V read... here the bitset, the
+        # CSR and g written; layers: dW and spike-gradient bytes), against the HBM peak
+        cmp_bytes = sum(4 * (T * B + 1) + 8 * nnz[l] + (4 * T * B * sizes[l + 1] if self.args.unfused else
+                                                          T * ((B * sizes[l + 1] + 63) // 64) * 8 + 4 * nnz[l])
+                        for l in range(L))
+        sparse_bytes = cmp_bytes + sum(p[0] + p[2] for p in per)
+        # dense chain: dW GEMM of every LIF layer and the spike-gradient GEMM of all but the first
+        dense_flops = sum(2 * T * B * sizes[l] * sizes[l + 1] * (2 if l > 0 else 1) for l in range(L))
         traffic = None
         if os.path.exists(TRAFFIC_FILE):
             with open(TRAFFIC_FILE) as f:
@@ -406,9 +457,14 @@ class Runner:
                 "algorithmic_flops": dw_flops, "algorithmic_bytes": dw_bytes, "launch_ms": dw_ms,
                 "hbm_achieved_gbs": dw_bytes / dw_s / 1e9, "hbm_frac": dw_bytes / dw_s / 1e9 / HBM_PEAK_GBS,
             },
+            "sparse_backward_gathered_bytes": sparse_bytes,
+            "sparse_backward_hbm_gbs": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9,
+            "sparse_backward_hbm_frac": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "wall_s_timed": wall,
         }
         if out["dense_backward_ms"] is not None:
+            out["dense_mfma_tflops"] = dense_flops / (out["dense_backward_ms"] * 1e-3) / 1e12
+            out["dense_mfma_frac"] = out["dense_mfma_tflops"] / MFMA_F32_TFLOPS
             out["speedup_vs_dense"] = out["dense_backward_ms"] / out["sparse_backward_ms"]
             out["overall_speedup_fwd_plus_bwd"] = (out["forward_ms"] + out["dense_backward_ms"]) / (
                 out["forward_ms"] + out["sparse_backward_ms"])
@@ -430,6 +486,8 @@ def main():
                     help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
+    ap.add_argument("--graph", action="store_true",
+                    help="each library call of the step captured once as a HIP graph and replayed")
     ap.add_argument("--train", action="store_true",
                     help="training runs, sparse vs full surrogate (App. E); prints one JSON line")
     ap.add_argument("--train-workload", default="latency_train")
@@ -437,6 +495,7 @@ def main():
     ap.add_argument("--train-batches", type=int, default=20, help="batches in the synthetic training set")
     ap.add_argument("--lr", type=float, default=2e-4)
     ap.add_argument("--nu-up", type=float, default=1.0)
+    ap.add_argument("--train-bth", default="", help="comma-separated bands of the sparse runs (default: the workload's)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the path is single-device here (multi-GPU is design only)",

@@ -148,25 +148,35 @@ class Network:
         return list(self.Ws) + [self.W_out]
 
     def train_step(self, opt: "Adam", b_th: float, reg: Optional["Penalty"] = None, sparse: bool = True,
-                   aux_stream=None):
+                   aux_stream=None, events=None):
         """One training step (App. E): forward, cross-entropy plus activity penalties, the sparse
         (or, with sparse=False, the dense) backward with truncation band b_th, and an Adam step on
         every weight matrix in place. b_th = inf with sparse=False is full-surrogate BPTT.
+        events: optional list of 6 timing events recorded on the current stream at the phase
+        boundaries (start, after forward, after loss and penalties, after compaction, after the
+        backward, after Adam).
         Returns a dict of device tensors: ce [1], penalty [1] (all layers), grads (list), nnz."""
+        mark = (lambda k: events[k].record()) if events is not None else (lambda k: None)
+        mark(0)
         self.forward(b_th if sparse and math.isfinite(b_th) else None)
+        mark(1)
         acts = self.activity(reg) if reg is not None else None
         coefs = [a[0] for a in acts] if acts else None
+        ro = self.readout(dense=not sparse)
+        mark(2)
         if sparse:
-            ro = self.readout()
             csrs = self.compact(b_th)
+            mark(3)
             dWs, dW_out, _ = self.sparse_backward(csrs, ro, aux_stream=aux_stream, reg_coefs=coefs)
             nnz = [c.nnz_dev for c in csrs]
         else:
-            ro = self.readout(dense=True)
+            mark(3)
             dWs, dW_out, _ = self.dense_backward(b_th, ro, reg_coefs=coefs)
             nnz = None
+        mark(4)
         grads = list(dWs) + [dW_out]
         opt.step(grads)
+        mark(5)
         pen = sum(a[1] for a in acts) if acts else torch.zeros(1, device=self.X.device)
         return {"ce": ro[2], "penalty": pen, "grads": grads, "nnz": nnz}
 
@@ -195,6 +205,26 @@ class Adam:
         self.k += 1
         for p, g, m, v in zip(self.params, grads, self.m, self.v):
             snn.adam_step(p, g, m, v, self.k, self.lr, self.betas, self.eps)
+
+
+class Graphed:
+    """Library calls captured once as a HIP graph and replayed. fn makes its calls on the current
+    stream (the capture stream) and returns what later work reads; those tensors stay the
+    outputs of every replay. Capture records work without running it, so replay before reading."""
+
+    def __init__(self, fn, stream=None):
+        self.graph = torch.cuda.CUDAGraph()
+        cur = stream or torch.cuda.current_stream()
+        cap = torch.cuda.Stream()  # default priority
+        cap.wait_stream(cur)
+        with torch.cuda.graph(self.graph, stream=cap):
+            self.out = fn()
+        cur.wait_stream(cap)
+
+    def __call__(self, stream=None):
+        with torch.cuda.stream(stream or torch.cuda.current_stream()):
+            self.graph.replay()
+        return self.out
 
 
 def from_inputs(inp, device="cuda") -> Network:

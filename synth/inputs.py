@@ -95,6 +95,11 @@ CONFIGS = {
         loss_mode="max", b_th=0.2, kind="classlatency",
         description="class-conditional latency code (F-MNIST-like training task): 28x28 class templates plus "
                     "noise, one spike per input at most; LIF 784->200->200, readout 200->10"),
+    "deep": Config(
+        "deep", 7, T=100, B=256, sizes=(784, 300, 300, 300, 300, 300, 10), tau_ratio_hidden=0.1,
+        tau_ratio_out=0.1, loss_mode="max", b_th=0.2, kind="classlatency",
+        description="five LIF layers of 300 on the class-conditional latency code (F-MNIST-like): "
+                    "784->300->300->300->300->300, readout 300->10, T=100, B=256"),
 }
 
 

@@ -148,6 +148,9 @@ def _ragged_sum():
     ("stress", list(range(8)), 0.02),
     ("stress", list(range(8)), 0.2),
     ("stress", list(range(8)), 0.8),
+    ("deep", list(range(32)), 0.2),
+    ("deep", list(range(16)), 0.95),
+    ("latency_train", list(range(32)), 0.2),
 ])
 def test_parity_configs(name, batch, b_th):
     print(f"\n[case] {name} batch={'all' if batch is None else len(batch)} b_th={b_th}", flush=True)
@@ -417,3 +420,46 @@ def test_fused_bits_capacity_overflow():
     assert int(nnz_dev.item()) == nnz
     assert torch.equal(col[:cap], full.col_idx[:cap]) and torch.equal(gg[:cap], full.g[:cap])
     assert bool((col[cap:] == -7).all()) and bool((gg[cap:] == -7.0).all())
+
+
+def test_graph_replays_match_eager():
+    """Readout loss, compaction and the sparse backward chain captured once as HIP graphs and
+    replayed three times; between replays the weights change and the forward runs eagerly. Each
+    replay equals an eager run on the same state: CSR, loss and spike gradients bit for bit, dW
+    to float64-accumulation order (its LDS adds are unordered)."""
+    inp = _case("deep", list(range(16)))
+    net = pipeline.from_inputs(inp).allocate()
+    b_th = 0.2
+    net.forward(b_th)
+    caps = [2 * c.nnz() + 4096 for c in net.compact(b_th)]
+    g_ro = pipeline.Graphed(lambda: net.readout())
+    g_cmp = pipeline.Graphed(lambda: net.compact(b_th, caps))
+    g_bwd = pipeline.Graphed(lambda: net.sparse_backward(g_cmp.out, g_ro.out))
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    for rep in range(3):
+        print(f"\n[case] graph replay {rep}", flush=True)
+        with torch.no_grad():
+            for W in net.Ws:
+                W.mul_(1.0 + 0.02 * torch.randn(W.shape, device=W.device, generator=gen))
+        net.forward(b_th)
+        ro_g = g_ro()
+        cs_g = g_cmp()
+        dW_g, dWo_g, eps_g = g_bwd()
+        torch.cuda.synchronize()
+        snap = {"loss": ro_g[2].clone(), "rp": [c.row_ptr.clone() for c in cs_g],
+                "col": [c.col_idx.clone() for c in cs_g], "nnz": [c.nnz() for c in cs_g],
+                "dW": [d.clone() for d in dW_g], "dWo": dWo_g.clone(), "eps": [e.clone() for e in eps_g]}
+        ro_e = net.readout()
+        cs_e = net.compact(b_th, caps)
+        dW_e, dWo_e, eps_e = net.sparse_backward(cs_e, ro_e)
+        torch.cuda.synchronize()
+        assert torch.equal(snap["loss"], ro_e[2])
+        for l in range(net.L):
+            n = cs_e[l].nnz()
+            assert n == snap["nnz"][l] and n <= caps[l]
+            assert torch.equal(snap["rp"][l], cs_e[l].row_ptr)
+            assert torch.equal(snap["col"][l][:n], cs_e[l].col_idx[:n])
+            assert torch.equal(snap["eps"][l][:n], eps_e[l][:n])
+            d = (snap["dW"][l] - dW_e[l]).abs().max().item()
+            assert d <= 1e-6 * dW_e[l].abs().max().item() + 1e-30, (l, d)
+        assert (snap["dWo"] - dWo_e).abs().max().item() <= 1e-6 * dWo_e.abs().max().item() + 1e-30

@@ -49,3 +49,28 @@ def test_inputs_bundle_shapes():
         assert [W.shape for W in inp.Ws] == [(cfg.sizes[l], cfg.sizes[l + 1]) for l in range(cfg.n_layers)]
         assert inp.W_out.shape == (cfg.sizes[-2], cfg.sizes[-1]) and inp.W_out.dtype == np.float32
         assert inp.labels.shape == (2,) and inp.labels.max() < cfg.sizes[-1]
+
+
+def test_class_latency_code():
+    """Class-conditional latency code: at most one spike per input, brighter template pixels
+    fire earlier, labels are a function of the sample index, and classes differ."""
+    from synth.inputs import class_templates, label_of, LAT_TAU_EFF, LAT_THETA
+    cfg = CONFIGS["latency_train"]
+    x = make_spikes(cfg, range(64))
+    assert x.sum(axis=0).max() == 1
+    y = make_inputs(cfg, range(64)).labels
+    assert all(int(y[k]) == label_of(cfg, k) for k in range(64))
+    assert np.array_equal(make_inputs(cfg, [70, 3]).labels, [label_of(cfg, 70), label_of(cfg, 3)])
+    tm = class_templates(cfg)
+    assert tm.shape == (10, 784) and tm.min() >= 0 and tm.max() <= 1
+    # a pixel of intensity 1 fires at floor(tau ln(1 / (1 - theta))) without noise
+    assert int(np.floor(LAT_TAU_EFF * np.log(1.0 / (1.0 - LAT_THETA)))) == 4
+    # mean spike time of bright template pixels is earlier than of dim ones
+    t = np.argmax(x, axis=0).astype(float)
+    fired = x.sum(axis=0) > 0
+    bright = np.array([tm[y[b]] > 0.7 for b in range(64)])
+    dim = np.array([tm[y[b]] < 0.1 for b in range(64)])
+    assert t[fired & bright].mean() + 5 < t[fired & dim].mean()
+    # class templates are distinct
+    d = np.abs(tm[:, None] - tm[None]).sum(axis=2)
+    assert d[~np.eye(10, dtype=bool)].min() > 10
