@@ -28,12 +28,16 @@ What it computes, and where the paper defines it:
 * adam.py     -- the Adam update (App. E's optimiser; Kingma and Ba, Algorithm 1).
 * train.py    -- a whole training step (loss with penalties, gradient, Adam) and
   the sparse vs full-surrogate gradient difference of App. H.
+* conv.py     -- the convolutional spiking layer (3x3, padding 1) with 2x2 max
+  pooling of its spikes into the readout (Sec. 3's convolutional experiment, App. E):
+  forward through the layer's Toeplitz matrix, pooling, gradient routed back through
+  the pooling, filter gradient.
 * smooth.py   -- a smoothed-surrogate model whose exact gradient is the
   truncated-surrogate BPTT gradient; finite differences of it pin O2.
 
 Parity status: every function here is pinned by tests in tests/test_oracle_*.py
 (closed forms, finite differences, autograd, limits, the App. C example,
-torch.optim.Adam).
+torch.optim.Adam, torch's conv2d and max_pool2d).
 The paper's experimental numbers themselves are parity unpinned: they need the
 datasets, trained weights or the authors' GPUs.
 """
