@@ -260,6 +260,83 @@ snn_status snn_activity_reg_grad(const float* coef, int T, int B, int N, const i
 snn_status snn_adam_step(float* W, const float* grad, float* m, float* v, int64_t n, float lr, float beta1,
                          float beta2, float eps, int step, void* stream);
 
+/*
+ * Convolutional LIF layer, forward (the convolutional experiment of Sec. 3; App. E: 3x3 filters,
+ * stride 1). Zero padding 1, channels last.
+ *   s_in   [T,B,H,W,C] uint8 input spikes (read; nonzero = spike)
+ *   Wc     [3,3,C,F] float32 filters (ky, kx, c, f); output (y, x) reads input (y+ky-1, x+kx-1)
+ *   V      [T,B,H*W*F] float32 (written), neuron n = (y*W + x)*F + f
+ *   s_out  [T,B,H*W*F] uint8 spikes (written)
+ *   trace_in [T,B,H*W*C] float32 input trace (written unless NULL)
+ *   active_bits (written unless NULL): the active set with band b_th, in the layout of
+ *          snn_lif_forward_active with N = H*W*F (snn_active_bits_words(T, B, H*W*F) words)
+ * The layer is a LIF layer whose weighted input is the convolution (its Toeplitz matrix): the
+ * weighted input is summed over spiking inputs in ascending input index (y', x', c) in float32
+ * from +0.0, then the recurrence of snn_lif_forward; results are bit-identical to
+ * snn_lif_forward on that matrix.
+ */
+snn_status snn_conv_lif_forward(const uint8_t* s_in, const float* Wc, int T, int B, int H, int W, int C, int F,
+                                float alpha, float theta, float b_th, float* V, uint8_t* s_out, float* trace_in,
+                                uint64_t* active_bits, void* stream);
+
+/*
+ * 2x2 max pooling (stride 2) of a convolutional layer's spikes [T,B,H,W,F] (H, W even):
+ *   P   [T,B,H/2,W/2,F] uint8 (written): OR of the window
+ *   arg [T,B,H/2,W/2,F] uint8 (written): window position (0..3, row-major) of the first spike,
+ *       0 when none; the window's gradient goes to that element (first maximal element).
+ */
+snn_status snn_maxpool_spikes(const uint8_t* S, int T, int B, int H, int W, int F, uint8_t* P, uint8_t* arg,
+                              void* stream);
+
+/*
+ * The pooled layer's share of the active set: pooled neuron (t, b, np) is active iff the conv
+ * neuron its pooling picked (arg) is active in conv_bits. Both bitsets in the layout of
+ * snn_lif_forward_active (N = H*W*F for conv_bits, (H/2)*(W/2)*F for pool_bits, written).
+ * snn_active_compact_bits(pool_bits, V = NULL, ..., g_act = NULL) gives its CSR, the input-side
+ * CSR of the readout's snn_sparse_backward.
+ */
+snn_status snn_pool_route_bits(const uint64_t* conv_bits, const uint8_t* arg, int T, int B, int H, int W, int F,
+                               uint64_t* pool_bits, void* stream);
+
+/*
+ * Routes the readout's spike gradient at the pooled entries (eps_pool, aligned with the pooled
+ * CSR) to the conv layer's CSR: eps_conv[e] = eps_pool of the pooled entry whose pooling picked
+ * conv entry e, else 0. eps_conv float32 [conv_cap] (written for e < conv_cap). Entries past the
+ * capacities are ignored; columns are found by binary search (rows ascending, as compaction
+ * writes them).
+ */
+snn_status snn_pool_scatter_eps(int T, int B, int H, int W, int F, const int32_t* pool_row_ptr,
+                                const int32_t* pool_col_idx, int64_t pool_cap, const float* eps_pool,
+                                const uint8_t* arg, const int32_t* conv_row_ptr, const int32_t* conv_col_idx,
+                                int64_t conv_cap, float* eps_conv, void* stream);
+
+/* Dense form: eps_conv [T,B,H*W*F] (written) from eps_pool [T,B,(H/2)*(W/2)*F] (read). */
+snn_status snn_pool_scatter_eps_dense(const float* eps_pool, const uint8_t* arg, int T, int B, int H, int W, int F,
+                                      float* eps_conv, void* stream);
+
+/*
+ * Sparse filter gradient of the convolutional layer (Eq. (w_grad) with the filter's shared
+ * weights): dWc[ky,kx,c,f] = sum over its active entries (t,b,y,x,f) of eps*g times
+ * trace_in[t,b,y+ky-1,x+kx-1,c]. conv CSR and g from snn_active_compact_bits; eps_conv from
+ * snn_pool_scatter_eps; conv_g may be NULL (g = 1). dWc [3,3,C,F] float32 (overwritten).
+ * SNN_ERR_UNSUPPORTED when C*F > 2048. Float64 accumulation.
+ */
+size_t snn_conv_sparse_dw_workspace(int T, int B, int H, int W, int C, int F);
+snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, int H, int W, int C, int F,
+                              const int32_t* conv_row_ptr, const int32_t* conv_col_idx, const float* conv_g,
+                              const float* eps_conv, int64_t conv_cap, float* dWc, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/*
+ * Dense filter gradient (the baseline): every neuron's G = eps_conv * g(V) * [|V - theta| < b_th]
+ * (b_th = +INFINITY: full surrogate) with eps_conv dense [T,B,H*W*F], then the same sum.
+ * SNN_ERR_UNSUPPORTED when C > 4.
+ */
+size_t snn_conv_dense_dw_workspace(int T, int B, int H, int W, int C, int F);
+snn_status snn_conv_dense_dw(const float* trace_in, const float* V, const float* eps_conv, int T, int B, int H, int W,
+                             int C, int F, float theta, float b_th, float beta, float* dWc, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,6 +26,7 @@ SOURCES = [
     "dense_backward.hip",
     "readout_ce.hip",
     "train_step.hip",
+    "conv_layer.hip",
 ]
 # The forward and the compaction decide spikes and active sets, which must be bit-exact:
 # no contraction of a*b+c into fused multiply-adds there.

@@ -1,0 +1,375 @@
+// The convolutional spiking layer's pooling and backward (the convolutional experiment of
+// Sec. 3; network details in App. E): 2x2 max pooling of its spikes into the readout, the
+// pooling's share of the active set, the readout's spike gradient routed back through the
+// pooling, and the filter gradient, sparse (at the layer's active entries) and dense.
+//
+// Layout: channels last. Conv neuron n = (y * W + x) * F + f of N = H * W * F; pooled neuron
+// np = (py * (W/2) + px) * F + f of Np = (H/2) * (W/2) * F; rows r = t * B + b. Filters
+// Wc [3, 3, C, F], output (y, x) reading input (y + ky - 1, x + kx - 1) (zero padding).
+// Pooling: P = OR of the 2x2 window; arg = the window position (0..3, row-major) of the first
+// spike, 0 when none; the window's gradient goes to that element.
+
+#include <algorithm>
+
+#include "common.h"
+
+namespace snn {
+namespace {
+
+constexpr int kCdwThreads = 256;
+constexpr int kCdwWaves = kCdwThreads / kWave;
+constexpr int kCdwMaxBlocks = 1024;
+constexpr int kDenseMaxC = 4;  // input channels held in registers by the dense filter gradient
+
+unsigned stream_blocks(int64_t items) {
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 65536));
+}
+
+__global__ void pool_kernel(const uint8_t* __restrict__ S, int H, int W, int F, int64_t total,
+                            uint8_t* __restrict__ P, uint8_t* __restrict__ arg) {
+  const int hw = W / 2;
+  const int hh = H / 2;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int f = (int)(i % F);
+    int64_t rest = i / F;
+    const int px = (int)(rest % hw);
+    rest /= hw;
+    const int py = (int)(rest % hh);
+    const int64_t tb = rest / hh;
+    const int64_t base = ((tb * H + 2 * py) * W + 2 * px) * F + f;
+    const bool s0 = S[base] != 0;
+    const bool s1 = S[base + F] != 0;
+    const bool s2 = S[base + (int64_t)W * F] != 0;
+    const bool s3 = S[base + (int64_t)W * F + F] != 0;
+    P[i] = (uint8_t)(s0 | s1 | s2 | s3);
+    arg[i] = (uint8_t)(s0 ? 0 : (s1 ? 1 : (s2 ? 2 : (s3 ? 3 : 0))));
+  }
+}
+
+// Pooled neuron (t, kp = b * Np + np) is active iff the conv neuron its pooling picked is
+// active: one ballot per wavefront and step writes one word of the pooled bitset.
+__global__ void route_bits_kernel(const uint64_t* __restrict__ cbits, const uint8_t* __restrict__ arg, int T, int B,
+                                  int H, int W, int F, uint64_t* __restrict__ pbits) {
+  const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
+  const int64_t N = (int64_t)H * W * F;
+  const int64_t W64p = (B * Np + kWave - 1) / kWave;
+  const int64_t W64c = (B * N + kWave - 1) / kWave;
+  const int64_t total = (int64_t)T * W64p * kWave;
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g - lane_id() < total;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t t = g / (W64p * kWave);
+    const int64_t kp = g - t * W64p * kWave;
+    bool on = false;
+    if (g < total && kp < B * Np) {
+      const int64_t b = kp / Np;
+      const int64_t np_ = kp - b * Np;
+      const int f = (int)(np_ % F);
+      const int64_t pp = np_ / F;
+      const int px = (int)(pp % (W / 2));
+      const int py = (int)(pp / (W / 2));
+      const int a = arg[(t * B + b) * Np + np_] & 3;
+      const int64_t kc = b * N + ((int64_t)(2 * py + (a >> 1)) * W + 2 * px + (a & 1)) * F + f;
+      on = (cbits[t * W64c + kc / kWave] >> (kc % kWave)) & 1ull;
+    }
+    const uint64_t m = __ballot(on);
+    if (lane_id() == 0 && g < total) pbits[t * W64p + kp / kWave] = m;
+  }
+}
+
+__global__ void fill_zero_f(float* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0.0f;
+}
+
+// One wavefront per row: each pooled entry's gradient goes to the conv entry its pooling
+// picked, found by binary search in the conv row (columns ascending). Entries are clamped to
+// the capacities; a conv neuron that is not in the conv row receives nothing.
+__global__ void scatter_kernel(int TB, int H, int W, int F, const int32_t* __restrict__ prp,
+                               const int32_t* __restrict__ pcol, int64_t pcap, const float* __restrict__ eps_p,
+                               const uint8_t* __restrict__ arg, const int32_t* __restrict__ crp,
+                               const int32_t* __restrict__ ccol, int64_t ccap, float* __restrict__ eps_c) {
+  const int Np = (H / 2) * (W / 2) * F;
+  const int r = (int)(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave);
+  if (r >= TB) return;
+  const int64_t e0 = std::min<int64_t>(std::max(prp[r], 0), pcap);
+  const int64_t e1 = std::min<int64_t>(std::max(prp[r + 1], 0), pcap);
+  const int64_t c0 = std::min<int64_t>(std::max(crp[r], 0), ccap);
+  const int64_t c1 = std::min<int64_t>(std::max(crp[r + 1], 0), ccap);
+  for (int64_t e = e0 + lane_id(); e < e1; e += kWave) {
+    const int np_ = pcol[e];
+    if ((unsigned)np_ >= (unsigned)Np) continue;
+    const int f = np_ % F;
+    const int pp = np_ / F;
+    const int px = pp % (W / 2);
+    const int py = pp / (W / 2);
+    const int a = arg[(int64_t)r * Np + np_] & 3;
+    const int n = ((2 * py + (a >> 1)) * W + 2 * px + (a & 1)) * F + f;
+    int64_t lo = c0, hi = c1;  // first position with col >= n
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (ccol[mid] < n) lo = mid + 1;
+      else hi = mid;
+    }
+    if (lo < c1 && ccol[lo] == n) eps_c[lo] = eps_p[e];
+  }
+}
+
+// Dense form: eps_c[t,b,y,x,f] = eps_p[t,b,y/2,x/2,f] where (y, x) is the picked element, else 0.
+__global__ void scatter_dense_kernel(const float* __restrict__ eps_p, const uint8_t* __restrict__ arg, int H, int W,
+                                     int F, int64_t total, float* __restrict__ eps_c) {
+  const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
+  const int64_t N = (int64_t)H * W * F;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = i / N;
+    const int n = (int)(i - r * N);
+    const int f = n % F;
+    const int pix = n / F;
+    const int y = pix / W;
+    const int x = pix - y * W;
+    const int64_t ip = r * Np + ((int64_t)(y / 2) * (W / 2) + x / 2) * F + f;
+    eps_c[i] = (int)(arg[ip] & 3) == (y & 1) * 2 + (x & 1) ? eps_p[ip] : 0.0f;
+  }
+}
+
+// Sparse filter gradient: blocks take contiguous row ranges, wavefronts rows, lanes the row's
+// entries; an entry with G = eps * g != 0 adds G * trace over its 3x3xC input patch into the
+// block's float64 accumulator [9 * C][F] in LDS. Each block writes its sums; a fixed-order
+// reduction over blocks gives dWc.
+__global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
+    const float* __restrict__ trace, int TB, int H, int W, int C, int F, const int32_t* __restrict__ rp,
+    const int32_t* __restrict__ col, const float* __restrict__ g, const float* __restrict__ eps, int64_t cap,
+    int rows_per_block, double* __restrict__ part) {
+  extern __shared__ double cacc[];  // [9 * C * F]
+  const int nacc = 9 * C * F;
+  for (int i = threadIdx.x; i < nacc; i += kCdwThreads) cacc[i] = 0.0;
+  __syncthreads();
+  const int N = H * W * F;
+  const int r_lo = blockIdx.x * rows_per_block;
+  const int r_hi = min(TB, r_lo + rows_per_block);
+  const int w = threadIdx.x / kWave;
+  for (int r = r_lo + w; r < r_hi; r += kCdwWaves) {
+    const int64_t e0 = std::min<int64_t>(std::max(rp[r], 0), cap);
+    const int64_t e1 = std::min<int64_t>(std::max(rp[r + 1], 0), cap);
+    const float* tr = trace + (int64_t)r * H * W * C;
+    for (int64_t e = e0 + lane_id(); e < e1; e += kWave) {
+      const int n = col[e];
+      if ((unsigned)n >= (unsigned)N) continue;
+      const float G = g ? eps[e] * g[e] : eps[e];
+      if (G == 0.0f) continue;
+      const int f = n % F;
+      const int pix = n / F;
+      const int y = pix / W;
+      const int x = pix - y * W;
+      for (int ky = 0; ky < 3; ++ky) {
+        const int yy = y + ky - 1;
+        if (yy < 0 || yy >= H) continue;
+        for (int kx = 0; kx < 3; ++kx) {
+          const int xx = x + kx - 1;
+          if (xx < 0 || xx >= W) continue;
+          const float* tp = tr + ((int64_t)yy * W + xx) * C;
+          for (int c = 0; c < C; ++c) atomicAdd(&cacc[((ky * 3 + kx) * C + c) * F + f], (double)G * (double)tp[c]);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nacc; i += kCdwThreads) part[(int64_t)blockIdx.x * nacc + i] = cacc[i];
+}
+
+__global__ void reduce_parts(const double* __restrict__ part, int n_parts, int n, float* __restrict__ out) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    double s = 0.0;
+    for (int p = 0; p < n_parts; ++p) s += part[(int64_t)p * n + i];
+    out[i] = (float)s;
+  }
+}
+
+// Dense filter gradient of the full (b_th = inf) or truncated surrogate: every position
+// (t, b, y, x) and filter f. Lane = filter (F <= 64 per wavefront pass), wavefronts take
+// positions; G = eps * g(V) * [|V - theta| < b_th] and the patch's trace values (uniform across
+// the wavefront) go into 9 * C float32 registers per lane; blocks then sum their wavefronts in
+// LDS (float64 sums) and write float64 partial sums.
+template <int CMAX>
+__global__ __launch_bounds__(kCdwThreads) void conv_dw_dense_kernel(
+    const float* __restrict__ trace, const float* __restrict__ V, const float* __restrict__ eps, int64_t n_pos,
+    int H, int W, int C, int F, float theta, float b_th, float beta, int64_t pos_per_block, double* __restrict__ part) {
+  __shared__ float red[kCdwWaves][9 * CMAX][kWave];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  const int nacc = 9 * C * F;
+  const int64_t p_lo = (int64_t)blockIdx.x * pos_per_block;
+  const int64_t p_hi = std::min<int64_t>(n_pos, p_lo + pos_per_block);
+  for (int f0 = 0; f0 < F; f0 += kWave) {
+    const int f = f0 + l;
+    const bool fv = f < F;
+    float acc[9 * CMAX];
+#pragma unroll
+    for (int q = 0; q < 9 * CMAX; ++q) acc[q] = 0.0f;
+    for (int64_t p = p_lo + w; p < p_hi; p += kCdwWaves) {
+      float G = 0.0f;
+      if (fv) {
+        const float v = V[p * F + f];
+        const float d = fabsf(v - theta);
+        const float q = beta * d + 1.0f;
+        G = d < b_th ? eps[p * F + f] / (q * q) : 0.0f;
+      }
+      if (__ballot(G != 0.0f) == 0ull) continue;
+      const int64_t r = p / ((int64_t)H * W);
+      const int pix = (int)(p - r * H * W);
+      const int y = pix / W;
+      const int x = pix - y * W;
+      const float* tr = trace + r * (int64_t)H * W * C;
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        const int yy = y + ky - 1;
+#pragma unroll
+        for (int kx = 0; kx < 3; ++kx) {
+          const int xx = x + kx - 1;
+          const bool in = yy >= 0 && yy < H && xx >= 0 && xx < W;
+#pragma unroll
+          for (int c = 0; c < CMAX; ++c)
+            if (c < C && in) acc[(ky * 3 + kx) * CMAX + c] += G * tr[((int64_t)yy * W + xx) * C + c];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 9 * CMAX; ++q) red[w][q][l] = acc[q];
+    __syncthreads();
+    for (int i = threadIdx.x; i < 9 * C * kWave; i += kCdwThreads) {
+      const int tap = i / (C * kWave);
+      const int c = (i / kWave) % C;
+      const int ll = i % kWave;
+      if (f0 + ll < F) {
+        double s = 0.0;
+        for (int ww = 0; ww < kCdwWaves; ++ww) s += (double)red[ww][tap * CMAX + c][ll];
+        part[(int64_t)blockIdx.x * nacc + (tap * C + c) * F + f0 + ll] = s;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+bool conv_dims_ok(int T, int B, int H, int W, int F) {
+  if (bad_dim(T) || bad_dim(B) || bad_dim(H) || bad_dim(W) || bad_dim(F)) return false;
+  if ((H & 1) || (W & 1)) return false;  // 2x2 pooling with stride 2
+  if ((int64_t)H * W * F >= ((int64_t)1 << 31)) return false;
+  return !too_big(T, B, H * W * F);
+}
+
+int cdw_blocks(int TB) { return std::max(1, std::min(kCdwMaxBlocks, TB)); }
+
+int64_t dense_blocks(int64_t n_pos) { return std::max<int64_t>(1, std::min<int64_t>(kCdwMaxBlocks, (n_pos + 63) / 64)); }
+
+}  // namespace
+}  // namespace snn
+
+using namespace snn;
+
+extern "C" snn_status snn_maxpool_spikes(const uint8_t* S, int T, int B, int H, int W, int F, uint8_t* P,
+                                         uint8_t* arg, void* stream) {
+  if (!S || !P || !arg) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
+  const int64_t total = (int64_t)T * B * (H / 2) * (W / 2) * F;
+  hipLaunchKernelGGL(pool_kernel, dim3(stream_blocks(total)), dim3(256), 0, static_cast<hipStream_t>(stream), S, H, W,
+                     F, total, P, arg);
+  return launch_status();
+}
+
+extern "C" snn_status snn_pool_route_bits(const uint64_t* conv_bits, const uint8_t* arg, int T, int B, int H, int W,
+                                          int F, uint64_t* pool_bits, void* stream) {
+  if (!conv_bits || !arg || !pool_bits) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
+  const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
+  const int64_t total = (int64_t)T * ((B * Np + kWave - 1) / kWave) * kWave;
+  hipLaunchKernelGGL(route_bits_kernel, dim3(stream_blocks(total)), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     conv_bits, arg, T, B, H, W, F, pool_bits);
+  return launch_status();
+}
+
+extern "C" snn_status snn_pool_scatter_eps(int T, int B, int H, int W, int F, const int32_t* pool_row_ptr,
+                                           const int32_t* pool_col_idx, int64_t pool_cap, const float* eps_pool,
+                                           const uint8_t* arg, const int32_t* conv_row_ptr,
+                                           const int32_t* conv_col_idx, int64_t conv_cap, float* eps_conv,
+                                           void* stream) {
+  if (!pool_row_ptr || !arg || !conv_row_ptr || !eps_conv) return SNN_ERR_INVALID_ARG;
+  if (pool_cap < 0 || conv_cap < 0) return SNN_ERR_INVALID_ARG;
+  if (pool_cap > 0 && (!pool_col_idx || !eps_pool)) return SNN_ERR_INVALID_ARG;
+  if (conv_cap > 0 && !conv_col_idx) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (conv_cap == 0) return SNN_OK;
+  hipLaunchKernelGGL(fill_zero_f, dim3(stream_blocks(conv_cap)), dim3(256), 0, s, eps_conv, conv_cap);
+  const int TB = T * B;
+  if (pool_cap > 0)
+    hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)(((int64_t)TB * kWave + 255) / 256)), dim3(256), 0, s, TB, H, W,
+                       F, pool_row_ptr, pool_col_idx, pool_cap, eps_pool, arg, conv_row_ptr, conv_col_idx, conv_cap,
+                       eps_conv);
+  return launch_status();
+}
+
+extern "C" snn_status snn_pool_scatter_eps_dense(const float* eps_pool, const uint8_t* arg, int T, int B, int H, int W,
+                                                 int F, float* eps_conv, void* stream) {
+  if (!eps_pool || !arg || !eps_conv) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
+  const int64_t total = (int64_t)T * B * H * W * F;
+  hipLaunchKernelGGL(scatter_dense_kernel, dim3(stream_blocks(total)), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     eps_pool, arg, H, W, F, total, eps_conv);
+  return launch_status();
+}
+
+extern "C" size_t snn_conv_sparse_dw_workspace(int T, int B, int H, int W, int C, int F) {
+  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || C * F > 2048) return 0;
+  return align256((size_t)cdw_blocks(T * B) * 9 * C * F * sizeof(double));
+}
+
+extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, int H, int W, int C, int F,
+                                         const int32_t* conv_row_ptr, const int32_t* conv_col_idx,
+                                         const float* conv_g, const float* eps_conv, int64_t conv_cap, float* dWc,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (!trace_in || !conv_row_ptr || !dWc || !workspace) return SNN_ERR_INVALID_ARG;
+  if (conv_cap < 0 || (conv_cap > 0 && (!conv_col_idx || !eps_conv))) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || too_big(T, B, H * W * C)) return SNN_ERR_INVALID_ARG;
+  if (C * F > 2048) return SNN_ERR_UNSUPPORTED;  // the block accumulator is 9 * C * F float64 in LDS
+  if (workspace_bytes < snn_conv_sparse_dw_workspace(T, B, H, W, C, F)) return SNN_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int TB = T * B;
+  const int nb = cdw_blocks(TB);
+  const int rpb = (TB + nb - 1) / nb;
+  const int nacc = 9 * C * F;
+  double* part = static_cast<double*>(workspace);
+  const size_t lds = (size_t)nacc * sizeof(double);
+  (void)hipFuncSetAttribute((const void*)conv_dw_sparse_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL(conv_dw_sparse_kernel, dim3((unsigned)nb), dim3(kCdwThreads), lds, s, trace_in, TB, H, W, C, F,
+                     conv_row_ptr, conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part);
+  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)((nacc + 255) / 256)), dim3(256), 0, s, part, nb, nacc, dWc);
+  return launch_status();
+}
+
+extern "C" size_t snn_conv_dense_dw_workspace(int T, int B, int H, int W, int C, int F) {
+  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || C > kDenseMaxC) return 0;
+  return align256((size_t)dense_blocks((int64_t)T * B * H * W) * 9 * C * F * sizeof(double));
+}
+
+extern "C" snn_status snn_conv_dense_dw(const float* trace_in, const float* V, const float* eps_conv, int T, int B,
+                                        int H, int W, int C, int F, float theta, float b_th, float beta, float* dWc,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  if (!trace_in || !V || !eps_conv || !dWc || !workspace) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || too_big(T, B, H * W * C)) return SNN_ERR_INVALID_ARG;
+  if (isnan(theta) || isnan(b_th) || b_th < 0.0f || isnan(beta) || beta < 0.0f) return SNN_ERR_INVALID_ARG;
+  if (C > kDenseMaxC) return SNN_ERR_UNSUPPORTED;
+  if (workspace_bytes < snn_conv_dense_dw_workspace(T, B, H, W, C, F)) return SNN_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t n_pos = (int64_t)T * B * H * W;
+  const int64_t nb = dense_blocks(n_pos);
+  const int64_t ppb = (n_pos + nb - 1) / nb;
+  const int nacc = 9 * C * F;
+  double* part = static_cast<double*>(workspace);
+  if (C == 1)
+    hipLaunchKernelGGL(conv_dw_dense_kernel<1>, dim3((unsigned)nb), dim3(kCdwThreads), 0, s, trace_in, V, eps_conv,
+                       n_pos, H, W, C, F, theta, b_th, beta, ppb, part);
+  else
+    hipLaunchKernelGGL(conv_dw_dense_kernel<kDenseMaxC>, dim3((unsigned)nb), dim3(kCdwThreads), 0, s, trace_in, V,
+                       eps_conv, n_pos, H, W, C, F, theta, b_th, beta, ppb, part);
+  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)((nacc + 255) / 256)), dim3(256), 0, s, part, (int)nb, nacc, dWc);
+  return launch_status();
+}

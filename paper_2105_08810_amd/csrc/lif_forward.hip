@@ -232,6 +232,73 @@ using namespace snn;
 
 namespace {
 
+// Convolutional LIF layer (3x3 filters, stride 1, zero padding 1, channels last): neuron
+// k = b * N + n, n = (y * W + x) * F + f, N = H * W * F. Its weighted input at step t is the
+// filter applied to the input spikes of the 3x3 patch, added in ascending input index
+// (y', x', c) from +0.0 in separately rounded float32 adds (the order of the layer's Toeplitz
+// matrix in the fully connected form), then the same recurrence and marking as lif_scan. The
+// currents of kConvAhead steps are formed before their recurrence so that their loads overlap.
+constexpr int kConvAhead = 8;
+
+__global__ __launch_bounds__(kScanThreads) void conv_scan(const uint8_t* __restrict__ s_in, const float* __restrict__ Wc,
+                                                          int T, int B, int H, int W, int C, int F, float alpha,
+                                                          float theta, float b_th, float* __restrict__ V,
+                                                          uint8_t* __restrict__ s_out, uint64_t* __restrict__ bits) {
+  const size_t N = (size_t)H * W * F;
+  const size_t step = (size_t)B * N;
+  const size_t k0 = (size_t)blockIdx.x * kScanThreads + (threadIdx.x & ~(kWave - 1));
+  if (k0 >= step) return;  // whole wavefront past the end
+  const size_t k = (size_t)blockIdx.x * kScanThreads + threadIdx.x;
+  const bool valid = k < step;
+  const size_t kc = valid ? k : k0;  // lanes past the end compute on a valid neuron, store nothing
+  const int b = (int)(kc / N);
+  const int n = (int)(kc - (size_t)b * N);
+  const int f = n % F;
+  const int pix = n / F;
+  const int y = pix / W;
+  const int x = pix - y * W;
+  const size_t W64 = (step + kWave - 1) / kWave;
+  const size_t wword = k0 / kWave;
+  const size_t in_step = (size_t)B * H * W * C;
+  const uint8_t* xb = s_in + (size_t)b * H * W * C;
+  float v = 0.0f;
+  if (valid) V[k] = 0.0f;
+  if (bits) mark_active(bits, wword, valid, v, theta, b_th);
+  for (int t0 = 0; t0 < T - 1; t0 += kConvAhead) {
+    const int np = min(kConvAhead, T - 1 - t0);
+    float in[kConvAhead];
+#pragma unroll
+    for (int p = 0; p < kConvAhead; ++p) {
+      const uint8_t* xt = xb + (size_t)(t0 + min(p, np - 1)) * in_step;
+      float acc = 0.0f;
+      for (int ky = 0; ky < 3; ++ky) {
+        const int yy = y + ky - 1;
+        if (yy < 0 || yy >= H) continue;
+        for (int kx = 0; kx < 3; ++kx) {
+          const int xx = x + kx - 1;
+          if (xx < 0 || xx >= W) continue;
+          const uint8_t* px = xt + ((size_t)yy * W + xx) * C;
+          for (int c = 0; c < C; ++c)
+            if (px[c]) acc = __fadd_rn(acc, Wc[((ky * 3 + kx) * C + c) * F + f]);
+        }
+      }
+      in[p] = acc;
+    }
+#pragma unroll
+    for (int p = 0; p < kConvAhead; ++p) {
+      if (p < np) {
+        const int t = t0 + p;
+        const bool sp = v > theta;
+        if (valid) s_out[(size_t)t * step + k] = (uint8_t)sp;
+        v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), in[p]), sp ? -1.0f : -0.0f);
+        if (valid) V[(size_t)(t + 1) * step + k] = v;
+        if (bits) mark_active(bits, (size_t)(t + 1) * W64 + wword, valid, v, theta, b_th);
+      }
+    }
+  }
+  if (valid) s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
+}
+
 snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out, float alpha,
                             float theta, float b_th, float* V, uint8_t* s_out, float* trace_in, uint64_t* bits,
                             void* stream) {
@@ -285,4 +352,32 @@ extern "C" snn_status snn_lif_forward_active(const uint8_t* s_in, const float* W
                                              float* trace_in, uint64_t* active_bits, void* stream) {
   if (!active_bits) return SNN_ERR_INVALID_ARG;
   return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, active_bits, stream);
+}
+
+extern "C" snn_status snn_conv_lif_forward(const uint8_t* s_in, const float* Wc, int T, int B, int H, int W, int C,
+                                           int F, float alpha, float theta, float b_th, float* V, uint8_t* s_out,
+                                           float* trace_in, uint64_t* active_bits, void* stream) {
+  if (!s_in || !Wc || !V || !s_out) return SNN_ERR_INVALID_ARG;
+  if (bad_dim(T) || bad_dim(B) || bad_dim(H) || bad_dim(W) || bad_dim(C) || bad_dim(F)) return SNN_ERR_INVALID_ARG;
+  if ((int64_t)H * W * F >= ((int64_t)1 << 31) || (int64_t)H * W * C >= ((int64_t)1 << 31)) return SNN_ERR_INVALID_ARG;
+  if (too_big(T, B, H * W * F) || too_big(T, B, H * W * C)) return SNN_ERR_INVALID_ARG;
+  if (bad_alpha(alpha) || isnan(theta)) return SNN_ERR_INVALID_ARG;
+  if (active_bits && (isnan(b_th) || b_th < 0.0f)) return SNN_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nv = (int)(((size_t)B * H * W * F + kScanThreads - 1) / kScanThreads);
+  hipLaunchKernelGGL(conv_scan, dim3((unsigned)nv), dim3(kScanThreads), 0, s, s_in, Wc, T, B, H, W, C, F, alpha, theta,
+                     b_th, V, s_out, active_bits);
+  if (trace_in) {  // the input trace: lif_scan's trace blocks alone
+    const int N_in = H * W * C;
+    const int nt = (int)(((size_t)B * ((N_in + 3) / 4) + kScanThreads - 1) / kScanThreads);
+    const bool tal = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0 &&
+                     (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0;
+    if (tal)
+      hipLaunchKernelGGL(lif_scan<true>, dim3((unsigned)nt), dim3(kScanThreads), 0, s, s_in, T, B, N_in, 1, alpha,
+                         theta, b_th, nullptr, nullptr, trace_in, nullptr, 0);
+    else
+      hipLaunchKernelGGL(lif_scan<false>, dim3((unsigned)nt), dim3(kScanThreads), 0, s, s_in, T, B, N_in, 1, alpha,
+                         theta, b_th, nullptr, nullptr, trace_in, nullptr, 0);
+  }
+  return launch_status();
 }

@@ -207,6 +207,128 @@ class Adam:
             snn.adam_step(p, g, m, v, self.k, self.lr, self.betas, self.eps)
 
 
+@dataclass
+class ConvNetwork:
+    """The convolutional network of Sec. 3's convolutional experiment (App. E): a convolutional
+    LIF layer (3x3, stride 1, padding 1, F filters) on input spikes [T, B, H, W, C], 2x2 max
+    pooling of its spikes, and the infinite-threshold readout on the flattened pooled spikes."""
+    X: torch.Tensor  # [T, B, H, W, C] uint8
+    Wc: torch.Tensor  # [3, 3, C, F]
+    W_out: torch.Tensor  # [(H/2)(W/2)F, classes]
+    alpha: float
+    alpha_out: float
+    labels: torch.Tensor
+    loss_mode: int
+    theta: float = 1.0
+    beta: float = 100.0
+    V: Optional[torch.Tensor] = None
+    S: Optional[torch.Tensor] = None
+    trace: Optional[torch.Tensor] = None
+    bits: Optional[torch.Tensor] = None
+    bits_bth: Optional[float] = None
+    P: Optional[torch.Tensor] = None
+    arg: Optional[torch.Tensor] = None
+    pbits: Optional[torch.Tensor] = None
+    V_out: Optional[torch.Tensor] = None
+    S_out: Optional[torch.Tensor] = None
+    trace_out: Optional[torch.Tensor] = None
+
+    @property
+    def dims(self):
+        T, B, H, W, C = self.X.shape
+        return T, B, H, W, C, self.Wc.shape[3]
+
+    @property
+    def N(self):
+        _, _, H, W, _, F = self.dims
+        return H * W * F
+
+    @property
+    def Np(self):
+        _, _, H, W, _, F = self.dims
+        return (H // 2) * (W // 2) * F
+
+    def allocate(self):
+        T, B, H, W, C, F = self.dims
+        dev = self.X.device
+        self.V = torch.empty((T, B, self.N), dtype=torch.float32, device=dev)
+        self.S = torch.empty((T, B, self.N), dtype=torch.uint8, device=dev)
+        self.trace = torch.empty((T, B, H * W * C), dtype=torch.float32, device=dev)
+        self.bits = torch.empty(snn.snn_active_bits_words(T, B, self.N), dtype=torch.int64, device=dev)
+        self.P = torch.empty((T, B, self.Np), dtype=torch.uint8, device=dev)
+        self.arg = torch.empty((T, B, self.Np), dtype=torch.uint8, device=dev)
+        self.pbits = torch.empty(snn.snn_active_bits_words(T, B, self.Np), dtype=torch.int64, device=dev)
+        Cl = self.W_out.shape[1]
+        self.V_out = torch.empty((T, B, Cl), dtype=torch.float32, device=dev)
+        self.S_out = torch.empty((T, B, Cl), dtype=torch.uint8, device=dev)
+        self.trace_out = torch.empty((T, B, self.Np), dtype=torch.float32, device=dev)
+        return self
+
+    def forward(self, b_th: Optional[float] = None):
+        """Conv layer (marking its active set when b_th is given), pooling, readout."""
+        if self.V is None:
+            self.allocate()
+        T, B, H, W, C, F = self.dims
+        snn.snn_conv_lif_forward(self.X, self.Wc, T, B, H, W, C, F, self.alpha, self.theta,
+                                 0.0 if b_th is None else b_th, self.V, self.S, self.trace,
+                                 None if b_th is None else self.bits)
+        self.bits_bth = b_th
+        snn.snn_maxpool_spikes(self.S, T, B, H, W, F, self.P, self.arg)
+        snn.snn_lif_forward(self.P, self.W_out, T, B, self.Np, self.W_out.shape[1], self.alpha_out, INF, self.V_out,
+                            self.S_out, self.trace_out)
+        return self
+
+    def readout(self, dense=False):
+        return snn.readout_ce(self.V_out, self.labels, self.loss_mode, dense=dense)
+
+    def compact(self, b_th, capacities: Optional[List[int]] = None):
+        """[conv CSR (with g), pooled CSR (the readout's input-active entries)]; the forward must
+        have marked the active set with this b_th."""
+        if self.bits_bth != b_th:
+            raise ValueError("compact(b_th): run forward(b_th) first")
+        T, B, H, W, C, F = self.dims
+        caps = capacities or [None, None]
+        conv = snn.active_compact_bits(self.bits, self.V, self.theta, self.beta, caps[0])
+        snn.snn_pool_route_bits(self.bits, self.arg, T, B, H, W, F, self.pbits)
+        pool = snn.active_compact_bits(self.pbits, None, self.theta, self.beta, caps[1], with_g=False,
+                                       shape=(T, B, self.Np))
+        return [conv, pool]
+
+    def sparse_backward(self, csrs, ro=None, ws=None):
+        """Readout backward at the pooled entries, routed to the conv layer's active entries, and
+        the sparse filter gradient. Returns (dWc, dW_out, eps at the conv entries)."""
+        if ro is None:
+            ro = self.readout()
+        conv, pool = csrs
+        T, B, H, W, C, F = self.dims
+        dW_out, eps_pool = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro[0], ro[1], inp=pool)
+        eps = torch.empty(conv.capacity, dtype=torch.float32, device=self.X.device)
+        snn.snn_pool_scatter_eps(T, B, H, W, F, pool.row_ptr, pool.col_idx, pool.capacity, eps_pool, self.arg,
+                                 conv.row_ptr, conv.col_idx, conv.capacity, eps)
+        dWc = torch.empty_like(self.Wc)
+        if ws is None:
+            ws = snn.workspace(snn.snn_conv_sparse_dw_workspace(T, B, H, W, C, F), self.X.device)
+        snn.snn_conv_sparse_dw(self.trace, T, B, H, W, C, F, conv.row_ptr, conv.col_idx, conv.g, eps, conv.capacity,
+                               dWc, ws)
+        return dWc, dW_out, eps
+
+    def dense_backward(self, b_th, ro=None, ws=None):
+        """The dense chain: dense readout backward, dense routing, dense filter gradient (b_th =
+        inf: full surrogate). Returns (dWc, dW_out, eps dense [T, B, N])."""
+        if ro is None or ro[3] is None:
+            ro = self.readout(dense=True)
+        T, B, H, W, C, F = self.dims
+        dW_out, eps_pool = snn.dense_backward_ref(self.W_out, self.trace_out, self.V_out, ro[3], self.alpha_out, INF,
+                                                  INF, self.beta, grad_in=True)
+        eps = torch.empty((T, B, self.N), dtype=torch.float32, device=self.X.device)
+        snn.snn_pool_scatter_eps_dense(eps_pool, self.arg, T, B, H, W, F, eps)
+        dWc = torch.empty_like(self.Wc)
+        if ws is None:
+            ws = snn.workspace(snn.snn_conv_dense_dw_workspace(T, B, H, W, C, F), self.X.device)
+        snn.snn_conv_dense_dw(self.trace, self.V, eps, T, B, H, W, C, F, self.theta, b_th, self.beta, dWc, ws)
+        return dWc, dW_out, eps
+
+
 class Graphed:
     """Library calls captured once as a HIP graph and replayed. fn makes its calls on the current
     stream (the capture stream) and returns what later work reads; those tensors stay the

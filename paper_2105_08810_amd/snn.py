@@ -51,6 +51,15 @@ _SIGNATURES = {
     "snn_activity_reg": (_I, [_P, _I, _I, _I, _F, _F, _F, _F, _P, _P, _P, _P, _SZ, _P]),
     "snn_activity_reg_grad": (_I, [_P, _I, _I, _I, _P, _P, _I64, _P, _P]),
     "snn_adam_step": (_I, [_P, _P, _P, _P, _I64, _F, _F, _F, _F, _I, _P]),
+    "snn_conv_lif_forward": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _P, _P, _P, _P]),
+    "snn_maxpool_spikes": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
+    "snn_pool_route_bits": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "snn_pool_scatter_eps": (_I, [_I, _I, _I, _I, _I, _P, _P, _I64, _P, _P, _P, _P, _I64, _P, _P]),
+    "snn_pool_scatter_eps_dense": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
+    "snn_conv_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "snn_conv_sparse_dw": (_I, [_P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_conv_dense_dw_workspace": (_SZ, [_I, _I, _I, _I, _I, _I]),
+    "snn_conv_dense_dw": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _P, _SZ, _P]),
 }
 
 _lib = None
@@ -248,6 +257,69 @@ def snn_adam_step(W, grad, m, v, n, lr, beta1, beta2, eps, step, stream=None):
         _stream(stream)))
 
 
+def _nbytes(ws):
+    return 0 if ws is None else ws.numel() * ws.element_size()
+
+
+def snn_conv_lif_forward(s_in, Wc, T, B, H, W, C, F, alpha, theta, b_th, V, s_out, trace_in=None, active_bits=None,
+                         stream=None):
+    _check("snn_conv_lif_forward", lib().snn_conv_lif_forward(
+        _ptr(s_in, torch.uint8, "s_in"), _ptr(Wc, torch.float32, "Wc"), T, B, H, W, C, F, float(alpha), float(theta),
+        float(b_th), _ptr(V, torch.float32, "V"), _ptr(s_out, torch.uint8, "s_out"),
+        _ptr(trace_in, torch.float32, "trace_in"), _ptr(active_bits, torch.int64, "active_bits"), _stream(stream)))
+
+
+def snn_maxpool_spikes(S, T, B, H, W, F, P, arg, stream=None):
+    _check("snn_maxpool_spikes", lib().snn_maxpool_spikes(
+        _ptr(S, torch.uint8, "S"), T, B, H, W, F, _ptr(P, torch.uint8, "P"), _ptr(arg, torch.uint8, "arg"),
+        _stream(stream)))
+
+
+def snn_pool_route_bits(conv_bits, arg, T, B, H, W, F, pool_bits, stream=None):
+    _check("snn_pool_route_bits", lib().snn_pool_route_bits(
+        _ptr(conv_bits, torch.int64, "conv_bits"), _ptr(arg, torch.uint8, "arg"), T, B, H, W, F,
+        _ptr(pool_bits, torch.int64, "pool_bits"), _stream(stream)))
+
+
+def snn_pool_scatter_eps(T, B, H, W, F, pool_row_ptr, pool_col_idx, pool_cap, eps_pool, arg, conv_row_ptr,
+                         conv_col_idx, conv_cap, eps_conv, stream=None):
+    _check("snn_pool_scatter_eps", lib().snn_pool_scatter_eps(
+        T, B, H, W, F, _ptr(pool_row_ptr, torch.int32, "pool_row_ptr"), _ptr(pool_col_idx, torch.int32, "pool_col_idx"),
+        int(pool_cap), _ptr(eps_pool, torch.float32, "eps_pool"), _ptr(arg, torch.uint8, "arg"),
+        _ptr(conv_row_ptr, torch.int32, "conv_row_ptr"), _ptr(conv_col_idx, torch.int32, "conv_col_idx"),
+        int(conv_cap), _ptr(eps_conv, torch.float32, "eps_conv"), _stream(stream)))
+
+
+def snn_pool_scatter_eps_dense(eps_pool, arg, T, B, H, W, F, eps_conv, stream=None):
+    _check("snn_pool_scatter_eps_dense", lib().snn_pool_scatter_eps_dense(
+        _ptr(eps_pool, torch.float32, "eps_pool"), _ptr(arg, torch.uint8, "arg"), T, B, H, W, F,
+        _ptr(eps_conv, torch.float32, "eps_conv"), _stream(stream)))
+
+
+def snn_conv_sparse_dw_workspace(T, B, H, W, C, F) -> int:
+    return int(lib().snn_conv_sparse_dw_workspace(T, B, H, W, C, F))
+
+
+def snn_conv_sparse_dw(trace_in, T, B, H, W, C, F, conv_row_ptr, conv_col_idx, conv_g, eps_conv, conv_cap, dWc, ws,
+                       stream=None):
+    _check("snn_conv_sparse_dw", lib().snn_conv_sparse_dw(
+        _ptr(trace_in, torch.float32, "trace_in"), T, B, H, W, C, F, _ptr(conv_row_ptr, torch.int32, "conv_row_ptr"),
+        _ptr(conv_col_idx, torch.int32, "conv_col_idx"), _ptr(conv_g, torch.float32, "conv_g"),
+        _ptr(eps_conv, torch.float32, "eps_conv"), int(conv_cap), _ptr(dWc, torch.float32, "dWc"),
+        _ptr(ws, None, "workspace"), _nbytes(ws), _stream(stream)))
+
+
+def snn_conv_dense_dw_workspace(T, B, H, W, C, F) -> int:
+    return int(lib().snn_conv_dense_dw_workspace(T, B, H, W, C, F))
+
+
+def snn_conv_dense_dw(trace_in, V, eps_conv, T, B, H, W, C, F, theta, b_th, beta, dWc, ws, stream=None):
+    _check("snn_conv_dense_dw", lib().snn_conv_dense_dw(
+        _ptr(trace_in, torch.float32, "trace_in"), _ptr(V, torch.float32, "V"), _ptr(eps_conv, torch.float32, "eps_conv"),
+        T, B, H, W, C, F, float(theta), float(b_th), float(beta), _ptr(dWc, torch.float32, "dWc"),
+        _ptr(ws, None, "workspace"), _nbytes(ws), _stream(stream)))
+
+
 # ------------------------------------------------------------------ allocation helpers
 
 def lif_forward(s_in: torch.Tensor, W: torch.Tensor, alpha, theta, want_trace=True):
@@ -288,11 +360,12 @@ def active_compact(V: torch.Tensor, theta, b_th, beta, capacity: Optional[int] =
     return Csr(row_ptr, col, g, nnz, cap)
 
 
-def active_compact_bits(bits: torch.Tensor, V: torch.Tensor, theta, beta, capacity: Optional[int] = None,
-                        with_g=True) -> Csr:
-    """Allocate and run snn_active_compact_bits. Without a capacity it first counts (one host sync)."""
-    T, B, N = V.shape
-    dev = V.device
+def active_compact_bits(bits: torch.Tensor, V: Optional[torch.Tensor], theta, beta, capacity: Optional[int] = None,
+                        with_g=True, shape=None) -> Csr:
+    """Allocate and run snn_active_compact_bits. Without a capacity it first counts (one host sync).
+    shape = (T, B, N) when V is None (then with_g must be False)."""
+    T, B, N = V.shape if V is not None else shape
+    dev = bits.device
     ws = workspace(snn_active_compact_bits_workspace(T, B, N), dev)
     row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device=dev)
     nnz = torch.empty(1, dtype=torch.int64, device=dev)

@@ -31,8 +31,26 @@ PILOT_B = 16
 KAPPA_SD = 0.4
 
 
+def calibrate_conv(name: str) -> dict:
+    """Filters: m = mean spiking inputs in a neuron's 3x3xC patch per step (interior neurons)."""
+    from oracle import conv as oconv
+    from synth.inputs import make_conv_inputs
+    cfg = CONFIGS[name]
+    H, W, C, F = cfg.conv
+    batch = list(range(min(PILOT_B, cfg.B)))
+    x = make_spikes(cfg, batch)
+    m = 9.0 * C * float((x != 0).mean())
+    s = KAPPA_SD * math.sqrt(1.0 - float(cfg.alpha) ** 2) / math.sqrt(m)
+    inp = make_conv_inputs(cfg, batch[:4], sigmas=[s, 1.0 / math.sqrt((H // 2) * (W // 2) * F)])
+    f = oconv.conv_network_forward(inp.X, inp.Wc, inp.W_out, cfg.alpha, cfg.alpha_out, cfg.theta)
+    rho = float(oracle.active_mask(f["V"], cfg.theta, cfg.b_th).mean())
+    return {"sigma": [s], "m": [m], "rho_pilot_default_bth": [rho], "pilot_batch": 4, "b_th": cfg.b_th}
+
+
 def calibrate(name: str) -> dict:
     cfg = CONFIGS[name]
+    if cfg.conv:
+        return calibrate_conv(name)
     batch = list(range(min(PILOT_B, cfg.B)))
     x = make_spikes(cfg, batch)
     sig, m_list, rho = [], [], []

@@ -52,6 +52,7 @@ class Config:
     theta: float = 1.0
     beta: float = 100.0
     description: str = ""
+    conv: tuple = ()  # (H, W, C, F) for a convolutional network: sizes = (H W C, H W F, classes)
 
     @property
     def n_layers(self) -> int:
@@ -95,6 +96,11 @@ CONFIGS = {
         loss_mode="max", b_th=0.2, kind="classlatency",
         description="class-conditional latency code (F-MNIST-like training task): 28x28 class templates plus "
                     "noise, one spike per input at most; LIF 784->200->200, readout 200->10"),
+    "conv": Config(
+        "conv", 8, T=100, B=256, sizes=(784, 28 * 28 * 64, 10), tau_ratio_hidden=0.1, tau_ratio_out=0.1,
+        loss_mode="max", b_th=0.2, kind="classlatency", conv=(28, 28, 1, 64),
+        description="convolutional LIF layer of 64 3x3 filters (padding 1) on the class-conditional latency "
+                    "code (28x28x1, F-MNIST-like), 2x2 max pooling, readout 12544->10, T=100, B=256"),
     "deep": Config(
         "deep", 7, T=100, B=256, sizes=(784, 300, 300, 300, 300, 300, 10), tau_ratio_hidden=0.1,
         tau_ratio_out=0.1, loss_mode="max", b_th=0.2, kind="classlatency",
@@ -276,6 +282,51 @@ def weight_std(cfg: Config, gains: Optional[dict] = None) -> List[float]:
     if cfg.name not in gains:
         raise KeyError(f"weight gains for '{cfg.name}' missing: run synth/calibrate.py")
     return list(gains[cfg.name]["sigma"]) + [1.0 / math.sqrt(cfg.sizes[-2])]
+
+
+def conv_weight_std(cfg: Config, gains: Optional[dict] = None) -> List[float]:
+    """Std of the filters and of the readout of a convolutional workload: filters
+    kappa / sqrt(m) with m = mean spiking inputs in a neuron's 3x3xC patch per step (frozen in
+    gains.json), readout 1/sqrt((H/2)(W/2)F)."""
+    H, W, C, F = cfg.conv
+    gains = load_gains() if gains is None else gains
+    if cfg.name not in gains:
+        raise KeyError(f"weight gains for '{cfg.name}' missing: run synth/calibrate.py")
+    return [gains[cfg.name]["sigma"][0], 1.0 / math.sqrt((H // 2) * (W // 2) * F)]
+
+
+def make_conv_weights(cfg: Config, sigmas: Optional[List[float]] = None):
+    """Filters Wc [3, 3, C, F] and readout weights [(H/2)(W/2)F, classes], float32."""
+    H, W, C, F = cfg.conv
+    sig = conv_weight_std(cfg) if sigmas is None else sigmas
+    Wc = (rng_for(cfg.cfg_id, 11).standard_normal((3, 3, C, F)) * sig[0]).astype(np.float32)
+    Wo = (rng_for(cfg.cfg_id, 20).standard_normal(((H // 2) * (W // 2) * F, cfg.sizes[-1])) * sig[1]).astype(np.float32)
+    return Wc, Wo
+
+
+@dataclass
+class ConvInputs:
+    cfg: Config
+    X: np.ndarray  # [T, B, H, W, C] uint8
+    Wc: np.ndarray
+    W_out: np.ndarray
+    labels: np.ndarray
+
+    @property
+    def alpha(self) -> np.float32:
+        return self.cfg.alpha
+
+    @property
+    def alpha_out(self) -> np.float32:
+        return self.cfg.alpha_out
+
+
+def make_conv_inputs(cfg: Config, batch: Optional[Sequence[int]] = None, sigmas=None) -> ConvInputs:
+    H, W, C, F = cfg.conv
+    X = make_spikes(cfg, batch)
+    Wc, Wo = make_conv_weights(cfg, sigmas)
+    return ConvInputs(cfg=cfg, X=X.reshape(X.shape[0], X.shape[1], H, W, C), Wc=Wc, W_out=Wo,
+                      labels=make_labels(cfg, batch))
 
 
 def make_weights(cfg: Config, sigmas: Optional[List[float]] = None) -> List[np.ndarray]:

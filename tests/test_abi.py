@@ -252,3 +252,34 @@ def test_adam_rejects(lib, kw):
     a.update(kw)
     assert lib.snn_adam_step(a["W"], a["g"], a["m"], a["v"], a["n"], a["lr"], a["b1"], a["b2"], a["eps"], a["step"],
                              None) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_conv_entry_points_reject(lib):
+    E = snn.SNN_ERR_INVALID_ARG
+    f = lambda **kw: lib.snn_conv_lif_forward(  # noqa: E731
+        kw.get("x", FAKE), kw.get("w", FAKE), kw.get("T", 10), 4, kw.get("H", 8), 8, 1, kw.get("F", 64),
+        kw.get("a", 0.9), kw.get("th", 1.0), kw.get("b", 0.2), kw.get("V", FAKE), FAKE, FAKE, kw.get("bits", FAKE), None)
+    for kw in (dict(x=None), dict(w=None), dict(V=None), dict(T=0), dict(F=0), dict(a=0.0), dict(a=NAN),
+               dict(th=NAN), dict(b=NAN), dict(b=-1.0), dict(H=70000, T=70000)):
+        assert f(**kw) == E, kw
+    assert lib.snn_maxpool_spikes(None, 10, 4, 8, 8, 64, FAKE, FAKE, None) == E
+    assert lib.snn_maxpool_spikes(FAKE, 10, 4, 7, 8, 64, FAKE, FAKE, None) == E  # odd height
+    assert lib.snn_maxpool_spikes(FAKE, 10, 4, 8, 8, 64, FAKE, None, None) == E
+    assert lib.snn_pool_route_bits(FAKE, FAKE, 10, 4, 8, 9, 64, FAKE, None) == E  # odd width
+    assert lib.snn_pool_route_bits(None, FAKE, 10, 4, 8, 8, 64, FAKE, None) == E
+    assert lib.snn_pool_scatter_eps(10, 4, 8, 8, 64, FAKE, FAKE, -1, FAKE, FAKE, FAKE, FAKE, 5, FAKE, None) == E
+    assert lib.snn_pool_scatter_eps(10, 4, 8, 8, 64, FAKE, None, 5, FAKE, FAKE, FAKE, FAKE, 5, FAKE, None) == E
+    assert lib.snn_pool_scatter_eps(10, 4, 8, 8, 64, FAKE, FAKE, 5, FAKE, FAKE, FAKE, FAKE, 5, None, None) == E
+    assert lib.snn_pool_scatter_eps_dense(FAKE, None, 10, 4, 8, 8, 64, FAKE, None) == E
+    ws = lib.snn_conv_sparse_dw_workspace(10, 4, 8, 8, 1, 64)
+    assert ws >= 9 * 64 * 8 and lib.snn_conv_sparse_dw_workspace(10, 4, 7, 8, 1, 64) == 0
+    assert lib.snn_conv_sparse_dw(FAKE, 10, 4, 8, 8, 1, 64, FAKE, FAKE, FAKE, FAKE, 100, FAKE, FAKE, 8, None) == E
+    assert lib.snn_conv_sparse_dw(FAKE, 10, 4, 8, 8, 1, 64, FAKE, None, FAKE, FAKE, 100, FAKE, FAKE, ws, None) == E
+    assert lib.snn_conv_sparse_dw(FAKE, 10, 4, 8, 8, 64, 64, FAKE, FAKE, FAKE, FAKE, 100, FAKE, FAKE, 1 << 40,
+                                  None) == snn.SNN_ERR_UNSUPPORTED
+    wd = lib.snn_conv_dense_dw_workspace(10, 4, 8, 8, 1, 64)
+    assert wd > 0 and lib.snn_conv_dense_dw_workspace(10, 4, 8, 8, 5, 64) == 0
+    assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 1, 64, 1.0, NAN, 100.0, FAKE, FAKE, wd, None) == E
+    assert lib.snn_conv_dense_dw(FAKE, None, FAKE, 10, 4, 8, 8, 1, 64, 1.0, 0.2, 100.0, FAKE, FAKE, wd, None) == E
+    assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 5, 64, 1.0, 0.2, 100.0, FAKE, FAKE, 1 << 40,
+                                 None) == snn.SNN_ERR_UNSUPPORTED

@@ -1,0 +1,139 @@
+"""The convolutional layer on the GPU (through the C ABI) against the CPU oracle (oracle/conv.py).
+
+Forward state bit for bit (V, spikes, traces, pooled spikes and the pooling's choice, readout),
+active sets bit for bit (the conv layer's CSR and the pooled entries whose picked conv neuron is
+active), gradients (filters, readout, the spike gradient at the conv layer's active entries)
+within 1e-4 of the oracle's magnitude envelope; the dense chain to the same bar.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import conv
+from paper_2105_08810_amd import pipeline
+from synth import CONFIGS
+from synth.inputs import make_conv_inputs
+
+pytestmark = pytest.mark.gpu
+F32 = np.float32
+TOL = 1e-4
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _small(T=20, B=4, H=8, W=8, C=1, Fo=64, Cls=5, rate=0.08, sigma=0.9, seed=1):
+    r = np.random.default_rng(seed)
+    X = (r.random((T, B, H, W, C)) < rate).astype(np.uint8)
+    Wc = (r.standard_normal((3, 3, C, Fo)) * sigma).astype(F32)
+    Np = (H // 2) * (W // 2) * Fo
+    Wo = (r.standard_normal((Np, Cls)) / math.sqrt(Np)).astype(F32)
+    y = r.integers(0, Cls, B).astype(np.int32)
+    return X, Wc, Wo, y
+
+
+def _bits_equal(x, r, what):
+    x, r = np.asarray(x), np.asarray(r)
+    assert x.shape == r.shape, (what, x.shape, r.shape)
+    same = (x.view(np.uint32) == r.view(np.uint32)) if x.dtype == np.float32 else (x == r)
+    assert same.all(), f"{what}: {int((~same).sum())} of {same.size} differ"
+
+
+def _env_ok(x, ref, env, what):
+    err = np.abs(np.asarray(x, np.float64) - ref)
+    bad = err > TOL * env + 1e-30
+    assert not bad.any(), f"{what}: {int(bad.sum())} outside, worst {(err / np.maximum(env, 1e-300)).max():.3g}"
+
+
+def _csr_from_mask(m):
+    T, B, N = m.shape
+    rows, cols = np.nonzero(m.reshape(T * B, N))
+    rp = np.zeros(T * B + 1, np.int64)
+    np.cumsum(np.bincount(rows, minlength=T * B), out=rp[1:])
+    return rp, cols.astype(np.int64)
+
+
+def _check(X, Wc, Wo, y, b_th, mode="max", dense=True):
+    T, B, H, W, C = X.shape
+    Fo = Wc.shape[3]
+    a = F32(math.exp(-0.1))
+    f = conv.conv_network_forward(X, Wc, Wo, a, a)
+    r = conv.conv_network_backward(f, Wc, Wo, a, y, mode, 1.0, b_th, 100.0)
+    env = conv.conv_network_backward(f, Wc, Wo, a, y, mode, 1.0, b_th, 100.0, absolute=True)
+    dev = torch.device("cuda")
+    net = pipeline.ConvNetwork(X=torch.from_numpy(X).to(dev), Wc=torch.from_numpy(Wc).to(dev),
+                               W_out=torch.from_numpy(Wo).to(dev), alpha=float(a), alpha_out=float(a),
+                               labels=torch.from_numpy(y).to(dev), loss_mode=0 if mode == "max" else 1)
+    net.forward(b_th)
+    ro = net.readout(dense=True)
+    csrs = net.compact(b_th)
+    dWc, dWo, eps = net.sparse_backward(csrs, ro)
+    if dense:
+        ddWc, ddWo, deps = net.dense_backward(b_th, ro)
+    torch.cuda.synchronize()
+    N = H * W * Fo
+    # forward, bit for bit
+    _bits_equal(_np(net.V), f["V"].reshape(T, B, N), "V")
+    _bits_equal(_np(net.S), f["S"].reshape(T, B, N), "S")
+    _bits_equal(_np(net.trace), f["trace"].reshape(T, B, -1), "trace")
+    _bits_equal(_np(net.P), f["P"].reshape(T, B, -1), "P")
+    _bits_equal(_np(net.arg).astype(np.int64), f["arg"].reshape(T, B, -1), "arg")
+    _bits_equal(_np(net.V_out), f["V_out"], "V_out")
+    _bits_equal(_np(net.trace_out), f["trace_out"], "trace_out")
+    # active sets
+    mask = r["mask"].reshape(T, B, N)
+    rp, ci = _csr_from_mask(mask)
+    c = csrs[0]
+    n = c.nnz()
+    assert n == rp[-1]
+    _bits_equal(_np(c.row_ptr).astype(np.int64), rp, "conv row_ptr")
+    _bits_equal(_np(c.col_idx)[:n].astype(np.int64), ci, "conv col_idx")
+    g_ref = oracle.csr_values(r["g"].reshape(T, B, N), rp, ci)
+    assert np.allclose(_np(c.g)[:n], g_ref, rtol=2e-6, atol=0)
+    # pooled entries whose picked conv neuron is active
+    m5 = r["mask"]
+    arg = f["arg"]
+    pm = np.zeros(arg.shape, bool)
+    for k, (dy, dx) in enumerate(((0, 0), (0, 1), (1, 0), (1, 1))):
+        pm |= (arg == k) & m5[:, :, dy::2, dx::2, :]
+    prp, pci = _csr_from_mask(pm.reshape(T, B, -1))
+    p = csrs[1]
+    _bits_equal(_np(p.row_ptr).astype(np.int64), prp, "pool row_ptr")
+    _bits_equal(_np(p.col_idx)[:p.nnz()].astype(np.int64), pci, "pool col_idx")
+    # gradients
+    _env_ok(_np(dWc), r["dWc"], env["dWc"], "dWc")
+    _env_ok(_np(dWo), r["dW_out"], env["dW_out"], "dW_out")
+    _env_ok(_np(eps)[:n], oracle.csr_values(r["eps"].reshape(T, B, N), rp, ci),
+            oracle.csr_values(env["eps"].reshape(T, B, N), rp, ci), "eps at conv entries")
+    assert np.abs(r["dWc"]).max() > 0
+    if dense:
+        _env_ok(_np(ddWc), r["dWc"], env["dWc"], "dense dWc")
+        _env_ok(_np(ddWo), r["dW_out"], env["dW_out"], "dense dW_out")
+        _env_ok(_np(deps), r["eps"].reshape(T, B, N), env["eps"].reshape(T, B, N), "dense eps")
+    return f, r
+
+
+@pytest.mark.parametrize("b_th,mode", [(0.2, "max"), (0.5, "sum"), (math.inf, "max")])
+def test_conv_parity_small(b_th, mode):
+    print(f"\n[case] conv small b_th={b_th} mode={mode}", flush=True)
+    X, Wc, Wo, y = _small()
+    _check(X, Wc, Wo, y, b_th, mode)
+
+
+def test_conv_parity_ragged():
+    """Filters not a multiple of 64, two input channels, a non-square map."""
+    print("\n[case] conv ragged", flush=True)
+    X, Wc, Wo, y = _small(T=17, B=3, H=6, W=10, C=2, Fo=40, Cls=3, rate=0.1, sigma=0.7, seed=4)
+    _check(X, Wc, Wo, y, 0.3)
+
+
+def test_conv_parity_workload_subset():
+    """The conv workload's own inputs and weights (28x28, 64 filters) on four samples."""
+    print("\n[case] conv workload, 4 samples", flush=True)
+    inp = make_conv_inputs(CONFIGS["conv"], [0, 1, 2, 3])
+    f, r = _check(inp.X, inp.Wc, inp.W_out, inp.labels, 0.2, dense=True)
+    assert r["mask"].mean() > 1e-3
