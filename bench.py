@@ -84,21 +84,36 @@ def cpu_baseline(cfg, b_th, n_samples):
         blas = [(d.get("internal_api"), d.get("num_threads")) for d in threadpool_info()]
     except Exception:  # pragma: no cover
         blas = []
-    n_samples = min(n_samples, cfg.B)
-    inp = make_inputs(cfg, list(range(n_samples)))
-    f = oracle.network_forward(inp.X, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, np.float32(cfg.theta))
+    n_samples = min(n_samples, cfg.B, 2 if cfg.conv else cfg.B)
+    if cfg.conv:
+        from oracle import conv as oconv
+        from synth.inputs import make_conv_inputs
+        inp = make_conv_inputs(cfg, list(range(n_samples)))
+        f = oconv.conv_network_forward(inp.X, inp.Wc, inp.W_out, cfg.alpha, cfg.alpha_out, cfg.theta)
+
+        def unit():
+            rp, _, _ = oracle.active_csr(f["V"].reshape(cfg.T, n_samples, -1), cfg.theta, b_th, cfg.beta)
+            oconv.conv_network_backward(f, inp.Wc, inp.W_out, cfg.alpha_out, inp.labels, cfg.loss_mode, cfg.theta,
+                                        b_th, cfg.beta)
+            return int(rp[-1])
+    else:
+        inp = make_inputs(cfg, list(range(n_samples)))
+        f = oracle.network_forward(inp.X, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, np.float32(cfg.theta))
+
+        def unit():
+            n = 0
+            for V in f["V"]:
+                rp, _, _ = oracle.active_csr(V, cfg.theta, b_th, cfg.beta)
+                n += int(rp[-1])
+            oracle.network_backward(f, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, inp.labels, cfg.loss_mode,
+                                    cfg.theta, b_th, cfg.beta)
+            return n
     # the timed unit is repeated until about CPU_TARGET_S of work has been measured
     reps, dt, nnz = 0, 0.0, 0
     while reps == 0 or (dt < CPU_TARGET_S and reps < 200):
         t0 = time.perf_counter()
-        n = 0
-        for V in f["V"]:
-            rp, _, _ = oracle.active_csr(V, cfg.theta, b_th, cfg.beta)
-            n += int(rp[-1])
-        oracle.network_backward(f, inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, inp.labels, cfg.loss_mode,
-                                cfg.theta, b_th, cfg.beta)
+        nnz += unit()
         dt += time.perf_counter() - t0
-        nnz += n
         reps += 1
     threads = max([n for _, n in blas if n] or [1])
     return {"value": nnz / dt, "unit": "active neuron-steps/s", "cores": threads, "kind": "oracle",
@@ -227,6 +242,117 @@ def train_experiment(args):
     result["train_step_speedup"] = result["full_surrogate"]["train_step_ms_median"] / result[runs[0][0]][
         "train_step_ms_median"]
     print(json.dumps(result), flush=True)
+
+
+class ConvRunner:
+    """The convolutional workload: conv LIF layer, 2x2 spike pooling, readout. Sparse chain =
+    compaction of the conv layer (and the pooled entries) + the readout's backward at the pooled
+    entries + routing to the conv entries + the sparse filter gradient; dense chain = the dense
+    readout backward + dense routing + the dense filter gradient."""
+
+    def __init__(self, cfg, args):
+        import torch
+        from paper_2105_08810_amd import pipeline, snn
+        from synth.inputs import make_conv_inputs
+        self.torch, self.snn = torch, snn
+        self.cfg, self.args = cfg, args
+        inp = make_conv_inputs(cfg)
+        dev = torch.device("cuda:0")
+        self.net = pipeline.ConvNetwork(
+            X=torch.from_numpy(inp.X).to(dev), Wc=torch.from_numpy(inp.Wc).to(dev),
+            W_out=torch.from_numpy(inp.W_out).to(dev), alpha=float(cfg.alpha), alpha_out=float(cfg.alpha_out),
+            labels=torch.from_numpy(inp.labels).to(dev), loss_mode=0 if cfg.loss_mode == "max" else 1,
+            theta=float(cfg.theta), beta=float(cfg.beta)).allocate()
+        T, B, H, W, C, F = self.net.dims
+        self.ws_sp = snn.workspace(snn.snn_conv_sparse_dw_workspace(T, B, H, W, C, F))
+        self.ws_dn = snn.workspace(snn.snn_conv_dense_dw_workspace(T, B, H, W, C, F))
+
+    def prepare(self, b_th):
+        self.b_th = b_th
+        self.net.forward(b_th)
+        self.caps = [c.capacity for c in self.net.compact(b_th)]
+
+    def events(self):
+        mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
+        return {k: mk() for k in ("fwd0", "fwd1", "cmp0", "cmp1", "bw1", "dn0", "dn1")}
+
+    def step(self, ev, dense=True):
+        net = self.net
+        with_dense = dense and not self.args.no_dense
+        ev["fwd0"].record()
+        net.forward(self.b_th)
+        ev["fwd1"].record()
+        ro = net.readout(dense=with_dense)
+        ev["cmp0"].record()
+        cs = net.compact(self.b_th, self.caps)
+        ev["cmp1"].record()
+        net.sparse_backward(cs, ro, ws=self.ws_sp)
+        ev["bw1"].record()
+        if with_dense:
+            ev["dn0"].record()
+            net.dense_backward(self.b_th, ro, ws=self.ws_dn)
+            ev["dn1"].record()
+        return cs
+
+    def run(self, steps, warmup, dense=True):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step(self.events(), dense)
+        torch.cuda.synchronize()
+        evs = [self.events() for _ in range(steps)]
+        t0 = time.perf_counter()
+        for k in range(steps):
+            cs = self.step(evs[k], dense)
+        torch.cuda.synchronize()
+        return evs, cs, time.perf_counter() - t0
+
+    def summarize(self, evs, cs, wall, dense=True):
+        med = lambda a: float(np.median(a))  # noqa: E731
+        span = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in evs])  # noqa: E731
+        T, B, H, W, C, F = self.net.dims
+        t_cmp = span("cmp0", "cmp1")
+        t_bw = span("cmp1", "bw1")
+        t_sparse = t_cmp + t_bw
+        with_dense = dense and not self.args.no_dense
+        nnz = cs[0].nnz()
+        nnz_pool = cs[1].nnz()
+        N = H * W * F
+        TB = T * B
+        # gathered bytes: compaction (bitset, CSR, g, V at active entries), pooled bits and CSR,
+        # readout backward at the pooled entries, routing, the filter gradient (entries and the
+        # input patches of entries with a gradient)
+        sparse_bytes = (TB * ((B * N + 63) // 64) // B * 8 + 12 * nnz + 4 * (TB + 1) + 2 * TB * self.net.Np
+                        + 8 * nnz_pool + 4 * (TB + 1) + 12 * nnz)
+        out = {
+            "metric": "sparse backward ms/batch + active neuron-steps/s, speedup vs dense BPTT",
+            "value": nnz / (med(t_sparse) * 1e-3),
+            "unit": "active neuron-steps/s",
+            "n_gpus": 1, "steps": len(evs), "warmup": self.args.warmup, "ms_per_step": med(span("fwd0", "dn1" if with_dense else "bw1")),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": f"{self.cfg.name}: {self.cfg.description}; B_th={self.b_th}", "T": T, "B": B,
+                       "H": H, "W": W, "C": C, "F": F, "b_th": self.b_th},
+            "sparse_backward_ms": med(t_sparse),
+            "sparse_backward_ms_iqr": [float(np.percentile(t_sparse, 25)), float(np.percentile(t_sparse, 75))],
+            "compaction_ms": med(t_cmp),
+            "sparse_chain_after_compaction_ms": med(t_bw),
+            "dense_backward_ms": med(span("dn0", "dn1")) if with_dense else None,
+            "forward_ms": med(span("fwd0", "fwd1")),
+            "active_fraction": [nnz / (TB * N)],
+            "pooled_active_entries": nnz_pool,
+            "nnz": [nnz],
+            "sparse_backward_gathered_bytes": sparse_bytes,
+            "sparse_backward_hbm_frac": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "memory_sparse_dense_bytes": [12 * nnz + 4 * (TB + 1) + 12 * nnz_pool + 4 * (TB + 1),
+                                          4 * TB * N + 4 * TB * self.net.Np],
+            "wall_s_timed": wall,
+        }
+        m = out["memory_sparse_dense_bytes"]
+        out["memory_saved_pct"] = [100.0 * (m[1] - m[0]) / m[1]]
+        if with_dense:
+            out["speedup_vs_dense"] = out["dense_backward_ms"] / out["sparse_backward_ms"]
+            out["overall_speedup_fwd_plus_bwd"] = (out["forward_ms"] + out["dense_backward_ms"]) / (
+                out["forward_ms"] + out["sparse_backward_ms"])
+        return out
 
 
 class Runner:
@@ -512,7 +638,7 @@ def main():
     from synth import CONFIGS
     snn.lib()
     cfg = CONFIGS[args.workload]
-    run = Runner(cfg, args)
+    run = ConvRunner(cfg, args) if cfg.conv else Runner(cfg, args)
     points = cfg.sweep() if args.sweep else (cfg.b_th if args.b_th is None else args.b_th,)
     dense_ms = None
     for k, b_th in enumerate(points):

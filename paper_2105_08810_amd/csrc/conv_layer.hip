@@ -19,30 +19,54 @@ namespace {
 constexpr int kCdwThreads = 256;
 constexpr int kCdwWaves = kCdwThreads / kWave;
 constexpr int kCdwMaxBlocks = 1024;
+constexpr int kDenseBlocks = 8192;  // blocks of the dense filter gradient (each walks its positions)
 constexpr int kDenseMaxC = 4;  // input channels held in registers by the dense filter gradient
 
 unsigned stream_blocks(int64_t items) {
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 65536));
 }
 
-__global__ void pool_kernel(const uint8_t* __restrict__ S, int H, int W, int F, int64_t total,
-                            uint8_t* __restrict__ P, uint8_t* __restrict__ arg) {
+// Rows r = t * B + b run along grid y (grid-stride), pooled neurons of a row along x; with
+// VEC (F % 4 == 0) a thread takes four neighbouring filters with 32-bit loads and stores.
+template <bool VEC>
+__global__ void pool_kernel(const uint8_t* __restrict__ S, int TB, int H, int W, int F, uint8_t* __restrict__ P,
+                            uint8_t* __restrict__ arg) {
   const int hw = W / 2;
-  const int hh = H / 2;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const int f = (int)(i % F);
-    int64_t rest = i / F;
-    const int px = (int)(rest % hw);
-    rest /= hw;
-    const int py = (int)(rest % hh);
-    const int64_t tb = rest / hh;
-    const int64_t base = ((tb * H + 2 * py) * W + 2 * px) * F + f;
-    const bool s0 = S[base] != 0;
-    const bool s1 = S[base + F] != 0;
-    const bool s2 = S[base + (int64_t)W * F] != 0;
-    const bool s3 = S[base + (int64_t)W * F + F] != 0;
-    P[i] = (uint8_t)(s0 | s1 | s2 | s3);
-    arg[i] = (uint8_t)(s0 ? 0 : (s1 ? 1 : (s2 ? 2 : (s3 ? 3 : 0))));
+  const int Np = (H / 2) * hw * F;
+  const int N = H * W * F;
+  const int j = (blockIdx.x * blockDim.x + threadIdx.x) * (VEC ? 4 : 1);
+  if (j >= Np) return;
+  const int f = j % F;
+  const int pp = j / F;
+  const int px = pp % hw;
+  const int py = pp / hw;
+  const int off = ((2 * py) * W + 2 * px) * F + f;
+  for (int r = blockIdx.y; r < TB; r += gridDim.y) {
+    const uint8_t* s = S + (int64_t)r * N + off;
+    const int64_t o = (int64_t)r * Np + j;
+    if (VEC) {
+      const uint32_t w0 = *reinterpret_cast<const uint32_t*>(s);
+      const uint32_t w1 = *reinterpret_cast<const uint32_t*>(s + F);
+      const uint32_t w2 = *reinterpret_cast<const uint32_t*>(s + W * F);
+      const uint32_t w3 = *reinterpret_cast<const uint32_t*>(s + W * F + F);
+      uint32_t pv = 0, av = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool s0 = (w0 >> (8 * q)) & 0xffu, s1 = (w1 >> (8 * q)) & 0xffu;
+        const bool s2 = (w2 >> (8 * q)) & 0xffu, s3 = (w3 >> (8 * q)) & 0xffu;
+        pv |= (uint32_t)(s0 | s1 | s2 | s3) << (8 * q);
+        av |= (uint32_t)(s0 ? 0 : (s1 ? 1 : (s2 ? 2 : (s3 ? 3 : 0)))) << (8 * q);
+      }
+      *reinterpret_cast<uint32_t*>(P + o) = pv;
+      *reinterpret_cast<uint32_t*>(arg + o) = av;
+    } else {
+      const bool s0 = s[0] != 0;
+      const bool s1 = s[F] != 0;
+      const bool s2 = s[W * F] != 0;
+      const bool s3 = s[W * F + F] != 0;
+      P[o] = (uint8_t)(s0 | s1 | s2 | s3);
+      arg[o] = (uint8_t)(s0 ? 0 : (s1 ? 1 : (s2 ? 2 : (s3 ? 3 : 0))));
+    }
   }
 }
 
@@ -50,29 +74,96 @@ __global__ void pool_kernel(const uint8_t* __restrict__ S, int H, int W, int F, 
 // active: one ballot per wavefront and step writes one word of the pooled bitset.
 __global__ void route_bits_kernel(const uint64_t* __restrict__ cbits, const uint8_t* __restrict__ arg, int T, int B,
                                   int H, int W, int F, uint64_t* __restrict__ pbits) {
-  const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
-  const int64_t N = (int64_t)H * W * F;
-  const int64_t W64p = (B * Np + kWave - 1) / kWave;
-  const int64_t W64c = (B * N + kWave - 1) / kWave;
-  const int64_t total = (int64_t)T * W64p * kWave;
-  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g - lane_id() < total;
-       g += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t t = g / (W64p * kWave);
-    const int64_t kp = g - t * W64p * kWave;
+  const int hw = W / 2;
+  const int Np = (H / 2) * hw * F;
+  const int N = H * W * F;
+  const int64_t W64p = ((int64_t)B * Np + kWave - 1) / kWave;
+  const int64_t W64c = ((int64_t)B * N + kWave - 1) / kWave;
+  const int kp = blockIdx.x * blockDim.x + threadIdx.x;  // kp - lane is a word start
+  if ((int64_t)(kp - lane_id()) >= W64p * kWave) return;  // whole wavefront past the last word
+  const bool valid = kp < B * Np;
+  int64_t kbase = 0;  // conv neuron of window position 0, and the arg offset inside a step
+  int ab = 0;
+  if (valid) {
+    const int b = kp / Np;
+    const int j = kp - b * Np;
+    const int f = j % F;
+    const int pp = j / F;
+    const int px = pp % hw;
+    const int py = pp / hw;
+    kbase = (int64_t)b * N + ((2 * py) * W + 2 * px) * F + f;
+    ab = b * Np + j;
+  }
+  for (int t = blockIdx.y; t < T; t += gridDim.y) {
     bool on = false;
-    if (g < total && kp < B * Np) {
-      const int64_t b = kp / Np;
-      const int64_t np_ = kp - b * Np;
-      const int f = (int)(np_ % F);
-      const int64_t pp = np_ / F;
-      const int px = (int)(pp % (W / 2));
-      const int py = (int)(pp / (W / 2));
-      const int a = arg[(t * B + b) * Np + np_] & 3;
-      const int64_t kc = b * N + ((int64_t)(2 * py + (a >> 1)) * W + 2 * px + (a & 1)) * F + f;
-      on = (cbits[t * W64c + kc / kWave] >> (kc % kWave)) & 1ull;
+    if (valid) {
+      const int a = arg[(int64_t)t * B * Np + ab] & 3;
+      const int64_t kc = kbase + ((a >> 1) * W + (a & 1)) * F;
+      on = (cbits[t * W64c + (kc >> 6)] >> (kc & 63)) & 1ull;
     }
     const uint64_t m = __ballot(on);
-    if (lane_id() == 0 && g < total) pbits[t * W64p + kp / kWave] = m;
+    if (lane_id() == 0) pbits[t * W64p + (kp >> 6)] = m;
+  }
+}
+
+// 16 bits to every fourth bit of a word: bit i goes to bit 4 i.
+__device__ __forceinline__ uint64_t spread16(uint64_t x) {
+  x &= 0xFFFFull;
+  x = (x | (x << 24)) & 0x000000FF000000FFull;
+  x = (x | (x << 12)) & 0x000F000F000F000Full;
+  x = (x | (x << 6)) & 0x0303030303030303ull;
+  x = (x | (x << 3)) & 0x1111111111111111ull;
+  return x;
+}
+
+// As route_bits_kernel with four neighbouring pooled neurons per lane (F % 4 == 0; one 32-bit
+// load of their pooling choices): a wavefront covers four words, built from four ballots whose
+// bits are interleaved (neuron 4 l + q of the wavefront is ballot q's lane l).
+__global__ void route_bits4_kernel(const uint64_t* __restrict__ cbits, const uint8_t* __restrict__ arg, int T, int B,
+                                   int H, int W, int F, uint64_t* __restrict__ pbits) {
+  const int hw = W / 2;
+  const int Np = (H / 2) * hw * F;
+  const int N = H * W * F;
+  const int64_t W64p = ((int64_t)B * Np + kWave - 1) / kWave;
+  const int64_t W64c = ((int64_t)B * N + kWave - 1) / kWave;
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  const int l = lane_id();
+  const int64_t word0 = (int64_t)(u - l) / 16;  // the wavefront's first word (256 neurons = 4 words)
+  if (word0 >= W64p) return;                    // whole wavefront past the last word
+  const int kp = 4 * u;
+  const bool valid = kp < B * Np;
+  int64_t kbase = 0;
+  int ab = 0;
+  if (valid) {
+    const int b = kp / Np;
+    const int j = kp - b * Np;
+    const int f = j % F;
+    const int pp = j / F;
+    const int px = pp % hw;
+    const int py = pp / hw;
+    kbase = (int64_t)b * N + ((2 * py) * W + 2 * px) * F + f;
+    ab = b * Np + j;
+  }
+  for (int t = blockIdx.y; t < T; t += gridDim.y) {
+    uint32_t a4 = 0;
+    if (valid) a4 = *reinterpret_cast<const uint32_t*>(arg + (int64_t)t * B * Np + ab);
+    uint64_t m[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      bool on = false;
+      if (valid) {
+        const int a = (a4 >> (8 * q)) & 3;
+        const int64_t kc = kbase + q + ((a >> 1) * W + (a & 1)) * F;
+        on = (cbits[t * W64c + (kc >> 6)] >> (kc & 63)) & 1ull;
+      }
+      m[q] = __ballot(on);
+    }
+    if (l < 4 && word0 + l < W64p) {
+      uint64_t w = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w |= spread16(m[q] >> (16 * l)) << q;
+      pbits[t * W64p + word0 + l] = w;
+    }
   }
 }
 
@@ -115,19 +206,34 @@ __global__ void scatter_kernel(int TB, int H, int W, int F, const int32_t* __res
 }
 
 // Dense form: eps_c[t,b,y,x,f] = eps_p[t,b,y/2,x/2,f] where (y, x) is the picked element, else 0.
-__global__ void scatter_dense_kernel(const float* __restrict__ eps_p, const uint8_t* __restrict__ arg, int H, int W,
-                                     int F, int64_t total, float* __restrict__ eps_c) {
-  const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
-  const int64_t N = (int64_t)H * W * F;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t r = i / N;
-    const int n = (int)(i - r * N);
-    const int f = n % F;
-    const int pix = n / F;
-    const int y = pix / W;
-    const int x = pix - y * W;
-    const int64_t ip = r * Np + ((int64_t)(y / 2) * (W / 2) + x / 2) * F + f;
-    eps_c[i] = (int)(arg[ip] & 3) == (y & 1) * 2 + (x & 1) ? eps_p[ip] : 0.0f;
+// Rows along grid y (grid-stride), conv neurons of a row along x.
+template <bool VEC>
+__global__ void scatter_dense_kernel(const float* __restrict__ eps_p, const uint8_t* __restrict__ arg, int TB, int H,
+                                     int W, int F, float* __restrict__ eps_c) {
+  const int Np = (H / 2) * (W / 2) * F;
+  const int N = H * W * F;
+  const int n = (blockIdx.x * blockDim.x + threadIdx.x) * (VEC ? 4 : 1);  // VEC: four filters of one pixel
+  if (n >= N) return;
+  const int f = n % F;
+  const int pix = n / F;
+  const int y = pix / W;
+  const int x = pix - y * W;
+  const int jp = ((y / 2) * (W / 2) + x / 2) * F + f;
+  const int pos = (y & 1) * 2 + (x & 1);
+  for (int r = blockIdx.y; r < TB; r += gridDim.y) {
+    const int64_t ip = (int64_t)r * Np + jp;
+    if (VEC) {
+      const uint32_t a4 = *reinterpret_cast<const uint32_t*>(arg + ip);
+      const float4 e4 = *reinterpret_cast<const float4*>(eps_p + ip);
+      float4 o;
+      o.x = (int)(a4 & 3u) == pos ? e4.x : 0.0f;
+      o.y = (int)((a4 >> 8) & 3u) == pos ? e4.y : 0.0f;
+      o.z = (int)((a4 >> 16) & 3u) == pos ? e4.z : 0.0f;
+      o.w = (int)((a4 >> 24) & 3u) == pos ? e4.w : 0.0f;
+      *reinterpret_cast<float4*>(eps_c + (int64_t)r * N + n) = o;
+    } else {
+      eps_c[(int64_t)r * N + n] = (int)(arg[ip] & 3) == pos ? eps_p[ip] : 0.0f;
+    }
   }
 }
 
@@ -135,6 +241,7 @@ __global__ void scatter_dense_kernel(const float* __restrict__ eps_p, const uint
 // entries; an entry with G = eps * g != 0 adds G * trace over its 3x3xC input patch into the
 // block's float64 accumulator [9 * C][F] in LDS. Each block writes its sums; a fixed-order
 // reduction over blocks gives dWc.
+template <int CT>  // CT > 0: C == CT and the patch's loads are issued together; 0: any C
 __global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
     const float* __restrict__ trace, int TB, int H, int W, int C, int F, const int32_t* __restrict__ rp,
     const int32_t* __restrict__ col, const float* __restrict__ g, const float* __restrict__ eps, int64_t cap,
@@ -160,14 +267,30 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
       const int pix = n / F;
       const int y = pix / W;
       const int x = pix - y * W;
-      for (int ky = 0; ky < 3; ++ky) {
-        const int yy = y + ky - 1;
-        if (yy < 0 || yy >= H) continue;
-        for (int kx = 0; kx < 3; ++kx) {
-          const int xx = x + kx - 1;
-          if (xx < 0 || xx >= W) continue;
-          const float* tp = tr + ((int64_t)yy * W + xx) * C;
-          for (int c = 0; c < C; ++c) atomicAdd(&cacc[((ky * 3 + kx) * C + c) * F + f], (double)G * (double)tp[c]);
+      if (CT > 0) {
+        float tv[9 * (CT > 0 ? CT : 1)];
+#pragma unroll
+        for (int tap = 0; tap < 9; ++tap) {
+          const int yy = y + tap / 3 - 1;
+          const int xx = x + tap % 3 - 1;
+          const bool in = yy >= 0 && yy < H && xx >= 0 && xx < W;
+          const float* tp = tr + ((int64_t)(in ? yy : 0) * W + (in ? xx : 0)) * CT;
+#pragma unroll
+          for (int c = 0; c < CT; ++c) tv[tap * CT + c] = in ? tp[c] : 0.0f;
+        }
+#pragma unroll
+        for (int i = 0; i < 9 * (CT > 0 ? CT : 1); ++i)  // a zero trace adds nothing: skipped
+          if (tv[i] != 0.0f) atomicAdd(&cacc[i * F + f], (double)G * (double)tv[i]);
+      } else {
+        for (int ky = 0; ky < 3; ++ky) {
+          const int yy = y + ky - 1;
+          if (yy < 0 || yy >= H) continue;
+          for (int kx = 0; kx < 3; ++kx) {
+            const int xx = x + kx - 1;
+            if (xx < 0 || xx >= W) continue;
+            const float* tp = tr + ((int64_t)yy * W + xx) * C;
+            for (int c = 0; c < C; ++c) atomicAdd(&cacc[((ky * 3 + kx) * C + c) * F + f], (double)G * (double)tp[c]);
+          }
         }
       }
     }
@@ -176,12 +299,21 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
   for (int i = threadIdx.x; i < nacc; i += kCdwThreads) part[(int64_t)blockIdx.x * nacc + i] = cacc[i];
 }
 
-__global__ void reduce_parts(const double* __restrict__ part, int n_parts, int n, float* __restrict__ out) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-    double s = 0.0;
-    for (int p = 0; p < n_parts; ++p) s += part[(int64_t)p * n + i];
-    out[i] = (float)s;
+// out[i] = sum over p of part[p][i]: one block per output, 256 threads take fixed strided
+// subsets of the partials and a fixed tree joins them (deterministic).
+__global__ __launch_bounds__(256) void reduce_parts(const double* __restrict__ part, int n_parts, int n,
+                                                    float* __restrict__ out) {
+  __shared__ double red[256];
+  const int i = blockIdx.x;
+  double s = 0.0;
+  for (int p = threadIdx.x; p < n_parts; p += 256) s += part[(int64_t)p * n + i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
   }
+  if (threadIdx.x == 0) out[i] = (float)red[0];
 }
 
 // Dense filter gradient of the full (b_th = inf) or truncated surrogate: every position
@@ -205,7 +337,18 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_dense_kernel(
     float acc[9 * CMAX];
 #pragma unroll
     for (int q = 0; q < 9 * CMAX; ++q) acc[q] = 0.0f;
+    const int HW = H * W;
+    int64_t r = (p_lo + w) / HW;  // position p = r * HW + pix, advanced without division
+    int pix = (int)(p_lo + w - r * HW);
     for (int64_t p = p_lo + w; p < p_hi; p += kCdwWaves) {
+      const int y = pix / W;
+      const int x = pix - y * W;
+      const int64_t r_here = r;
+      pix += kCdwWaves;
+      while (pix >= HW) {
+        pix -= HW;
+        ++r;
+      }
       float G = 0.0f;
       if (fv) {
         const float v = V[p * F + f];
@@ -214,11 +357,7 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_dense_kernel(
         G = d < b_th ? eps[p * F + f] / (q * q) : 0.0f;
       }
       if (__ballot(G != 0.0f) == 0ull) continue;
-      const int64_t r = p / ((int64_t)H * W);
-      const int pix = (int)(p - r * H * W);
-      const int y = pix / W;
-      const int x = pix - y * W;
-      const float* tr = trace + r * (int64_t)H * W * C;
+      const float* tr = trace + r_here * (int64_t)HW * C;
 #pragma unroll
       for (int ky = 0; ky < 3; ++ky) {
         const int yy = y + ky - 1;
@@ -258,7 +397,7 @@ bool conv_dims_ok(int T, int B, int H, int W, int F) {
 
 int cdw_blocks(int TB) { return std::max(1, std::min(kCdwMaxBlocks, TB)); }
 
-int64_t dense_blocks(int64_t n_pos) { return std::max<int64_t>(1, std::min<int64_t>(kCdwMaxBlocks, (n_pos + 63) / 64)); }
+int64_t dense_blocks(int64_t n_pos) { return std::max<int64_t>(1, std::min<int64_t>(kDenseBlocks, (n_pos + 63) / 64)); }
 
 }  // namespace
 }  // namespace snn
@@ -269,9 +408,18 @@ extern "C" snn_status snn_maxpool_spikes(const uint8_t* S, int T, int B, int H, 
                                          uint8_t* arg, void* stream) {
   if (!S || !P || !arg) return SNN_ERR_INVALID_ARG;
   if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
-  const int64_t total = (int64_t)T * B * (H / 2) * (W / 2) * F;
-  hipLaunchKernelGGL(pool_kernel, dim3(stream_blocks(total)), dim3(256), 0, static_cast<hipStream_t>(stream), S, H, W,
-                     F, total, P, arg);
+  const int Np = (H / 2) * (W / 2) * F;
+  const int TB = T * B;
+  const bool vec = F % 4 == 0 && ((uintptr_t)S & 3u) == 0 && ((uintptr_t)P & 3u) == 0 && ((uintptr_t)arg & 3u) == 0;
+  const int per = vec ? 4 : 1;
+  const unsigned bx = (unsigned)((Np / per + 255) / 256);
+  const unsigned by = (unsigned)std::max(1, std::min(TB, (int)(65536 / bx) + 1));
+  if (vec)
+    hipLaunchKernelGGL(pool_kernel<true>, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream), S, TB, H, W, F,
+                       P, arg);
+  else
+    hipLaunchKernelGGL(pool_kernel<false>, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream), S, TB, H, W,
+                       F, P, arg);
   return launch_status();
 }
 
@@ -280,9 +428,20 @@ extern "C" snn_status snn_pool_route_bits(const uint64_t* conv_bits, const uint8
   if (!conv_bits || !arg || !pool_bits) return SNN_ERR_INVALID_ARG;
   if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
   const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
-  const int64_t total = (int64_t)T * ((B * Np + kWave - 1) / kWave) * kWave;
-  hipLaunchKernelGGL(route_bits_kernel, dim3(stream_blocks(total)), dim3(256), 0, static_cast<hipStream_t>(stream),
-                     conv_bits, arg, T, B, H, W, F, pool_bits);
+  if ((int64_t)B * Np + kWave >= ((int64_t)1 << 31)) return SNN_ERR_INVALID_ARG;
+  const int64_t lanes = ((B * Np + kWave - 1) / kWave) * kWave;
+  if (F % 4 == 0 && ((uintptr_t)arg & 3u) == 0) {
+    const int64_t threads = ((B * Np / 4 + kWave - 1) / kWave) * kWave;
+    const unsigned bx = (unsigned)((threads + 255) / 256);
+    const unsigned by = (unsigned)std::max(1, std::min(T, (int)(65536 / bx) + 1));
+    hipLaunchKernelGGL(route_bits4_kernel, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream), conv_bits, arg,
+                       T, B, H, W, F, pool_bits);
+  } else {
+    const unsigned bx = (unsigned)((lanes + 255) / 256);
+    const unsigned by = (unsigned)std::max(1, std::min(T, (int)(65536 / bx) + 1));
+    hipLaunchKernelGGL(route_bits_kernel, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream), conv_bits, arg,
+                       T, B, H, W, F, pool_bits);
+  }
   return launch_status();
 }
 
@@ -311,9 +470,18 @@ extern "C" snn_status snn_pool_scatter_eps_dense(const float* eps_pool, const ui
                                                  int F, float* eps_conv, void* stream) {
   if (!eps_pool || !arg || !eps_conv) return SNN_ERR_INVALID_ARG;
   if (!conv_dims_ok(T, B, H, W, F)) return SNN_ERR_INVALID_ARG;
-  const int64_t total = (int64_t)T * B * H * W * F;
-  hipLaunchKernelGGL(scatter_dense_kernel, dim3(stream_blocks(total)), dim3(256), 0, static_cast<hipStream_t>(stream),
-                     eps_pool, arg, H, W, F, total, eps_conv);
+  const int N = H * W * F;
+  const int TB = T * B;
+  const bool vec = F % 4 == 0 && ((uintptr_t)arg & 3u) == 0 && ((uintptr_t)eps_pool & 15u) == 0 &&
+                   ((uintptr_t)eps_conv & 15u) == 0;
+  const unsigned bx = (unsigned)((N / (vec ? 4 : 1) + 255) / 256);
+  const unsigned by = (unsigned)std::max(1, std::min(TB, (int)(65536 / bx) + 1));
+  if (vec)
+    hipLaunchKernelGGL(scatter_dense_kernel<true>, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream),
+                       eps_pool, arg, TB, H, W, F, eps_conv);
+  else
+    hipLaunchKernelGGL(scatter_dense_kernel<false>, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream),
+                       eps_pool, arg, TB, H, W, F, eps_conv);
   return launch_status();
 }
 
@@ -338,10 +506,15 @@ extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, in
   const int nacc = 9 * C * F;
   double* part = static_cast<double*>(workspace);
   const size_t lds = (size_t)nacc * sizeof(double);
-  (void)hipFuncSetAttribute((const void*)conv_dw_sparse_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  hipLaunchKernelGGL(conv_dw_sparse_kernel, dim3((unsigned)nb), dim3(kCdwThreads), lds, s, trace_in, TB, H, W, C, F,
-                     conv_row_ptr, conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part);
-  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)((nacc + 255) / 256)), dim3(256), 0, s, part, nb, nacc, dWc);
+  auto launch = [&](auto kernel) {
+    (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCdwThreads), lds, s, trace_in, TB, H, W, C, F, conv_row_ptr,
+                       conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part);
+  };
+  if (C == 1) launch(conv_dw_sparse_kernel<1>);
+  else if (C == 2) launch(conv_dw_sparse_kernel<2>);
+  else launch(conv_dw_sparse_kernel<0>);
+  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)nacc), dim3(256), 0, s, part, nb, nacc, dWc);
   return launch_status();
 }
 
@@ -370,6 +543,6 @@ extern "C" snn_status snn_conv_dense_dw(const float* trace_in, const float* V, c
   else
     hipLaunchKernelGGL(conv_dw_dense_kernel<kDenseMaxC>, dim3((unsigned)nb), dim3(kCdwThreads), 0, s, trace_in, V,
                        eps_conv, n_pos, H, W, C, F, theta, b_th, beta, ppb, part);
-  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)((nacc + 255) / 256)), dim3(256), 0, s, part, (int)nb, nacc, dWc);
+  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)nacc), dim3(256), 0, s, part, (int)nb, nacc, dWc);
   return launch_status();
 }

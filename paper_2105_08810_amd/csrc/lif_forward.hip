@@ -236,10 +236,14 @@ namespace {
 // k = b * N + n, n = (y * W + x) * F + f, N = H * W * F. Its weighted input at step t is the
 // filter applied to the input spikes of the 3x3 patch, added in ascending input index
 // (y', x', c) from +0.0 in separately rounded float32 adds (the order of the layer's Toeplitz
-// matrix in the fully connected form), then the same recurrence and marking as lif_scan. The
-// currents of kConvAhead steps are formed before their recurrence so that their loads overlap.
+// matrix in the fully connected form), then the same recurrence and marking as lif_scan.
+// WAVE_PIXEL (F a multiple of 64): a wavefront's 64 neurons share one pixel, so its lanes load
+// the patch bytes of several steps at once (lane = (step, tap)), one ballot gives the spiking
+// taps of those steps, and each lane adds its filter's weights for the set taps in tap order.
+// Otherwise each lane forms its own patch sums, kConvAhead steps at a time.
 constexpr int kConvAhead = 8;
 
+template <bool WAVE_PIXEL>
 __global__ __launch_bounds__(kScanThreads) void conv_scan(const uint8_t* __restrict__ s_in, const float* __restrict__ Wc,
                                                           int T, int B, int H, int W, int C, int F, float alpha,
                                                           float theta, float b_th, float* __restrict__ V,
@@ -261,28 +265,60 @@ __global__ __launch_bounds__(kScanThreads) void conv_scan(const uint8_t* __restr
   const size_t wword = k0 / kWave;
   const size_t in_step = (size_t)B * H * W * C;
   const uint8_t* xb = s_in + (size_t)b * H * W * C;
+  const int ntap = 9 * C;
+  // WAVE_PIXEL: lane l < q * ntap loads tap (l % ntap) of step (l / ntap) of the group
+  const int q = WAVE_PIXEL ? min(kConvAhead, kWave / ntap) : kConvAhead;
+  const int l = lane_id();
+  const int lp = l / ntap;
+  const int ltap = l - lp * ntap;
+  const int lky = ltap / (3 * C);
+  const int lkx = (ltap / C) % 3;
+  const int lc = ltap % C;
+  const int lyy = y + lky - 1;
+  const int lxx = x + lkx - 1;
+  const bool lin = lp < q && lyy >= 0 && lyy < H && lxx >= 0 && lxx < W;
+  const size_t loff = ((size_t)(lin ? lyy : 0) * W + (lin ? lxx : 0)) * C + lc;
+  const uint64_t tapmask = ntap >= 64 ? ~0ull : ((1ull << ntap) - 1ull);
   float v = 0.0f;
   if (valid) V[k] = 0.0f;
   if (bits) mark_active(bits, wword, valid, v, theta, b_th);
-  for (int t0 = 0; t0 < T - 1; t0 += kConvAhead) {
-    const int np = min(kConvAhead, T - 1 - t0);
+  for (int t0 = 0; t0 < T - 1; t0 += q) {
+    const int np = min(q, T - 1 - t0);
     float in[kConvAhead];
+    if (WAVE_PIXEL) {
+      const bool ld = lin && lp < np;
+      const uint64_t m = __ballot(ld && xb[(size_t)(t0 + lp) * in_step + loff] != 0);
 #pragma unroll
-    for (int p = 0; p < kConvAhead; ++p) {
-      const uint8_t* xt = xb + (size_t)(t0 + min(p, np - 1)) * in_step;
-      float acc = 0.0f;
-      for (int ky = 0; ky < 3; ++ky) {
-        const int yy = y + ky - 1;
-        if (yy < 0 || yy >= H) continue;
-        for (int kx = 0; kx < 3; ++kx) {
-          const int xx = x + kx - 1;
-          if (xx < 0 || xx >= W) continue;
-          const uint8_t* px = xt + ((size_t)yy * W + xx) * C;
-          for (int c = 0; c < C; ++c)
-            if (px[c]) acc = __fadd_rn(acc, Wc[((ky * 3 + kx) * C + c) * F + f]);
+      for (int p = 0; p < kConvAhead; ++p) {
+        float acc = 0.0f;
+        if (p < np) {
+          uint64_t taps = (m >> (p * ntap)) & tapmask;
+          while (taps) {
+            const int tap = __builtin_ctzll(taps);
+            acc = __fadd_rn(acc, Wc[tap * F + f]);
+            taps &= taps - 1ull;
+          }
         }
+        in[p] = acc;
       }
-      in[p] = acc;
+    } else {
+#pragma unroll
+      for (int p = 0; p < kConvAhead; ++p) {
+        const uint8_t* xt = xb + (size_t)(t0 + min(p, np - 1)) * in_step;
+        float acc = 0.0f;
+        for (int ky = 0; ky < 3; ++ky) {
+          const int yy = y + ky - 1;
+          if (yy < 0 || yy >= H) continue;
+          for (int kx = 0; kx < 3; ++kx) {
+            const int xx = x + kx - 1;
+            if (xx < 0 || xx >= W) continue;
+            const uint8_t* px = xt + ((size_t)yy * W + xx) * C;
+            for (int c = 0; c < C; ++c)
+              if (px[c]) acc = __fadd_rn(acc, Wc[((ky * 3 + kx) * C + c) * F + f]);
+          }
+        }
+        in[p] = acc;
+      }
     }
 #pragma unroll
     for (int p = 0; p < kConvAhead; ++p) {
@@ -365,8 +401,12 @@ extern "C" snn_status snn_conv_lif_forward(const uint8_t* s_in, const float* Wc,
   if (active_bits && (isnan(b_th) || b_th < 0.0f)) return SNN_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int nv = (int)(((size_t)B * H * W * F + kScanThreads - 1) / kScanThreads);
-  hipLaunchKernelGGL(conv_scan, dim3((unsigned)nv), dim3(kScanThreads), 0, s, s_in, Wc, T, B, H, W, C, F, alpha, theta,
-                     b_th, V, s_out, active_bits);
+  if (F % kWave == 0 && 9 * C <= kWave)  // a wavefront's lanes are the filters of one pixel
+    hipLaunchKernelGGL(conv_scan<true>, dim3((unsigned)nv), dim3(kScanThreads), 0, s, s_in, Wc, T, B, H, W, C, F, alpha,
+                       theta, b_th, V, s_out, active_bits);
+  else
+    hipLaunchKernelGGL(conv_scan<false>, dim3((unsigned)nv), dim3(kScanThreads), 0, s, s_in, Wc, T, B, H, W, C, F,
+                       alpha, theta, b_th, V, s_out, active_bits);
   if (trace_in) {  // the input trace: lif_scan's trace blocks alone
     const int N_in = H * W * C;
     const int nt = (int)(((size_t)B * ((N_in + 3) / 4) + kScanThreads - 1) / kScanThreads);
