@@ -330,7 +330,7 @@ snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, int H, int W,
 /*
  * Dense filter gradient (the baseline): every neuron's G = eps_conv * g(V) * [|V - theta| < b_th]
  * (b_th = +INFINITY: full surrogate) with eps_conv dense [T,B,H*W*F], then the same sum.
- * SNN_ERR_UNSUPPORTED when C > 4.
+ * SNN_ERR_UNSUPPORTED when C*F > 2^20.
  */
 size_t snn_conv_dense_dw_workspace(int T, int B, int H, int W, int C, int F);
 snn_status snn_conv_dense_dw(const float* trace_in, const float* V, const float* eps_conv, int T, int B, int H, int W,

@@ -20,7 +20,7 @@ constexpr int kCdwThreads = 256;
 constexpr int kCdwWaves = kCdwThreads / kWave;
 constexpr int kCdwMaxBlocks = 1024;
 constexpr int kDenseBlocks = 8192;  // blocks of the dense filter gradient (each walks its positions)
-constexpr int kDenseMaxC = 4;  // input channels held in registers by the dense filter gradient
+constexpr int kDenseMaxC = 4;  // input channels per register group of the dense filter gradient
 
 unsigned stream_blocks(int64_t items) {
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 65536));
@@ -331,61 +331,63 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_dense_kernel(
   const int nacc = 9 * C * F;
   const int64_t p_lo = (int64_t)blockIdx.x * pos_per_block;
   const int64_t p_hi = std::min<int64_t>(n_pos, p_lo + pos_per_block);
-  for (int f0 = 0; f0 < F; f0 += kWave) {
-    const int f = f0 + l;
-    const bool fv = f < F;
-    float acc[9 * CMAX];
+  for (int f0 = 0; f0 < F; f0 += kWave)
+    for (int c0 = 0; c0 < C; c0 += CMAX) {  // channels in groups of CMAX registers
+      const int CG = min(CMAX, C - c0);
+      const int f = f0 + l;
+      const bool fv = f < F;
+      float acc[9 * CMAX];
 #pragma unroll
-    for (int q = 0; q < 9 * CMAX; ++q) acc[q] = 0.0f;
-    const int HW = H * W;
-    int64_t r = (p_lo + w) / HW;  // position p = r * HW + pix, advanced without division
-    int pix = (int)(p_lo + w - r * HW);
-    for (int64_t p = p_lo + w; p < p_hi; p += kCdwWaves) {
-      const int y = pix / W;
-      const int x = pix - y * W;
-      const int64_t r_here = r;
-      pix += kCdwWaves;
-      while (pix >= HW) {
-        pix -= HW;
-        ++r;
-      }
-      float G = 0.0f;
-      if (fv) {
-        const float v = V[p * F + f];
-        const float d = fabsf(v - theta);
-        const float q = beta * d + 1.0f;
-        G = d < b_th ? eps[p * F + f] / (q * q) : 0.0f;
-      }
-      if (__ballot(G != 0.0f) == 0ull) continue;
-      const float* tr = trace + r_here * (int64_t)HW * C;
+      for (int q = 0; q < 9 * CMAX; ++q) acc[q] = 0.0f;
+      const int HW = H * W;
+      int64_t r = (p_lo + w) / HW;  // position p = r * HW + pix, advanced without division
+      int pix = (int)(p_lo + w - r * HW);
+      for (int64_t p = p_lo + w; p < p_hi; p += kCdwWaves) {
+        const int y = pix / W;
+        const int x = pix - y * W;
+        const int64_t r_here = r;
+        pix += kCdwWaves;
+        while (pix >= HW) {
+          pix -= HW;
+          ++r;
+        }
+        float G = 0.0f;
+        if (fv) {
+          const float v = V[p * F + f];
+          const float d = fabsf(v - theta);
+          const float q = beta * d + 1.0f;
+          G = d < b_th ? eps[p * F + f] / (q * q) : 0.0f;
+        }
+        if (__ballot(G != 0.0f) == 0ull) continue;
+        const float* tr = trace + r_here * (int64_t)HW * C + c0;
 #pragma unroll
-      for (int ky = 0; ky < 3; ++ky) {
-        const int yy = y + ky - 1;
+        for (int ky = 0; ky < 3; ++ky) {
+          const int yy = y + ky - 1;
 #pragma unroll
-        for (int kx = 0; kx < 3; ++kx) {
-          const int xx = x + kx - 1;
-          const bool in = yy >= 0 && yy < H && xx >= 0 && xx < W;
+          for (int kx = 0; kx < 3; ++kx) {
+            const int xx = x + kx - 1;
+            const bool in = yy >= 0 && yy < H && xx >= 0 && xx < W;
 #pragma unroll
-          for (int c = 0; c < CMAX; ++c)
-            if (c < C && in) acc[(ky * 3 + kx) * CMAX + c] += G * tr[((int64_t)yy * W + xx) * C + c];
+            for (int c = 0; c < CMAX; ++c)
+              if (c < CG && in) acc[(ky * 3 + kx) * CMAX + c] += G * tr[((int64_t)yy * W + xx) * C + c];
+          }
         }
       }
-    }
 #pragma unroll
-    for (int q = 0; q < 9 * CMAX; ++q) red[w][q][l] = acc[q];
-    __syncthreads();
-    for (int i = threadIdx.x; i < 9 * C * kWave; i += kCdwThreads) {
-      const int tap = i / (C * kWave);
-      const int c = (i / kWave) % C;
-      const int ll = i % kWave;
-      if (f0 + ll < F) {
-        double s = 0.0;
-        for (int ww = 0; ww < kCdwWaves; ++ww) s += (double)red[ww][tap * CMAX + c][ll];
-        part[(int64_t)blockIdx.x * nacc + (tap * C + c) * F + f0 + ll] = s;
+      for (int q = 0; q < 9 * CMAX; ++q) red[w][q][l] = acc[q];
+      __syncthreads();
+      for (int i = threadIdx.x; i < 9 * CG * kWave; i += kCdwThreads) {
+        const int tap = i / (CG * kWave);
+        const int c = (i / kWave) % CG;
+        const int ll = i % kWave;
+        if (f0 + ll < F) {
+          double s = 0.0;
+          for (int ww = 0; ww < kCdwWaves; ++ww) s += (double)red[ww][tap * CMAX + c][ll];
+          part[(int64_t)blockIdx.x * nacc + (tap * C + c0 + c) * F + f0 + ll] = s;
+        }
       }
+      __syncthreads();
     }
-    __syncthreads();
-  }
 }
 
 bool conv_dims_ok(int T, int B, int H, int W, int F) {
@@ -519,7 +521,7 @@ extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, in
 }
 
 extern "C" size_t snn_conv_dense_dw_workspace(int T, int B, int H, int W, int C, int F) {
-  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || C > kDenseMaxC) return 0;
+  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || C * F > (1 << 20)) return 0;
   return align256((size_t)dense_blocks((int64_t)T * B * H * W) * 9 * C * F * sizeof(double));
 }
 
@@ -529,7 +531,7 @@ extern "C" snn_status snn_conv_dense_dw(const float* trace_in, const float* V, c
   if (!trace_in || !V || !eps_conv || !dWc || !workspace) return SNN_ERR_INVALID_ARG;
   if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || too_big(T, B, H * W * C)) return SNN_ERR_INVALID_ARG;
   if (isnan(theta) || isnan(b_th) || b_th < 0.0f || isnan(beta) || beta < 0.0f) return SNN_ERR_INVALID_ARG;
-  if (C > kDenseMaxC) return SNN_ERR_UNSUPPORTED;
+  if (C * F > (1 << 20)) return SNN_ERR_UNSUPPORTED;
   if (workspace_bytes < snn_conv_dense_dw_workspace(T, B, H, W, C, F)) return SNN_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t n_pos = (int64_t)T * B * H * W;

@@ -278,8 +278,8 @@ def test_conv_entry_points_reject(lib):
     assert lib.snn_conv_sparse_dw(FAKE, 10, 4, 8, 8, 64, 64, FAKE, FAKE, FAKE, FAKE, 100, FAKE, FAKE, 1 << 40,
                                   None) == snn.SNN_ERR_UNSUPPORTED
     wd = lib.snn_conv_dense_dw_workspace(10, 4, 8, 8, 1, 64)
-    assert wd > 0 and lib.snn_conv_dense_dw_workspace(10, 4, 8, 8, 5, 64) == 0
+    assert wd > 0 and lib.snn_conv_dense_dw_workspace(10, 4, 7, 8, 1, 64) == 0
     assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 1, 64, 1.0, NAN, 100.0, FAKE, FAKE, wd, None) == E
     assert lib.snn_conv_dense_dw(FAKE, None, FAKE, 10, 4, 8, 8, 1, 64, 1.0, 0.2, 100.0, FAKE, FAKE, wd, None) == E
-    assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 5, 64, 1.0, 0.2, 100.0, FAKE, FAKE, 1 << 40,
+    assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 4096, 512, 1.0, 0.2, 100.0, FAKE, FAKE, 1 << 40,
                                  None) == snn.SNN_ERR_UNSUPPORTED

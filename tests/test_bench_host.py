@@ -1,0 +1,90 @@
+"""bench.py's host-side logic and its output contract.
+
+CPU: the one-GPU guard, the algorithmic byte and flop counts against a hand count, and the
+App. H statistics against the oracle's. GPU: one short run of the default line on the tiny
+workload and of the training mode, checked for the fields the line must carry.
+"""
+import json
+import math
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import bench
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _run(args, env=None, timeout=600):
+    e = dict(os.environ)
+    e.update(env or {})
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                          env=e, timeout=timeout)
+
+
+@pytest.mark.parametrize("args,env", [(["--gpus", "2"], None), ([], {"WORLD_SIZE": "4"})])
+def test_more_than_one_gpu_is_refused(args, env):
+    r = _run(args, env)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_algorithmic_counts_by_hand():
+    # T=2, B=3, 5 inputs, 4 outputs; 7 active outputs on 4 rows, 6 input-active entries
+    by_dw, fl_dw, by_gi, fl_gi = bench.algorithmic(2, 3, 5, 4, nnz_out=7, r_out=4, nnz_in=6)
+    assert by_dw == 4 * 5 * 4 + 12 * 7 + 4 * 7 + 4 * 5 * 4
+    assert fl_dw == 2 * 7 * 5
+    assert by_gi == 4 * 5 * 4 + 8 * 6 + 4 * 7
+    assert fl_gi == 2 * 6 * 4 + 2 * 6 * 4
+    assert bench.algorithmic(2, 3, 5, 4, 7, 4)[2:] == (0, 0)
+
+
+def test_grad_difference_matches_oracle():
+    r = np.random.default_rng(2)
+    full = r.standard_normal((30, 20))
+    sparse = full + 0.05 * r.standard_normal((30, 20))
+    sparse[full == full.max()] = 0.0
+    a = bench._grad_difference(sparse, full)
+    b = oracle.gradient_difference(sparse, full)
+    for k in b:
+        assert a[k] == pytest.approx(b[k], rel=1e-12)
+
+
+def test_roofline_peaks_from_unit_counts():
+    assert bench.LDS_F64_RMW_TFLOPS == pytest.approx(2 * 256 * 2.4e9 * 128 / 16 / 1e12)
+    assert bench.HBM_PEAK_GBS == 8000.0
+    assert bench.MFMA_F32_TFLOPS == 157.3
+
+
+@pytest.mark.gpu
+def test_bench_line_on_tiny():
+    r = _run(["--workload", "tiny", "--steps", "3", "--warmup", "1"])
+    assert r.returncode == 0, r.stderr[-2000:]
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better", "scaling",
+              "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"):
+        assert k in line, k
+    assert line["n_gpus"] == 1 and line["steps"] == 3 and line["warmup"] == 1
+    assert line["config"]["workload"].startswith("tiny")
+    rl = line["roofline"]
+    assert rl["bound"] in ("hbm", "mfma", "alu") and rl["peak"] > 0 and 0 < rl["frac"] < 1
+    assert math.isclose(rl["frac"], rl["achieved"] / rl["peak"], rel_tol=1e-9)
+    cb = line["cpu_baseline"]
+    assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0
+    assert line["value"] > 0 and line["sparse_backward_ms"] > 0 and line["dense_backward_ms"] > 0
+
+
+@pytest.mark.gpu
+def test_bench_train_mode_short():
+    r = _run(["--train", "--train-steps", "20", "--train-batches", "2", "--train-bth", "0.2"])
+    assert r.returncode == 0, r.stderr[-2000:]
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    assert line["mode"] == "train" and line["steps"] == 20
+    for run in ("sparse_bth_0.2", "full_surrogate"):
+        assert len(line[run]["ce"]) == 20 and all(np.isfinite(line[run]["ce"]))
+        assert line[run]["ce"][-1] < line[run]["ce"][0]  # 20 Adam steps lower the loss
+    assert len(line["grad_difference_init"]) == 3

@@ -57,7 +57,7 @@ def _csr_from_mask(m):
     return rp, cols.astype(np.int64)
 
 
-def _check(X, Wc, Wo, y, b_th, mode="max", dense=True):
+def _check(X, Wc, Wo, y, b_th, mode="max", dense=True, nonzero=True):
     T, B, H, W, C = X.shape
     Fo = Wc.shape[3]
     a = F32(math.exp(-0.1))
@@ -109,7 +109,8 @@ def _check(X, Wc, Wo, y, b_th, mode="max", dense=True):
     _env_ok(_np(dWo), r["dW_out"], env["dW_out"], "dW_out")
     _env_ok(_np(eps)[:n], oracle.csr_values(r["eps"].reshape(T, B, N), rp, ci),
             oracle.csr_values(env["eps"].reshape(T, B, N), rp, ci), "eps at conv entries")
-    assert np.abs(r["dWc"]).max() > 0
+    if nonzero:  # the case has gradient to check (not a degenerate one)
+        assert np.abs(r["dWc"]).max() > 0
     if dense:
         _env_ok(_np(ddWc), r["dWc"], env["dWc"], "dense dWc")
         _env_ok(_np(ddWo), r["dW_out"], env["dW_out"], "dense dW_out")
@@ -137,3 +138,12 @@ def test_conv_parity_workload_subset():
     inp = make_conv_inputs(CONFIGS["conv"], [0, 1, 2, 3])
     f, r = _check(inp.X, inp.Wc, inp.W_out, inp.labels, 0.2, dense=True)
     assert r["mask"].mean() > 1e-3
+
+
+@pytest.mark.parametrize("T,B,H,W,C,Fo", [(1, 1, 2, 2, 1, 1), (2, 1, 2, 2, 1, 64), (5, 2, 2, 4, 3, 8), (3, 1, 4, 2, 7, 64)])
+def test_conv_degenerate_shapes(T, B, H, W, C, Fo):
+    """One step, one sample, a single 2x2 window, one filter; the wavefront-per-pixel forward with
+    a one-pixel-wide map; the most input channels the one-ballot forward takes (9 C <= 64)."""
+    print(f"\n[case] conv degenerate T={T} B={B} H={H} W={W} C={C} F={Fo}", flush=True)
+    X, Wc, Wo, y = _small(T=T, B=B, H=H, W=W, C=C, Fo=Fo, Cls=2, rate=0.5, sigma=1.5, seed=T + Fo)
+    _check(X, Wc, Wo, y, 0.4, dense=True, nonzero=T > 2)
