@@ -135,8 +135,11 @@ snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, 
  *   a truncated result). The CSRs are expected as the compaction writes them: row_ptr
  *   non-decreasing, columns strictly ascending inside a row. Entries with a column outside
  *   [0, N) are skipped; for other malformed input the results are unspecified, but every memory
- *   access stays inside the arrays and workspace given (indices are clamped). The workspace size depends on out_cap (a slab-major copy of the
- *   active entries is built in it).
+ *   access stays inside the arrays and workspace given (indices are clamped).
+ *   Workspace: for N_out > 32 its size depends on out_cap (a slab-major copy of the active
+ *   entries is built in it); for N_out <= 32 (narrow layers: G written densely, padded to 8, 16
+ *   or 32 columns) it holds that G and delta (T*B*ld floats each), a bitset of the rows with an
+ *   entry and per-chunk partial dW, and does not depend on out_cap.
  *   aux_stream (may be NULL): a second hipStream_t. When given, the spike-gradient part runs on
  *   it beside the dW part on `stream`; the call makes aux_stream wait for the work already on
  *   `stream`, and `stream` wait for the aux work, so work enqueued on `stream` afterwards sees

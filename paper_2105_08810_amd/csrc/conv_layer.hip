@@ -167,6 +167,66 @@ __global__ void route_bits4_kernel(const uint64_t* __restrict__ cbits, const uin
   }
 }
 
+// As route_bits_kernel with sixteen neighbouring pooled neurons per lane (F % 16 == 0, arg
+// 16-byte aligned): the 16 neurons share one pixel, so each window position's candidates are one
+// 16-bit field of one conv word; the lane loads its 16 pooling choices and the four words at once
+// (no load waits on another), selects per neuron, and four lanes OR their fields into one word.
+__device__ __forceinline__ uint32_t low_bits_of_bytes(uint32_t x) {  // bit 0 of byte i -> bit i
+  return (((x & 0x01010101u) * 0x01020408u) >> 24) & 0xFu;
+}
+
+__global__ void route_bits16_kernel(const uint64_t* __restrict__ cbits, const uint8_t* __restrict__ arg, int T, int B,
+                                    int H, int W, int F, uint64_t* __restrict__ pbits) {
+  const int hw = W / 2;
+  const int64_t Np = (int64_t)(H / 2) * hw * F;
+  const int64_t N = (int64_t)H * W * F;
+  const int64_t BNp = B * Np;
+  const int64_t W64p = (BNp + kWave - 1) / kWave;
+  const int64_t W64c = (B * N + kWave - 1) / kWave;
+  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int l = lane_id();
+  if ((u - l) * 16 >= BNp) return;  // whole wavefront past the last neuron
+  const int64_t kp = 16 * u;
+  const bool valid = kp < BNp;
+  int64_t cw[4] = {0, 0, 0, 0};  // conv word of each window position, and the field's shift
+  int sh[4] = {0, 0, 0, 0};
+  if (valid) {
+    const int64_t b = kp / Np;
+    const int64_t j = kp - b * Np;
+    const int64_t f = j % F;
+    const int64_t pp = j / F;
+    const int64_t px = pp % hw;
+    const int64_t py = pp / hw;
+    const int64_t base = b * N + ((2 * py) * W + 2 * px) * F + f;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const int64_t kc = base + ((a >> 1) * W + (a & 1)) * F;
+      cw[a] = kc >> 6;
+      sh[a] = (int)(kc & 63);
+    }
+  }
+  const int64_t word = kp >> 6;
+  for (int t = blockIdx.y; t < T; t += gridDim.y) {
+    uint32_t r = 0;
+    if (valid) {
+      const uint4 c = *reinterpret_cast<const uint4*>(arg + (int64_t)t * BNp + kp);
+      const uint64_t* wt = cbits + (int64_t)t * W64c;
+      uint32_t g[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) g[a] = (uint32_t)(wt[cw[a]] >> sh[a]);
+      const uint32_t m0 = low_bits_of_bytes(c.x) | low_bits_of_bytes(c.y) << 4 | low_bits_of_bytes(c.z) << 8 |
+                          low_bits_of_bytes(c.w) << 12;
+      const uint32_t m1 = low_bits_of_bytes(c.x >> 1) | low_bits_of_bytes(c.y >> 1) << 4 |
+                          low_bits_of_bytes(c.z >> 1) << 8 | low_bits_of_bytes(c.w >> 1) << 12;
+      r = ((g[0] & ~m0 & ~m1) | (g[1] & m0 & ~m1) | (g[2] & ~m0 & m1) | (g[3] & m0 & m1)) & 0xFFFFu;
+    }
+    uint64_t v = (uint64_t)r << (16 * (l & 3));
+    v |= __shfl_xor(v, 1);
+    v |= __shfl_xor(v, 2);
+    if ((l & 3) == 0 && word < W64p) pbits[(int64_t)t * W64p + word] = v;
+  }
+}
+
 __global__ void fill_zero_f(float* __restrict__ p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0.0f;
@@ -432,7 +492,13 @@ extern "C" snn_status snn_pool_route_bits(const uint64_t* conv_bits, const uint8
   const int64_t Np = (int64_t)(H / 2) * (W / 2) * F;
   if ((int64_t)B * Np + kWave >= ((int64_t)1 << 31)) return SNN_ERR_INVALID_ARG;
   const int64_t lanes = ((B * Np + kWave - 1) / kWave) * kWave;
-  if (F % 4 == 0 && ((uintptr_t)arg & 3u) == 0) {
+  if (F % 16 == 0 && ((uintptr_t)arg & 15u) == 0) {
+    const int64_t threads = ((B * Np / 16 + kWave - 1) / kWave) * kWave;
+    const unsigned bx = (unsigned)((threads + 255) / 256);
+    const unsigned by = (unsigned)std::max(1, std::min(T, (int)(65536 / bx) + 1));
+    hipLaunchKernelGGL(route_bits16_kernel, dim3(bx, by), dim3(256), 0, static_cast<hipStream_t>(stream), conv_bits,
+                       arg, T, B, H, W, F, pool_bits);
+  } else if (F % 4 == 0 && ((uintptr_t)arg & 3u) == 0) {
     const int64_t threads = ((B * Np / 4 + kWave - 1) / kWave) * kWave;
     const unsigned bx = (unsigned)((threads + 255) / 256);
     const unsigned by = (unsigned)std::max(1, std::min(T, (int)(65536 / bx) + 1));

@@ -312,6 +312,264 @@ __global__ void reduce_chunks(const float* __restrict__ part, int n_chunks, size
   }
 }
 
+// ------------------------------------------------------------------ narrow layers
+//
+// With few outputs (N_out <= kNarrowOut, e.g. a readout of a few classes) a wavefront per row
+// or per (chunk, sample) wastes most lanes. Narrow layers work from G written densely instead,
+// rows padded to ld = 8, 16 or 32 columns (zeros past N_out), so that a row is one uniform
+// load:
+//   spike gradient: delta for every (t, b, j) by one thread per (b, j) walking t down, then one
+//     lane per input-active entry forms W[i, :] . delta[t, b, :] (ascending j);
+//   dW: a wavefront owns 64 inputs, 8 or 16 columns and a chunk of rows, visits the rows that
+//     have an entry (a bitset of them is built once) eight at a time and keeps sums per (input,
+//     column) (float32 over 64 rows, then float64); one float partial per chunk, summed in chunk
+//     order.
+// Deterministic.
+constexpr int kNarrowOut = 32;
+static_assert(kNarrowOut <= kWave, "one lane per output column in the G scatter");
+constexpr int kNarrowBatch = 8;  // 8 rows x 8 (or more) columns fill at least one load of 64 lanes
+
+int narrow_ld(int N_out) { return N_out <= 8 ? 8 : (N_out <= 16 ? 16 : 32); }
+
+// One wave per row writes the row's whole padded G: lane j < ld owns column j and picks its
+// value out of the row's entries, which the wave reads 64 at a time.
+__global__ void narrow_scatter_g(int TB, int N_out, int ld, const int32_t* __restrict__ rp,
+                                 const int32_t* __restrict__ col, const float* __restrict__ g,
+                                 const float* __restrict__ eps, int64_t cap, float* __restrict__ Gd) {
+  const int r = __builtin_amdgcn_readfirstlane((int)(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave));
+  if (r >= TB) return;
+  const int l = lane_id();
+  const int64_t e0 = clamp_entry(rp[r], cap);
+  const int64_t e1 = clamp_entry(rp[r + 1], cap);
+  float x = 0.0f;
+  for (int64_t base = e0; base < e1; base += kWave) {
+    const int64_t e = base + l;
+    int c = -1;
+    float v = 0.0f;
+    if (e < e1) {
+      c = col[e];
+      v = g ? eps[e] * g[e] : eps[e];
+    }
+    const int n = (int)std::min<int64_t>(e1 - base, kWave);
+    for (int k = 0; k < n; ++k) {
+      const int ck = __shfl(c, k);
+      const float vk = __shfl(v, k);
+      if (ck == l && l < N_out) x = vk;
+    }
+  }
+  if (l < ld) Gd[(int64_t)r * ld + l] = x;
+}
+
+// D[T-1] = 0, D[t] = alpha D[t+1] + G[t+1] for each (b, column); BL = B * ld. The G values of
+// 32 steps are loaded at once (the recurrence waits only on its own multiply-add).
+constexpr int kDeltaSteps = 32;
+
+__global__ void narrow_delta(int T, int64_t BL, float alpha, const float* __restrict__ Gd, float* __restrict__ D) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= BL) return;
+  float d = 0.0f;
+  D[(int64_t)(T - 1) * BL + k] = 0.0f;
+  for (int t1 = T - 1; t1 > 0; t1 -= kDeltaSteps) {  // steps t = t1 - 1 down to t1 - 32 (>= 0)
+    float g[kDeltaSteps];
+#pragma unroll
+    for (int u = 0; u < kDeltaSteps; ++u) g[u] = t1 - u >= 1 ? Gd[(int64_t)(t1 - u) * BL + k] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < kDeltaSteps; ++u) {
+      if (t1 - u >= 1) {
+        d = alpha * d + g[u];
+        D[(int64_t)(t1 - u - 1) * BL + k] = d;
+      }
+    }
+  }
+}
+
+// eps_in at each input-active entry of row r = t B + b: W[i, :] . D[r, :]; the padded columns of
+// D are zero, so the weight index is clamped to the row instead of tested.
+template <int NJ>
+__global__ void narrow_gin(int TB, int N_in, int N_out, const float* __restrict__ W, const float* __restrict__ D,
+                           const int32_t* __restrict__ rp, const int32_t* __restrict__ col, int64_t cap,
+                           float* __restrict__ eps_in) {
+  const int r = __builtin_amdgcn_readfirstlane((int)(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave));
+  if (r >= TB) return;
+  const int64_t e0 = clamp_entry(rp[r], cap);
+  const int64_t e1 = clamp_entry(rp[r + 1], cap);
+  if (e0 >= e1) return;
+  const float* d = D + (int64_t)r * NJ;
+  float dv[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) dv[j] = d[j];
+  for (int64_t e = e0 + lane_id(); e < e1; e += kWave) {
+    const int i = col[e];
+    const int ic = min(max(i, 0), N_in - 1);
+    const float* w = W + (int64_t)ic * N_out;
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) s += w[min(j, N_out - 1)] * dv[j];
+    eps_in[e] = (unsigned)i < (unsigned)N_in ? s : 0.0f;
+  }
+}
+
+// Bit k of word w: row 64 w + k has an entry.
+__global__ void narrow_busy_rows(int TB, const int32_t* __restrict__ rp, int64_t cap, uint64_t* __restrict__ busy) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  const bool on = r < TB && clamp_entry(rp[r + 1], cap) > clamp_entry(rp[r], cap);
+  const uint64_t m = __ballot(on);
+  if (lane_id() == 0 && r < TB) busy[r / kWave] = m;
+}
+
+struct NarrowDwPlan {
+  int n_iw, n_chunks, rows_per_chunk;  // rows_per_chunk: a multiple of 8
+};
+
+NarrowDwPlan plan_narrow_dw(int T, int B, int N_in) {
+  NarrowDwPlan p{};
+  const int TB = T * B;
+  p.n_iw = (N_in + kWave - 1) / kWave;
+  constexpr int kMaxRows = 63 * kWave;  // a chunk (starting at a multiple of 8) spans <= 64 bitset words
+  const int units = (TB + kNarrowBatch - 1) / kNarrowBatch;
+  int nc = (32 * kAssumedCUs + p.n_iw - 1) / p.n_iw;  // about 32 wavefronts per CU
+  nc = std::min(nc, std::min(units, 1024));
+  nc = std::max(nc, (TB + kMaxRows - 1) / kMaxRows);
+  p.rows_per_chunk = std::min(kMaxRows, ((units + nc - 1) / nc) * kNarrowBatch);
+  p.n_chunks = (TB + p.rows_per_chunk - 1) / p.rows_per_chunk;
+  return p;
+}
+
+template <int NJ>
+__global__ void narrow_dw(const float* __restrict__ trace, int TB, int N_in, int N_out,
+                          const uint64_t* __restrict__ busy, const float* __restrict__ Gd, int ld, int rows_per_chunk,
+                          int n_iw, float* __restrict__ part) {
+  const int j0 = blockIdx.y * NJ;  // this block's columns: j0 .. j0 + NJ - 1 of the padded G
+  const int wv = __builtin_amdgcn_readfirstlane((int)(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave));
+  const int c = wv / n_iw;
+  const int iw = wv - c * n_iw;
+  const int r_lo = c * rows_per_chunk;
+  if (r_lo >= TB) return;
+  const int r_hi = min(TB, r_lo + rows_per_chunk);
+  const int l = lane_id();
+  const int i = iw * kWave + l;
+  const int ic = min(i, N_in - 1);  // lanes past N_in read a valid column and write nothing
+  // float32 sums over up to 64 rows (eight batches), added into float64 sums: the rounding error
+  // stays at the level of a 64-term float32 sum, at float32 arithmetic's speed
+  double acc[NJ];
+  float acc32[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    acc[j] = 0.0;
+    acc32[j] = 0.0f;
+  }
+  int pending = 0;
+  auto flush = [&]() {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      acc[j] += (double)acc32[j];
+      acc32[j] = 0.0f;
+    }
+    pending = 0;
+  };
+  const int w_lo = r_lo / kWave;
+  const int nw = (r_hi + kWave - 1) / kWave - w_lo;  // at most 64 bitset words (the plan's chunks)
+  uint64_t mine = l < nw ? busy[w_lo + l] : 0ull;
+  if (l == 0) mine &= ~0ull << (r_lo & (kWave - 1));  // rows of the chunk only
+  if (l == nw - 1 && (r_hi & (kWave - 1))) mine &= (1ull << (r_hi & (kWave - 1))) - 1;
+  auto word = [&](int q) {  // uniform: the rows' G loads become scalar-indexed
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(mine >> 32), q) << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mine, q);
+  };
+  int q = 0;
+  uint64_t m = word(0);
+  // the next (up to) eight rows with an entry; rows past the count are r_lo (loaded, weight 0)
+  auto next_rows = [&](int* rows) {
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kNarrowBatch; ++k) {
+      while (m == 0 && q + 1 < nw) m = word(++q);
+      rows[k] = m ? (w_lo + q) * kWave + (int)__builtin_ctzll(m) : r_lo;
+      cnt += m ? 1 : 0;
+      m &= m - 1;
+    }
+    return cnt;
+  };
+  // A batch's G rows (8 x NJ values) spread over the lanes, NJ / 8 per lane, and its trace values;
+  // a G value is broadcast by a lane read when it is used.
+  constexpr int kSlots = NJ * kNarrowBatch / kWave;
+  auto load = [&](const int* rows, float* tv, float* gv) {
+    int rowv = rows[0];
+#pragma unroll
+    for (int k = 1; k < kNarrowBatch; ++k) rowv = l == k ? rows[k] : rowv;
+#pragma unroll
+    for (int z = 0; z < kSlots; ++z) {
+      const int f = z * kWave + l;
+      gv[z] = Gd[(int64_t)__shfl(rowv, f / NJ) * ld + j0 + (f % NJ)];
+    }
+#pragma unroll
+    for (int k = 0; k < kNarrowBatch; ++k) tv[k] = trace[(int64_t)rows[k] * N_in + ic];
+  };
+  auto accumulate = [&](const float* tv, const float* gv, int cnt) {
+#pragma unroll
+    for (int k = 0; k < kNarrowBatch; ++k) {
+      const float t = k < cnt ? tv[k] : 0.0f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int f = k * NJ + j;
+        const float g = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(gv[f / kWave]), f % kWave));
+        acc32[j] = fmaf(t, g, acc32[j]);
+      }
+    }
+    if (++pending == kNarrowBatch) flush();
+  };
+  // two batches in flight: the next one's loads are issued before this one's sums (ping-pong
+  // between two register sets, so no loaded value is copied)
+  int ra[kNarrowBatch], rn[kNarrowBatch];
+  float ta[kNarrowBatch], tn[kNarrowBatch], ga[kSlots], gn[kSlots];
+  int ca = next_rows(ra);
+  if (ca > 0) {
+    load(ra, ta, ga);
+    while (true) {
+      const int cn = next_rows(rn);
+      load(rn, tn, gn);
+      accumulate(ta, ga, ca);
+      if (cn == 0) break;
+      ca = next_rows(ra);
+      load(ra, ta, ga);
+      accumulate(tn, gn, cn);
+      if (ca == 0) break;
+    }
+  }
+  flush();
+  if (i < N_in) {
+    float* dst = part + ((int64_t)c * N_in + i) * N_out;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j0 + j < N_out) dst[j0 + j] = (float)acc[j];
+  }
+}
+
+// dW = sum of the chunk partials: a block of 16 wavefronts per 64 outputs, wavefront w summing
+// chunks w, w + 16, ... in order, then the 16 sums in order (float64 throughout).
+constexpr int kReduceWaves = 16;
+
+__global__ __launch_bounds__(kReduceWaves * kWave) void narrow_reduce(const float* __restrict__ part, int n_chunks,
+                                                                      int64_t n, float* __restrict__ out) {
+  __shared__ double red[kReduceWaves][kWave];
+  const int l = lane_id();
+  const int w = threadIdx.x / kWave;
+  const int64_t k = (int64_t)blockIdx.x * kWave + l;
+  double s = 0.0;
+  if (k < n) {
+#pragma unroll 4
+    for (int c = w; c < n_chunks; c += kReduceWaves) s += (double)part[(int64_t)c * n + k];
+  }
+  red[w][l] = s;
+  __syncthreads();
+  if (w == 0 && k < n) {
+    double t = 0.0;
+#pragma unroll
+    for (int v = 0; v < kReduceWaves; ++v) t += red[v][l];
+    out[k] = (float)t;
+  }
+}
+
 // ------------------------------------------------------------------ grad_in
 
 // L[c][b][:] = sum_{t in chunk c} alpha^(t - start_c) G[t, b, :]   (sparse accumulation in LDS)
@@ -539,6 +797,14 @@ namespace snn {
 namespace {
 
 size_t dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
+  if (N_out <= kNarrowOut) {  // padded dense G, the busy-row bitset and the chunk partials
+    const NarrowDwPlan q = plan_narrow_dw(T, B, N_in);
+    Carve c(nullptr);
+    c.take<float>((size_t)T * B * narrow_ld(N_out));
+    c.take<uint64_t>(((size_t)T * B + kWave - 1) / kWave);
+    if (q.n_chunks > 1) c.take<float>((size_t)q.n_chunks * N_in * N_out);
+    return c.off;
+  }
   const DwPlan p = plan_dw(T, B, N_in, N_out);
   const int nsp = p.n_slabs * T * B;
   Carve c(nullptr);
@@ -551,8 +817,13 @@ size_t dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
 }
 
 size_t gin_workspace(int T, int B, int N_out) {
-  const WalkPlan wp = plan_walk(T);
   Carve c(nullptr);
+  if (N_out <= kNarrowOut) {  // padded dense G and delta
+    c.take<float>((size_t)T * B * narrow_ld(N_out));
+    c.take<float>((size_t)T * B * narrow_ld(N_out));
+    return c.off;
+  }
+  const WalkPlan wp = plan_walk(T);
   c.take<float>((size_t)wp.C * B * N_out);
   return c.off;
 }
@@ -569,11 +840,47 @@ void fill_zero_async(float* p, size_t n, hipStream_t s) {
 
 // dW of one layer: group-major records of the active entries, the slab accumulation, the
 // reduction over row chunks. Arguments already validated.
+// Padded dense G of a narrow layer (N_out <= kNarrowOut), zeros included: [T*B][narrow_ld].
+void enqueue_narrow_g(int TB, int N_out, const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
+                      const float* eps_out, int64_t out_cap, float* Gd, hipStream_t s) {
+  const unsigned row_blocks = (unsigned)(((int64_t)TB * kWave + 255) / 256);
+  hipLaunchKernelGGL(narrow_scatter_g, dim3(row_blocks), dim3(256), 0, s, TB, N_out, narrow_ld(N_out), out_row_ptr,
+                     out_col_idx, out_g, eps_out, out_cap, Gd);
+}
+
+// dW of one layer. For a narrow layer the dense G goes to the front of the workspace; g_ready
+// says it is there already (written by enqueue_narrow_g on this stream).
 void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const int32_t* out_row_ptr,
                 const int32_t* out_col_idx, const float* out_g, const float* eps_out, int64_t out_cap, float* dW,
-                void* workspace, hipStream_t s) {
+                void* workspace, hipStream_t s, bool g_ready = false) {
   if (out_cap == 0) {  // no active output entry: dW = 0 and no entry array is read
     fill_zero_async(dW, (size_t)N_in * N_out, s);
+    return;
+  }
+  if (N_out <= kNarrowOut) {
+    const int TB = T * B;
+    const NarrowDwPlan q = plan_narrow_dw(T, B, N_in);
+    Carve ws(workspace);
+    float* Gd = ws.take<float>((size_t)TB * narrow_ld(N_out));
+    uint64_t* busy = ws.take<uint64_t>(((size_t)TB + kWave - 1) / kWave);
+    float* part = q.n_chunks > 1 ? ws.take<float>((size_t)q.n_chunks * N_in * N_out) : dW;
+    if (!g_ready) enqueue_narrow_g(TB, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, Gd, s);
+    hipLaunchKernelGGL(narrow_busy_rows, dim3((unsigned)((TB + 255) / 256)), dim3(256), 0, s, TB, out_row_ptr, out_cap,
+                       busy);
+    // columns in blocks of 8 (N_out <= 8) or 16 (grid y: one or two blocks)
+    const int ld = narrow_ld(N_out);
+    const unsigned blocks = (unsigned)(((int64_t)q.n_chunks * q.n_iw * kWave + 255) / 256);
+    if (ld == 8)
+      hipLaunchKernelGGL(narrow_dw<8>, dim3(blocks), dim3(256), 0, s, trace_in, TB, N_in, N_out, busy, Gd, ld,
+                         q.rows_per_chunk, q.n_iw, part);
+    else
+      hipLaunchKernelGGL(narrow_dw<16>, dim3(blocks, (unsigned)(ld / 16)), dim3(256), 0, s, trace_in, TB, N_in, N_out,
+                         busy, Gd, ld, q.rows_per_chunk, q.n_iw, part);
+    if (q.n_chunks > 1) {
+      const int64_t n = (int64_t)N_in * N_out;
+      hipLaunchKernelGGL(narrow_reduce, dim3((unsigned)((n + kWave - 1) / kWave)), dim3(kReduceWaves * kWave), 0, s,
+                         part, q.n_chunks, n, dW);
+    }
     return;
   }
   const int TB = T * B;
@@ -616,10 +923,33 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
 void enqueue_grad_in(const float* W, int T, int B, int N_in, int N_out, float alpha, const int32_t* out_row_ptr,
                      const int32_t* out_col_idx, const float* out_g, const float* eps_out, int64_t out_cap,
                      const int32_t* in_row_ptr, const int32_t* in_col_idx, int64_t in_cap, float* eps_in,
-                     bool share_cu, void* workspace, hipStream_t s) {
+                     bool share_cu, void* workspace, hipStream_t s, const float* g_dense = nullptr) {
   if (in_cap == 0) return;
   if (out_cap == 0) {  // no active output entry: delta = 0 everywhere
     fill_zero_async(eps_in, (size_t)in_cap, s);
+    return;
+  }
+  if (N_out <= kNarrowOut) {
+    const int ld = narrow_ld(N_out);
+    Carve ws(workspace);
+    const size_t n = (size_t)T * B * ld;
+    float* Gd = ws.take<float>(n);
+    float* D = ws.take<float>(n);
+    const int TB = T * B;
+    if (g_dense)
+      Gd = const_cast<float*>(g_dense);
+    else
+      enqueue_narrow_g(TB, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, Gd, s);
+    const int64_t BL = (int64_t)B * ld;
+    hipLaunchKernelGGL(narrow_delta, dim3((unsigned)((BL + 255) / 256)), dim3(256), 0, s, T, BL, alpha, Gd, D);
+    const unsigned row_blocks = (unsigned)(((int64_t)TB * kWave + 255) / 256);
+#define SNN_NGIN(NJ_)                                                                                        \
+  hipLaunchKernelGGL(narrow_gin<NJ_>, dim3(row_blocks), dim3(256), 0, s, TB, N_in, N_out, W, D, in_row_ptr, \
+                     in_col_idx, in_cap, eps_in)
+    if (ld == 8) SNN_NGIN(8);
+    else if (ld == 16) SNN_NGIN(16);
+    else SNN_NGIN(32);
+#undef SNN_NGIN
     return;
   }
   const WalkPlan wp = plan_walk(T);
@@ -720,6 +1050,11 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
   char* dw_ws = static_cast<char*>(workspace);
   char* gin_ws = dw_ws + align256(dw_workspace(T, B, N_in, N_out, out_cap));
   const bool do_gin = grad_in && in_cap > 0;
+  // A narrow layer's dense G is written once, at the front of the dW workspace, before the fork.
+  const bool narrow_g = N_out <= kNarrowOut && out_cap > 0;
+  if (narrow_g)
+    enqueue_narrow_g(T * B, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, reinterpret_cast<float*>(dw_ws),
+                     s);
   // The spike gradient (L1/L2-gather bound) and dW (LDS-atomic bound) lean on different parts of
   // a CU; with an auxiliary stream they run side by side. aux waits for what is already on s,
   // and s waits for aux before anything enqueued after this call.
@@ -736,9 +1071,10 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
     // CU (per product, a dW entry costs about 1.5 times a walk entry)
     const bool dw_longer = 3.0 * (double)out_cap * N_in >= 2.0 * (double)in_cap * N_out;
     enqueue_grad_in(W, T, B, N_in, N_out, alpha, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, in_row_ptr,
-                    in_col_idx, in_cap, eps_in, sa != s && dw_longer, gin_ws, sa);
+                    in_col_idx, in_cap, eps_in, sa != s && dw_longer, gin_ws, sa,
+                    narrow_g ? reinterpret_cast<const float*>(dw_ws) : nullptr);
   }
-  enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, dw_ws, s);
+  enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, dw_ws, s, narrow_g);
   if (sa != s) {
     if (hipEventRecord(ev_out, sa) != hipSuccess || hipStreamWaitEvent(s, ev_out, 0) != hipSuccess)
       (void)hipStreamSynchronize(sa);  // never leave aux work unordered with later work on s

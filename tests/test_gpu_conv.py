@@ -140,10 +140,12 @@ def test_conv_parity_workload_subset():
     assert r["mask"].mean() > 1e-3
 
 
-@pytest.mark.parametrize("T,B,H,W,C,Fo", [(1, 1, 2, 2, 1, 1), (2, 1, 2, 2, 1, 64), (5, 2, 2, 4, 3, 8), (3, 1, 4, 2, 7, 64)])
+@pytest.mark.parametrize("T,B,H,W,C,Fo", [(1, 1, 2, 2, 1, 1), (2, 1, 2, 2, 1, 64), (5, 2, 2, 4, 3, 8), (3, 1, 4, 2, 7, 64),
+                                           (4, 3, 4, 6, 2, 48), (3, 2, 2, 2, 1, 16)])
 def test_conv_degenerate_shapes(T, B, H, W, C, Fo):
     """One step, one sample, a single 2x2 window, one filter; the wavefront-per-pixel forward with
-    a one-pixel-wide map; the most input channels the one-ballot forward takes (9 C <= 64)."""
+    a one-pixel-wide map; the most input channels the one-ballot forward takes (9 C <= 64);
+    16-neuron pooled routing with fields inside a conv word (48 and 16 filters)."""
     print(f"\n[case] conv degenerate T={T} B={B} H={H} W={W} C={C} F={Fo}", flush=True)
     X, Wc, Wo, y = _small(T=T, B=B, H=H, W=W, C=C, Fo=Fo, Cls=2, rate=0.5, sigma=1.5, seed=T + Fo)
     _check(X, Wc, Wo, y, 0.4, dense=True, nonzero=T > 2)

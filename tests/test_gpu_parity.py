@@ -377,6 +377,17 @@ def test_parity_wide_layers(hidden, n_in, n_ro):
     check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
 
 
+@pytest.mark.parametrize("hidden,n_ro", [((24, 31), 3), ((31,), 8), ((24,), 9), ((40, 17), 16), ((32,), 32),
+                                          ((29,), 33)])
+def test_parity_narrow_outputs(hidden, n_ro):
+    """Layers of at most 32 outputs (hidden LIF layers and readouts) take the spike gradient's
+    narrow path (dense G, per-output delta, one lane per input-active entry); 33 outputs and up
+    take the walk. Widths at and beside each register-block boundary (8, 16, 32)."""
+    inp = _wide(hidden, 37, n_ro, T=41, B=3)
+    print(f"\n[case] narrow 37->{hidden}->{n_ro}", flush=True)
+    check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
+
+
 @pytest.mark.parametrize("name,b_th", [("tiny", 0.2), ("tiny", math.inf), ("latency", 0.2), ("event", 0.05),
                                        ("audio", 0.2), ("ragged", 0.3), ("ragged_sum", 0.25), ("wide", 0.4),
                                        ("stress8", 0.02), ("stress8", 0.8)])
