@@ -16,8 +16,10 @@
 namespace snn {
 namespace {
 
-constexpr int kCdwThreads = 256;
+constexpr int kCdwThreads = 256;  // dense filter gradient
 constexpr int kCdwWaves = kCdwThreads / kWave;
+constexpr int kCsdThreads = 1024;  // sparse filter gradient: 16 wavefronts share a block's accumulator
+constexpr int kCsdWaves = kCsdThreads / kWave;
 constexpr int kCdwMaxBlocks = 1024;
 constexpr int kDenseBlocks = 8192;  // blocks of the dense filter gradient (each walks its positions)
 constexpr int kDenseMaxC = 4;  // input channels per register group of the dense filter gradient
@@ -302,29 +304,32 @@ __global__ void scatter_dense_kernel(const float* __restrict__ eps_p, const uint
 // block's float64 accumulator [9 * C][F] in LDS. Each block writes its sums; a fixed-order
 // reduction over blocks gives dWc.
 template <int CT>  // CT > 0: C == CT and the patch's loads are issued together; 0: any C
-__global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
+__global__ __launch_bounds__(kCsdThreads) void conv_dw_sparse_kernel(
     const float* __restrict__ trace, int TB, int H, int W, int C, int F, const int32_t* __restrict__ rp,
     const int32_t* __restrict__ col, const float* __restrict__ g, const float* __restrict__ eps, int64_t cap,
     int rows_per_block, double* __restrict__ part) {
   extern __shared__ double cacc[];  // [9 * C * F]
   const int nacc = 9 * C * F;
-  for (int i = threadIdx.x; i < nacc; i += kCdwThreads) cacc[i] = 0.0;
+  for (int i = threadIdx.x; i < nacc; i += kCsdThreads) cacc[i] = 0.0;
   __syncthreads();
   const int N = H * W * F;
   const int r_lo = blockIdx.x * rows_per_block;
   const int r_hi = min(TB, r_lo + rows_per_block);
   const int w = threadIdx.x / kWave;
-  for (int r = r_lo + w; r < r_hi; r += kCdwWaves) {
+  for (int r = r_lo + w; r < r_hi; r += kCsdWaves) {
     const int64_t e0 = std::min<int64_t>(std::max(rp[r], 0), cap);
     const int64_t e1 = std::min<int64_t>(std::max(rp[r + 1], 0), cap);
     const float* tr = trace + (int64_t)r * H * W * C;
     for (int64_t e = e0 + lane_id(); e < e1; e += kWave) {
+      // the entry's column and gradient loads go out together; a bad column or a zero gradient
+      // is masked, not branched on, so the patch loads below are not held back either
       const int n = col[e];
-      if ((unsigned)n >= (unsigned)N) continue;
-      const float G = g ? eps[e] * g[e] : eps[e];
-      if (G == 0.0f) continue;
-      const int f = n % F;
-      const int pix = n / F;
+      const float G0 = g ? eps[e] * g[e] : eps[e];
+      const bool ok = (unsigned)n < (unsigned)N && G0 != 0.0f;
+      const int nc = ok ? n : 0;
+      const double G = (double)G0;
+      const int f = nc % F;
+      const int pix = nc / F;
       const int y = pix / W;
       const int x = pix - y * W;
       if (CT > 0) {
@@ -333,15 +338,18 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
         for (int tap = 0; tap < 9; ++tap) {
           const int yy = y + tap / 3 - 1;
           const int xx = x + tap % 3 - 1;
-          const bool in = yy >= 0 && yy < H && xx >= 0 && xx < W;
+          const bool in = ok && yy >= 0 && yy < H && xx >= 0 && xx < W;
           const float* tp = tr + ((int64_t)(in ? yy : 0) * W + (in ? xx : 0)) * CT;
 #pragma unroll
-          for (int c = 0; c < CT; ++c) tv[tap * CT + c] = in ? tp[c] : 0.0f;
+          for (int c = 0; c < CT; ++c) {
+            const float v = tp[c];  // in bounds either way: pixel (0, 0) stands in outside the map
+            tv[tap * CT + c] = in ? v : 0.0f;
+          }
         }
 #pragma unroll
         for (int i = 0; i < 9 * (CT > 0 ? CT : 1); ++i)  // a zero trace adds nothing: skipped
-          if (tv[i] != 0.0f) atomicAdd(&cacc[i * F + f], (double)G * (double)tv[i]);
-      } else {
+          if (tv[i] != 0.0f) atomicAdd(&cacc[i * F + f], G * (double)tv[i]);
+      } else if (ok) {
         for (int ky = 0; ky < 3; ++ky) {
           const int yy = y + ky - 1;
           if (yy < 0 || yy >= H) continue;
@@ -349,14 +357,14 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_sparse_kernel(
             const int xx = x + kx - 1;
             if (xx < 0 || xx >= W) continue;
             const float* tp = tr + ((int64_t)yy * W + xx) * C;
-            for (int c = 0; c < C; ++c) atomicAdd(&cacc[((ky * 3 + kx) * C + c) * F + f], (double)G * (double)tp[c]);
+            for (int c = 0; c < C; ++c) atomicAdd(&cacc[((ky * 3 + kx) * C + c) * F + f], G * (double)tp[c]);
           }
         }
       }
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nacc; i += kCdwThreads) part[(int64_t)blockIdx.x * nacc + i] = cacc[i];
+  for (int i = threadIdx.x; i < nacc; i += kCsdThreads) part[(int64_t)blockIdx.x * nacc + i] = cacc[i];
 }
 
 // out[i] = sum over p of part[p][i]: one block per output, 256 threads take fixed strided
@@ -457,7 +465,11 @@ bool conv_dims_ok(int T, int B, int H, int W, int F) {
   return !too_big(T, B, H * W * F);
 }
 
-int cdw_blocks(int TB) { return std::max(1, std::min(kCdwMaxBlocks, TB)); }
+// blocks of the sparse filter gradient: enough to fill the chip, partial sums kept under 64 MB
+int cdw_blocks(int TB, int nacc) {
+  const int by_mem = (int)std::max<int64_t>(1, ((int64_t)64 << 20) / ((int64_t)nacc * (int64_t)sizeof(double)));
+  return std::max(1, std::min(std::min(kCdwMaxBlocks, by_mem), TB));
+}
 
 int64_t dense_blocks(int64_t n_pos) { return std::max<int64_t>(1, std::min<int64_t>(kDenseBlocks, (n_pos + 63) / 64)); }
 
@@ -555,7 +567,7 @@ extern "C" snn_status snn_pool_scatter_eps_dense(const float* eps_pool, const ui
 
 extern "C" size_t snn_conv_sparse_dw_workspace(int T, int B, int H, int W, int C, int F) {
   if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || C * F > 2048) return 0;
-  return align256((size_t)cdw_blocks(T * B) * 9 * C * F * sizeof(double));
+  return align256((size_t)cdw_blocks(T * B, 9 * C * F) * 9 * C * F * sizeof(double));
 }
 
 extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, int H, int W, int C, int F,
@@ -569,14 +581,14 @@ extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, in
   if (workspace_bytes < snn_conv_sparse_dw_workspace(T, B, H, W, C, F)) return SNN_ERR_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int TB = T * B;
-  const int nb = cdw_blocks(TB);
+  const int nb = cdw_blocks(TB, 9 * C * F);
   const int rpb = (TB + nb - 1) / nb;
   const int nacc = 9 * C * F;
   double* part = static_cast<double*>(workspace);
   const size_t lds = (size_t)nacc * sizeof(double);
   auto launch = [&](auto kernel) {
     (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCdwThreads), lds, s, trace_in, TB, H, W, C, F, conv_row_ptr,
+    hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCsdThreads), lds, s, trace_in, TB, H, W, C, F, conv_row_ptr,
                        conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part);
   };
   if (C == 1) launch(conv_dw_sparse_kernel<1>);
