@@ -167,13 +167,32 @@ def train_experiment(args):
     B, T, P = cfg.B, cfg.T, args.train_batches
     dev = torch.device("cuda:0")
     t0 = time.time()
-    Xs = [torch.from_numpy(make_spikes(cfg, range(k * B, (k + 1) * B))).to(dev) for k in range(P)]
+    shape = (T, B, *cfg.conv[:3]) if cfg.conv else (T, B, cfg.sizes[0])  # conv: [T, B, H, W, C]
+
+    def spikes(idx):
+        return torch.from_numpy(make_spikes(cfg, idx).reshape(shape)).to(dev)
+
+    Xs = [spikes(range(k * B, (k + 1) * B)) for k in range(P)]
     Ys = [torch.from_numpy(make_labels(cfg, range(k * B, (k + 1) * B))).to(dev) for k in range(P)]
     held = 10 ** 6  # held-out samples come from far above the training indices
-    Xt = [torch.from_numpy(make_spikes(cfg, range(held + k * B, held + (k + 1) * B))).to(dev) for k in range(2)]
+    Xt = [spikes(range(held + k * B, held + (k + 1) * B)) for k in range(2)]
     Yt = [torch.from_numpy(make_labels(cfg, range(held + k * B, held + (k + 1) * B))).to(dev) for k in range(2)]
     gen_s = time.time() - t0
-    inp0 = make_inputs(cfg, range(B))
+    if cfg.conv:
+        from synth.inputs import make_conv_inputs
+        cin = make_conv_inputs(cfg, range(B))
+
+        def new_net():
+            return pipeline.ConvNetwork(
+                X=torch.from_numpy(cin.X).to(dev), Wc=torch.from_numpy(cin.Wc).to(dev),
+                W_out=torch.from_numpy(cin.W_out).to(dev), alpha=float(cfg.alpha), alpha_out=float(cfg.alpha_out),
+                labels=torch.from_numpy(cin.labels).to(dev), loss_mode=0 if cfg.loss_mode == "max" else 1,
+                theta=float(cfg.theta), beta=float(cfg.beta)).allocate()
+    else:
+        inp0 = make_inputs(cfg, range(B))
+
+        def new_net():
+            return pipeline.from_inputs(inp0, "cuda:0").allocate()
     pen = pipeline.Penalty(nu_up=args.nu_up)
     aux = torch.cuda.Stream()
 
@@ -204,7 +223,7 @@ def train_experiment(args):
     runs = [(f"sparse_bth_{b:g}", True, b) for b in bths] + [("full_surrogate", False, math.inf)]
     nets = {}
     for name, sparse, b_th in runs:
-        net = pipeline.from_inputs(inp0, "cuda:0").allocate()
+        net = new_net()
         if name == runs[0][0]:
             result["grad_difference_init"] = diff(net, b_th)
         opt = pipeline.Adam(net.params(), lr=args.lr)
@@ -616,7 +635,8 @@ def main():
                     help="each library call of the step captured once as a HIP graph and replayed")
     ap.add_argument("--train", action="store_true",
                     help="training runs, sparse vs full surrogate (App. E); prints one JSON line")
-    ap.add_argument("--train-workload", default="latency_train")
+    ap.add_argument("--train-workload", default="latency_train",
+                    help="latency_train (784-200-10), deep (five LIF layers of 300) or conv (conv layer + pooling)")
     ap.add_argument("--train-steps", type=int, default=600)
     ap.add_argument("--train-batches", type=int, default=20, help="batches in the synthetic training set")
     ap.add_argument("--lr", type=float, default=2e-4)

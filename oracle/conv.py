@@ -102,10 +102,12 @@ def conv_weight_grad(G: np.ndarray, trace: np.ndarray) -> np.ndarray:
 
 
 def conv_network_backward(fwd: dict, Wc, W_out, alpha_out, labels, mode: str, theta, b_th, beta,
-                          absolute: bool = False):
+                          absolute: bool = False, reg=None):
     """Truncated-surrogate gradient of the conv network (float64): loss, dWc [3, 3, C, F],
     dW_out, eps_P (w.r.t. pooled spikes), eps (w.r.t. conv spikes), G, mask, g. With
-    absolute=True the magnitude envelope (as backward.network_backward)."""
+    absolute=True the magnitude envelope (as backward.network_backward). reg ([B, H, W, F],
+    d penalty / d spike count from regularize.activity_grad, App. E) joins the gradient w.r.t.
+    every conv spike S[t] before the surrogate gate, as the spike count sums S over t."""
     T, B, H, W, Fo = fwd["V"].shape
     ro = readout_grad(fwd["V_out"], labels, mode)
     G_out = ro["G_abs"] if absolute else ro["G"]
@@ -113,6 +115,9 @@ def conv_network_backward(fwd: dict, Wc, W_out, alpha_out, labels, mode: str, th
     dW_out, eps_P = layer_backward(G_out, Wo, fwd["trace_out"], alpha_out, grad_in=True)
     eps_P = eps_P.reshape(T, B, H // 2, W // 2, Fo)
     eps = route_to_conv(eps_P, fwd["arg"], H, W)
+    if reg is not None:
+        r = np.asarray(reg, np.float64).reshape(B, H, W, Fo)
+        eps = eps + (np.abs(r) if absolute else r)[None]
     mask = active_mask(fwd["V"], theta, b_th)
     g = surrogate(fwd["V"], theta, beta)
     G = eps * g * mask

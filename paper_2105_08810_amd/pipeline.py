@@ -294,9 +294,17 @@ class ConvNetwork:
                                        shape=(T, B, self.Np))
         return [conv, pool]
 
-    def sparse_backward(self, csrs, ro=None, ws=None):
+    def params(self) -> List[torch.Tensor]:
+        return [self.Wc, self.W_out]
+
+    def activity(self, reg: "Penalty", want_zeta=False):
+        """Activity penalties (App. E) of the conv layer's spikes: (coef [B, N], penalty [1], zeta)."""
+        return snn.activity_reg(self.S, reg.lam_low, reg.nu_low, reg.lam_up, reg.nu_up, want_zeta)
+
+    def sparse_backward(self, csrs, ro=None, ws=None, reg_coef=None):
         """Readout backward at the pooled entries, routed to the conv layer's active entries, and
-        the sparse filter gradient. Returns (dWc, dW_out, eps at the conv entries)."""
+        the sparse filter gradient. reg_coef ([B, N], from activity()) joins the conv spikes'
+        gradient before the filter gradient. Returns (dWc, dW_out, eps at the conv entries)."""
         if ro is None:
             ro = self.readout()
         conv, pool = csrs
@@ -305,6 +313,8 @@ class ConvNetwork:
         eps = torch.empty(conv.capacity, dtype=torch.float32, device=self.X.device)
         snn.snn_pool_scatter_eps(T, B, H, W, F, pool.row_ptr, pool.col_idx, pool.capacity, eps_pool, self.arg,
                                  conv.row_ptr, conv.col_idx, conv.capacity, eps)
+        if reg_coef is not None:
+            snn.activity_reg_grad(reg_coef, T, eps, conv)
         dWc = torch.empty_like(self.Wc)
         if ws is None:
             ws = snn.workspace(snn.snn_conv_sparse_dw_workspace(T, B, H, W, C, F), self.X.device)
@@ -312,9 +322,10 @@ class ConvNetwork:
                                dWc, ws)
         return dWc, dW_out, eps
 
-    def dense_backward(self, b_th, ro=None, ws=None):
+    def dense_backward(self, b_th, ro=None, ws=None, reg_coef=None):
         """The dense chain: dense readout backward, dense routing, dense filter gradient (b_th =
-        inf: full surrogate). Returns (dWc, dW_out, eps dense [T, B, N])."""
+        inf: full surrogate); reg_coef as in sparse_backward. Returns (dWc, dW_out, eps dense
+        [T, B, N])."""
         if ro is None or ro[3] is None:
             ro = self.readout(dense=True)
         T, B, H, W, C, F = self.dims
@@ -322,11 +333,44 @@ class ConvNetwork:
                                                   INF, self.beta, grad_in=True)
         eps = torch.empty((T, B, self.N), dtype=torch.float32, device=self.X.device)
         snn.snn_pool_scatter_eps_dense(eps_pool, self.arg, T, B, H, W, F, eps)
+        if reg_coef is not None:
+            snn.activity_reg_grad(reg_coef, T, eps)
         dWc = torch.empty_like(self.Wc)
         if ws is None:
             ws = snn.workspace(snn.snn_conv_dense_dw_workspace(T, B, H, W, C, F), self.X.device)
         snn.snn_conv_dense_dw(self.trace, self.V, eps, T, B, H, W, C, F, self.theta, b_th, self.beta, dWc, ws)
         return dWc, dW_out, eps
+
+    def train_step(self, opt: "Adam", b_th: float, reg: Optional["Penalty"] = None, sparse: bool = True,
+                   aux_stream=None, events=None):
+        """One training step of the conv network (App. E), as Network.train_step: forward,
+        cross-entropy plus the conv layer's activity penalties, the sparse (or dense) backward with
+        band b_th, Adam on Wc and W_out in place. aux_stream is accepted for a common interface
+        and not used. Returns a dict of device tensors: ce [1], penalty [1], grads [dWc, dW_out],
+        nnz ([conv layer's active-entry count] or None)."""
+        mark = (lambda k: events[k].record()) if events is not None else (lambda k: None)
+        mark(0)
+        self.forward(b_th if sparse and math.isfinite(b_th) else None)
+        mark(1)
+        act = self.activity(reg) if reg is not None else None
+        coef = act[0] if act else None
+        ro = self.readout(dense=not sparse)
+        mark(2)
+        if sparse:
+            csrs = self.compact(b_th)
+            mark(3)
+            dWc, dW_out, _ = self.sparse_backward(csrs, ro, reg_coef=coef)
+            nnz = [csrs[0].nnz_dev]
+        else:
+            mark(3)
+            dWc, dW_out, _ = self.dense_backward(b_th, ro, reg_coef=coef)
+            nnz = None
+        mark(4)
+        grads = [dWc, dW_out]
+        opt.step(grads)
+        mark(5)
+        pen = act[1] if act else torch.zeros(1, device=self.X.device)
+        return {"ce": ro[2], "penalty": pen, "grads": grads, "nnz": nnz}
 
 
 class Graphed:

@@ -149,3 +149,47 @@ def test_conv_degenerate_shapes(T, B, H, W, C, Fo):
     print(f"\n[case] conv degenerate T={T} B={B} H={H} W={W} C={C} F={Fo}", flush=True)
     X, Wc, Wo, y = _small(T=T, B=B, H=H, W=W, C=C, Fo=Fo, Cls=2, rate=0.5, sigma=1.5, seed=T + Fo)
     _check(X, Wc, Wo, y, 0.4, dense=True, nonzero=T > 2)
+
+
+@pytest.mark.parametrize("sparse,b_th", [(True, 0.3), (False, math.inf)])
+def test_conv_train_step(sparse, b_th):
+    """A training step of the conv network with the activity penalties of App. E on the conv
+    layer (bounds chosen so both hinges are active): the gradients (sparse chain with a band, or
+    the dense chain with the full surrogate) match the oracle's with the penalty coefficient
+    joining every conv spike's gradient, and the weights after the step equal the oracle's Adam
+    step applied to the GPU's gradients."""
+    from test_gpu_train import _adam_bound, _f32
+    print(f"\n[case] conv train step sparse={sparse} b_th={b_th}", flush=True)
+    X, Wc, Wo, y = _small(rate=0.1, sigma=1.0, seed=7)
+    T, B, H, W, C = X.shape
+    Fo = Wc.shape[3]
+    a = F32(math.exp(-0.1))
+    pen = (3.0, 2.0, 0.7, 0.4)
+    f = conv.conv_network_forward(X, Wc, Wo, a, a)
+    zeta = oracle.spike_counts(f["S"].reshape(T, B, -1))
+    assert (zeta < pen[1]).any() and (zeta.mean(axis=1) > pen[3]).any()
+    coef = oracle.activity_grad(zeta, *_f32(*pen)).reshape(B, H, W, Fo)
+    r = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, b_th, 100.0, reg=coef)
+    env = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, b_th, 100.0, absolute=True, reg=coef)
+    dev = torch.device("cuda")
+    net = pipeline.ConvNetwork(X=torch.from_numpy(X).to(dev), Wc=torch.from_numpy(Wc).to(dev),
+                               W_out=torch.from_numpy(Wo).to(dev), alpha=float(a), alpha_out=float(a),
+                               labels=torch.from_numpy(y).to(dev), loss_mode=0)
+    lr = 1e-3
+    opt = pipeline.Adam(net.params(), lr=lr)
+    before = [_np(p).copy() for p in net.params()]
+    out = net.train_step(opt, b_th, pipeline.Penalty(*pen), sparse=sparse)
+    torch.cuda.synchronize()
+    assert float(out["penalty"].item()) == pytest.approx(float(np.mean(oracle.activity_penalty(zeta, *pen))),
+                                                         rel=1e-5)
+    _env_ok(_np(out["grads"][0]), r["dWc"], env["dWc"], "dWc")
+    _env_ok(_np(out["grads"][1]), r["dW_out"], env["dW_out"], "dW_out")
+    plain = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, b_th, 100.0)
+    assert not np.allclose(plain["dWc"], r["dWc"], rtol=1e-3)  # the penalty changed the filter gradient
+    L = _f32(lr, 0.9, 0.999, 1e-8)
+    for j, p in enumerate(net.params()):
+        g = _np(out["grads"][j]).astype(np.float64)
+        z = np.zeros_like(g)
+        w_ref, m_ref, v_ref = oracle.adam_update(before[j], g, z, z, 1, *L)
+        _, _, bw = _adam_bound(before[j].astype(np.float64), g, z, z, 1, *L, m_ref, v_ref, w_ref)
+        assert (np.abs(_np(p) - w_ref) <= bw).all(), j

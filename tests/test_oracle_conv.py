@@ -76,7 +76,7 @@ def test_pool_matches_torch():
     assert (arg[P == 0] == 0).all()
 
 
-def _torch_conv_grads(X, Wc, Wo, y, b_th, beta=100.0, alpha=math.exp(-0.1), mode="max"):
+def _torch_conv_grads(X, Wc, Wo, y, b_th, beta=100.0, alpha=math.exp(-0.1), mode="max", pen=None):
     class Spike(torch.autograd.Function):
         @staticmethod
         def forward(ctx, v):
@@ -99,8 +99,10 @@ def _torch_conv_grads(X, Wc, Wo, y, b_th, beta=100.0, alpha=math.exp(-0.1), mode
     tr = torch.zeros(x.shape[1:], dtype=torch.float64)
     tro = torch.zeros(B, wo.shape[0], dtype=torch.float64)
     vol, vl, sl, tl, tol = [], [], [], [], []
+    sg = []
     for t in range(T):
         s = Spike.apply(v)
+        sg.append(s)
         p = torch.nn.functional.max_pool2d(s, 2).permute(0, 2, 3, 1).reshape(B, -1)  # channels last
         vol.append(vo)
         vl.append(v.detach())
@@ -123,6 +125,13 @@ def _torch_conv_grads(X, Wc, Wo, y, b_th, beta=100.0, alpha=math.exp(-0.1), mode
     else:
         logits = Vo.sum(0)
     loss = torch.nn.functional.cross_entropy(logits, torch.tensor(y, dtype=torch.long))
+    if pen is not None:  # App. E activity penalties on the spike counts, (1/B) sum over samples
+        lam_low, nu_low, lam_up, nu_up = pen
+        zeta = torch.stack(sg).sum(0).reshape(B, -1)
+        n = zeta.shape[1]
+        r = (lam_low / n) * torch.clamp(nu_low - zeta, min=0.0).pow(2).sum(1) \
+            + lam_up * torch.clamp(zeta.mean(1) - nu_up, min=0.0)
+        loss = loss + r.mean()
     loss.backward()
     return float(loss.detach()), wc.grad.permute(2, 3, 1, 0).numpy(), wo.grad.numpy(), fwd
 
@@ -178,3 +187,23 @@ def test_wrong_pool_routing_is_caught():
     a = F32(math.exp(-0.1))
     r = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, np.inf, 100.0)
     assert not np.allclose(r["dWc"], gWc, rtol=1e-3)
+
+
+def test_activity_penalty_gradient_matches_torch_autograd():
+    """With the activity penalties of App. E on the conv layer's spike counts, dWc (through the
+    spike-count coefficient joining every conv spike's gradient) equals torch autograd of
+    cross-entropy + (1/B) sum_b R(zeta_b); bounds chosen so both hinges are active."""
+    X, Wc, Wo, y = _case(T=14, B=3, H=6, W=6, C=2, Fo=5, rate=0.2, sigma=0.8, seed=11)
+    pen = (3.0, 2.0, 0.7, 0.4)
+    a = F32(math.exp(-0.1))
+    loss, gWc, gWo, f = _torch_conv_grads(X, Wc, Wo, y, 0.3, pen=pen)
+    zeta = oracle.spike_counts(f["S"].reshape(14, 3, -1))
+    assert (zeta < pen[1]).any() and (zeta.mean(axis=1) > pen[3]).any()
+    coef = oracle.activity_grad(zeta, *pen)
+    r = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, 0.3, 100.0, reg=coef.reshape(3, 6, 6, 5))
+    pen_total = float(np.mean(oracle.activity_penalty(zeta, *pen)))
+    assert r["loss"] + pen_total == pytest.approx(loss, rel=1e-9)
+    assert np.allclose(r["dWc"], gWc, rtol=1e-7, atol=1e-9 * np.abs(gWc).max())
+    assert np.allclose(r["dW_out"], gWo, rtol=1e-7, atol=1e-9 * np.abs(gWo).max())
+    plain = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, 0.3, 100.0)
+    assert not np.allclose(plain["dWc"], gWc, rtol=1e-3)  # the penalty term is not negligible
