@@ -23,6 +23,7 @@ constexpr int kCsdWaves = kCsdThreads / kWave;
 constexpr int kCdwMaxBlocks = 1024;
 constexpr int kDenseBlocks = 8192;  // blocks of the dense filter gradient (each walks its positions)
 constexpr int kDenseMaxC = 4;  // input channels per register group of the dense filter gradient
+constexpr int kDenseBatch = 4;  // positions (one channel) per wavefront whose loads are in flight together
 
 unsigned stream_blocks(int64_t items) {
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>((items + 255) / 256, 65536));
@@ -394,7 +395,7 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_dense_kernel(
     const float* __restrict__ trace, const float* __restrict__ V, const float* __restrict__ eps, int64_t n_pos,
     int H, int W, int C, int F, float theta, float b_th, float beta, int64_t pos_per_block, double* __restrict__ part) {
   __shared__ float red[kCdwWaves][9 * CMAX][kWave];
-  const int w = threadIdx.x / kWave;
+  const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   const int l = lane_id();
   const int nacc = 9 * C * F;
   const int64_t p_lo = (int64_t)blockIdx.x * pos_per_block;
@@ -408,37 +409,74 @@ __global__ __launch_bounds__(kCdwThreads) void conv_dw_dense_kernel(
 #pragma unroll
       for (int q = 0; q < 9 * CMAX; ++q) acc[q] = 0.0f;
       const int HW = H * W;
-      int64_t r = (p_lo + w) / HW;  // position p = r * HW + pix, advanced without division
+      const int64_t n_rows = n_pos / HW;
+      // positions p = r * HW + pix, U = kDenseBatch of them per wavefront at a time (stride
+      // kCdwWaves). Their V values and 3x3xCG patches (lane k of the wavefront loads patch value
+      // k, 9 CG U <= 64) go out together; eps is read only for lanes in the band; a patch value
+      // reaches every lane by a lane read.
+      constexpr int U = kDenseBatch / CMAX;
+      const int n_pv = 9 * CG;  // patch values per position
+      int64_t r = (p_lo + w) / HW;
       int pix = (int)(p_lo + w - r * HW);
-      for (int64_t p = p_lo + w; p < p_hi; p += kCdwWaves) {
-        const int y = pix / W;
-        const int x = pix - y * W;
-        const int64_t r_here = r;
-        pix += kCdwWaves;
-        while (pix >= HW) {
-          pix -= HW;
-          ++r;
+      for (int64_t p0 = p_lo + w; p0 < p_hi; p0 += U * kCdwWaves) {
+        int64_t ru[U];
+        int yu[U], xu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          ru[u] = r;
+          yu[u] = pix / W;
+          xu[u] = pix - yu[u] * W;
+          pix += kCdwWaves;
+          while (pix >= HW) {
+            pix -= HW;
+            ++r;
+          }
         }
-        float G = 0.0f;
-        if (fv) {
-          const float v = V[p * F + f];
-          const float d = fabsf(v - theta);
+        float vu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int64_t pu = min(p0 + (int64_t)u * kCdwWaves, p_hi - 1);  // in range; weight 0 past p_hi
+          vu[u] = fv ? V[pu * F + f] : 0.0f;
+        }
+        float pv = 0.0f;  // lane k < n_pv U: value k % n_pv of position k / n_pv's patch
+        {
+          const int u = l / n_pv;
+          const int k = l - u * n_pv;
+          const int tap = k / CG;
+          const int c = k - tap * CG;
+          int64_t rr = 0;
+          int yy = -1, xx = -1;
+#pragma unroll
+          for (int v = 0; v < U; ++v)
+            if (v == u) {
+              rr = ru[v];
+              yy = yu[v] + tap / 3 - 1;
+              xx = xu[v] + tap % 3 - 1;
+            }
+          const bool in = u < U && rr < n_rows && yy >= 0 && yy < H && xx >= 0 && xx < W;
+          if (in) pv = trace[(rr * HW + (int64_t)yy * W + xx) * C + c0 + c];
+        }
+        float Gu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const float d = fabsf(vu[u] - theta);
           const float q = beta * d + 1.0f;
-          G = d < b_th ? eps[p * F + f] / (q * q) : 0.0f;
+          const bool band = fv && p0 + (int64_t)u * kCdwWaves < p_hi && d < b_th;
+          const int64_t pu = min(p0 + (int64_t)u * kCdwWaves, p_hi - 1);
+          Gu[u] = band ? eps[pu * F + f] / (q * q) : 0.0f;
         }
-        if (__ballot(G != 0.0f) == 0ull) continue;
-        const float* tr = trace + r_here * (int64_t)HW * C + c0;
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky) {
-          const int yy = y + ky - 1;
+        for (int u = 0; u < U; ++u) {
+          if (__ballot(Gu[u] != 0.0f) == 0ull) continue;
 #pragma unroll
-          for (int kx = 0; kx < 3; ++kx) {
-            const int xx = x + kx - 1;
-            const bool in = yy >= 0 && yy < H && xx >= 0 && xx < W;
+          for (int tap = 0; tap < 9; ++tap)
 #pragma unroll
             for (int c = 0; c < CMAX; ++c)
-              if (c < CG && in) acc[(ky * 3 + kx) * CMAX + c] += G * tr[((int64_t)yy * W + xx) * C + c];
-          }
+              if (c < CG) {
+                const float t = __int_as_float(
+                    __builtin_amdgcn_readlane(__float_as_int(pv), u * n_pv + tap * CG + c));
+                acc[tap * CMAX + c] += Gu[u] * t;
+              }
         }
       }
 #pragma unroll
