@@ -407,8 +407,16 @@ class Runner:
         self.net.forward(None if self.args.unfused else b_th)
         csrs = self.net.compact(b_th)
         self.caps = [c.capacity for c in csrs]
-        self.ws_dw = [snn.workspace(snn.snn_sparse_dw_workspace(T, B, sizes[l], sizes[l + 1], self.caps[l]))
-                      for l in range(L)]
+        K = self.args.recompute
+        if K:  # trace recompute: dW from the input spikes and checkpoints of the trace every K steps
+            self.ws_dw = [snn.workspace(snn.snn_sparse_dw_spikes_workspace(T, B, sizes[l], sizes[l + 1],
+                                                                           self.caps[l], K)) for l in range(L)]
+            nck = snn.snn_trace_checkpoint_count(T, K)
+            self.ck = [self.torch.empty((nck, B, sizes[l]), dtype=self.torch.float32, device="cuda:0")
+                       for l in range(L)]
+        else:
+            self.ws_dw = [snn.workspace(snn.snn_sparse_dw_workspace(T, B, sizes[l], sizes[l + 1], self.caps[l]))
+                          for l in range(L)]
         self.dW = [self.torch.empty((sizes[l], sizes[l + 1]), dtype=self.torch.float32, device="cuda:0")
                    for l in range(L)]
         self.eps = [self.torch.empty(self.caps[l], dtype=self.torch.float32, device="cuda:0") for l in range(L)]
@@ -438,6 +446,13 @@ class Runner:
         E("fwd0").record(main)
         R("fwd", main, lambda: net.forward(None if self.args.unfused else self.b_th))
         E("fwd1").record(main)
+        K = self.args.recompute
+        if K:
+            def checkpoints():
+                for l in range(L):
+                    snn.trace_checkpoints(net.X if l == 0 else net.S[l - 1], net.alphas[l], K, ck=self.ck[l])
+            R("ck", main, checkpoints)
+            E("ck1").record(main)
         r = R("readout" + ("d" if with_dense else ""), main, lambda: net.readout(dense=with_dense))
         E("cmp0").record(main)
         cs = R("compact", main, lambda: net.compact(self.b_th, self.caps))
@@ -459,8 +474,13 @@ class Runner:
                     ws=self.ws_gi, eps_in=self.eps[l - 1]))
                 ev["gi1"][i].record(aux)
             ev["dw0"][i].record(main)
-            R(f"dw{l}", main, lambda l=l, eps=eps: snn.sparse_dw(net.trace[l], cs[l], eps, net.Ws[l].shape[1],
-                                                                ws=self.ws_dw[l], dW=self.dW[l]))
+            if K:
+                R(f"dw{l}", main, lambda l=l, eps=eps: snn.sparse_dw_spikes(
+                    net.X if l == 0 else net.S[l - 1], self.ck[l], K, net.alphas[l], cs[l], eps, net.Ws[l].shape[1],
+                    ws=self.ws_dw[l], dW=self.dW[l]))
+            else:
+                R(f"dw{l}", main, lambda l=l, eps=eps: snn.sparse_dw(net.trace[l], cs[l], eps, net.Ws[l].shape[1],
+                                                                    ws=self.ws_dw[l], dW=self.dW[l]))
             ev["dw1"][i].record(main)
             if l > 0:
                 if aux is not main:
@@ -504,7 +524,7 @@ class Runner:
 
     def events(self):
         mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
-        ev = {k: mk() for k in ("fwd0", "fwd1", "cmp0", "cmp1", "ro1", "dn0", "dn1")}
+        ev = {k: mk() for k in ("fwd0", "fwd1", "ck1", "cmp0", "cmp1", "ro1", "dn0", "dn1")}
         for k in ("lay0", "lay1", "gi0", "gi1", "dw0", "dw1"):
             ev[k] = [mk() for _ in range(self.L)]
         return ev
@@ -607,6 +627,16 @@ class Runner:
             "sparse_backward_hbm_frac": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "wall_s_timed": wall,
         }
+        K = self.args.recompute
+        if K:
+            nck = self.snn.snn_trace_checkpoint_count(T, K)
+            out["trace_recompute"] = {
+                "K": K, "checkpoint_ms": med(span("fwd1", "ck1")),
+                "stored_trace_bytes": sum(4 * T * B * sizes[l] for l in range(L)),
+                "checkpoint_bytes": sum(4 * nck * B * sizes[l] for l in range(L)),
+                "dw_kernel": "dw_slab_spikes_kernel (trace rebuilt in registers from the input spikes)"}
+            out["roofline"]["kernel"] = "snn_sparse_dw_spikes (slab records + dw_slab_spikes_kernel + chunk reduction)"
+            out["roofline"]["traffic"] = None
         if out["dense_backward_ms"] is not None:
             out["dense_mfma_tflops"] = dense_flops / (out["dense_backward_ms"] * 1e-3) / 1e12
             out["dense_mfma_frac"] = out["dense_mfma_tflops"] / MFMA_F32_TFLOPS
@@ -631,6 +661,8 @@ def main():
                     help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
+    ap.add_argument("--recompute", type=int, default=0, metavar="K",
+                    help="trace recompute: dW rebuilds the input trace from the spikes and checkpoints every K steps")
     ap.add_argument("--graph", action="store_true",
                     help="each library call of the step captured once as a HIP graph and replayed")
     ap.add_argument("--train", action="store_true",
@@ -658,6 +690,9 @@ def main():
     from synth import CONFIGS
     snn.lib()
     cfg = CONFIGS[args.workload]
+    if cfg.conv and args.recompute:
+        print("--recompute applies to the fully connected workloads", file=sys.stderr)
+        sys.exit(2)
     run = ConvRunner(cfg, args) if cfg.conv else Runner(cfg, args)
     points = cfg.sweep() if args.sweep else (cfg.b_th if args.b_th is None else args.b_th,)
     dense_ms = None

@@ -181,6 +181,33 @@ snn_status snn_sparse_grad_in(const float* W, int T, int B, int N_in, int N_out,
                               float* eps_in, int share_cu, void* workspace, size_t workspace_bytes,
                               void* stream);
 
+/*
+ * Trace recompute: dW without the stored input trace. The trace of Eq. (w_grad) obeys
+ * trace[0] = 0, trace[t+1] = alpha trace[t] + S_in[t] (Sec. 2; float32, product and sum each
+ * rounded, as the forward computes it), so it is determined by the input spikes and its values
+ * at every K-th step.
+ *
+ * snn_trace_checkpoints: ck [ceil(T/K), B, N_in] float32 (written): ck[q] = trace[q K], from
+ *   s_in [T,B,N_in] uint8 (read; nonzero = spike) with the forward's recurrence (bit-identical
+ *   to the trace snn_lif_forward writes). snn_trace_checkpoint_count(T, K) = ceil(T/K).
+ * snn_sparse_dw_spikes: the same dW as snn_sparse_dw (same CSR arguments), reading s_in and ck
+ *   (with the K and alpha they were made with) instead of trace_in: each block rebuilds the trace
+ *   values it needs in registers from the checkpoint at the start of its steps. The traces used
+ *   are bit-identical to the stored ones; dW can differ from snn_sparse_dw's in the last bit only
+ *   (float64 accumulation in another order). Memory: B N_in (ceil(T/K) floats + T bytes of
+ *   spikes the forward keeps anyway) instead of T B N_in floats. Any N_out <= 4096 (narrow
+ *   layers too, through the slab kernel). Errors: SNN_ERR_INVALID_ARG for NULL pointers, K < 1,
+ *   alpha outside (0, 1], bad sizes or a short workspace; SNN_ERR_UNSUPPORTED for N_out > 4096.
+ */
+int64_t snn_trace_checkpoint_count(int T, int K);
+snn_status snn_trace_checkpoints(const uint8_t* s_in, int T, int B, int N_in, float alpha, int K, float* ck,
+                                 void* stream);
+size_t snn_sparse_dw_spikes_workspace(int T, int B, int N_in, int N_out, int64_t out_cap, int K);
+snn_status snn_sparse_dw_spikes(const uint8_t* s_in, const float* ck, int K, float alpha, int T, int B, int N_in,
+                                int N_out, const int32_t* out_row_ptr, const int32_t* out_col_idx,
+                                const float* out_g, const float* eps_out, int64_t out_cap, float* dW,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
 
 /*
  * Dense surrogate BPTT of one layer on matrix cores: the baseline the sparse rule is

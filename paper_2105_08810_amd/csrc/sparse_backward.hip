@@ -300,6 +300,160 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   }
 }
 
+// dW with the input trace rebuilt from the input spikes (trace recompute). The trace at every
+// K-th step (checkpoints) and the spikes S_in replace the stored trace: the trace recurrence runs
+// forward in registers with the float32 operations of the forward, so every trace value equals
+// the stored one bit for bit. Block = (chunk: steps [t_lo, t_lo + tlen) x 128 samples, input
+// tile, slab). Wavefront w owns 8 samples and walks the chunk's steps; at step t its batch is the
+// rows t B + b of its samples, with their trace values in the lane's registers (8 samples x 2
+// inputs); after the batch the registers advance one step with S[t]. Records, LDS accumulators,
+// the per-entry work and the software pipeline (the next step's records, row pointers and spikes
+// in flight) are those of dw_slab_kernel.
+constexpr int kSamplesPerChunk = kDwWaves * kRowsPerBatch;
+
+__global__ __launch_bounds__(kDwThreads) void dw_slab_spikes_kernel(
+    const uint8_t* __restrict__ s_in, const float* __restrict__ ck, int K, float alpha, int T, int B, int N_in,
+    int N_out, const int32_t* __restrict__ sp, const SlabRec* __restrict__ rec, int64_t nrec, float* __restrict__ out,
+    int tlen, int n_bblk, int n_itiles, int n_slabs, int slab) {
+#pragma clang fp contract(off)  // the trace recurrence rounds its product and its sum separately
+  extern __shared__ double acc[];  // [slab][kLd]
+  int id = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) id = (id & 7) * (nb >> 3) + (id >> 3);
+  const int tiles = n_itiles * n_slabs;
+  const int c = id / tiles;
+  const int sl = (id - c * tiles) % n_slabs;
+  const int it = (id - c * tiles) / n_slabs;
+  const int tid = threadIdx.x;
+  const int w = tid / kWave;
+  const int l = tid % kWave;
+  const int TB = T * B;
+  const int i0 = it * kItile + l;
+  const int ic0 = min(i0, N_in - 1);
+  const int ic1 = min(i0 + kWave, N_in - 1);
+  const int j0 = sl * slab;
+  const int j1 = min(N_out, j0 + slab);
+  const int32_t* spl = sp + (size_t)sl * TB;
+  char* accb = reinterpret_cast<char*>(acc) + l * (int)sizeof(double);
+  const int max_off = (slab - 1) * kLd * (int)sizeof(double);
+
+  for (int k = tid; k < slab * kLd; k += kDwThreads) acc[k] = 0.0;
+  __syncthreads();
+
+  const int tb = c / n_bblk;
+  const int bb = c - tb * n_bblk;
+  const int t_lo = tb * tlen;  // a multiple of K
+  const int t_hi = min(T, t_lo + tlen);
+  const int b0 = bb * kSamplesPerChunk + w * kRowsPerBatch;
+  const int nbv = max(0, min(kRowsPerBatch, B - b0));  // this wavefront's samples
+  const int2* rec2 = reinterpret_cast<const int2*>(rec);
+  float tr0[kRowsPerBatch], tr1[kRowsPerBatch];
+#pragma unroll
+  for (int k = 0; k < kRowsPerBatch; ++k) {
+    const size_t row = ((size_t)(t_lo / K) * B + min(b0 + k, B - 1)) * N_in;
+    tr0[k] = ck[row + ic0];
+    tr1[k] = ck[row + ic1];
+  }
+  // lane k <= 8: row pointer of row t B + b0 + min(k, nbv) (rows past the samples: empty ranges)
+  auto load_sp = [&](int t) { return spl[(size_t)t * B + min(b0, B - 1) + min(l, nbv)]; };
+  auto load_rec = [&](int spv) { return rec2[min((int64_t)rdlane(spv, 0) + l, nrec - 1)]; };
+  auto load_spk = [&](int t, uint32_t* sk) {  // S[t] of the 8 samples at the lane's two inputs
+#pragma unroll
+    for (int k = 0; k < kRowsPerBatch; ++k) {
+      const uint8_t* row = s_in + ((size_t)t * B + min(b0 + k, B - 1)) * N_in;
+      sk[k] = (uint32_t)row[ic0] | ((uint32_t)row[ic1] << 8);
+    }
+  };
+  if (nbv > 0 && t_lo < t_hi) {
+    int spv = load_sp(t_lo);
+    int2 ra = load_rec(spv);
+    uint32_t sk[kRowsPerBatch];
+    load_spk(t_lo, sk);
+    int spv_n = load_sp(min(t_lo + 1, T - 1));
+    for (int t = t_lo; t < t_hi; ++t) {
+      const int2 ran = load_rec(spv_n);
+      uint32_t skn[kRowsPerBatch];
+      load_spk(min(t + 1, T - 1), skn);
+      const int spv_nn = load_sp(min(t + 2, T - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      const int base = rdlane(spv, 0);
+      const int n = rdlane(spv, kRowsPerBatch) - base;
+      if (n <= kWave) {
+        int lo = 0;
+#pragma unroll
+        for (int k = 0; k < kRowsPerBatch; ++k) {
+          const double t0 = (double)tr0[k], t1 = (double)tr1[k];
+          const int hi = rdlane(spv, k + 1) - base;
+          for (int s = lo; s < hi; ++s) {
+            const int off = (int)min((unsigned)rdlane(ra.x, s), (unsigned)max_off);
+            const double G = (double)__int_as_float(rdlane(ra.y, s));
+            double* a = reinterpret_cast<double*>(accb + off);
+            atomicAdd(a, t0 * G);
+            atomicAdd(a + kWave, t1 * G);
+          }
+          lo = hi;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < kRowsPerBatch; ++k) {
+          const double t0 = (double)tr0[k], t1 = (double)tr1[k];
+          const int lo = rdlane(spv, k);
+          const int hi = rdlane(spv, k + 1);
+          for (int s = lo; s < hi; ++s) {
+            const int2 x = rec2[min((int64_t)s, nrec - 1)];
+            const double G = (double)__int_as_float(x.y);
+            double* a = reinterpret_cast<double*>(accb + min(max(x.x, 0), max_off));
+            atomicAdd(a, t0 * G);
+            atomicAdd(a + kWave, t1 * G);
+          }
+        }
+      }
+      // trace[t + 1] = alpha trace[t] + S[t], separately rounded as in the forward
+#pragma unroll
+      for (int k = 0; k < kRowsPerBatch; ++k) {
+        tr0[k] = alpha * tr0[k] + ((sk[k] & 0xffu) ? 1.0f : 0.0f);  // not fused (contract off)
+        tr1[k] = alpha * tr1[k] + ((sk[k] & 0xff00u) ? 1.0f : 0.0f);
+        sk[k] = skn[k];
+      }
+      spv = spv_n;
+      spv_n = spv_nn;
+      ra = ran;
+    }
+  }
+  __syncthreads();
+  float* dst = out + (size_t)c * N_in * N_out;
+  const int width = j1 - j0;
+  for (int k = tid; k < kItile * width; k += kDwThreads) {
+    const int ii = k / width;
+    const int jj = k - ii * width;
+    if (it * kItile + ii < N_in) dst[(size_t)(it * kItile + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
+  }
+}
+
+// Trace checkpoints: ck[q, b, i] = the input trace at step q K (q < ceil(T / K)), from the spikes
+// by the forward's recurrence (one thread per (b, i)).
+__global__ void trace_checkpoints_kernel(const uint8_t* __restrict__ s_in, int T, int B, int N_in, float alpha, int K,
+                                         float* __restrict__ ck) {
+#pragma clang fp contract(off)  // the trace recurrence rounds its product and its sum separately
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // b * N_in + i
+  if (k >= (int64_t)B * N_in) return;
+  const int64_t step = (int64_t)B * N_in;
+  float tr = 0.0f;
+  for (int t0 = 0; t0 < T; t0 += K) {
+    ck[(int64_t)(t0 / K) * step + k] = tr;
+    const int t1 = min(T - 1, t0 + K);  // advance to step t1 (or stop at the last step)
+    uint8_t sv[16];
+    for (int t = t0; t < t1; t += 16) {
+      const int m = min(16, t1 - t);
+#pragma unroll
+      for (int u = 0; u < 16; ++u) sv[u] = s_in[(int64_t)(t + min(u, m - 1)) * step + k];
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (u < m) tr = alpha * tr + (sv[u] ? 1.0f : 0.0f);  // not fused (contract off)
+    }
+  }
+}
+
 __global__ void fill_zero(float* __restrict__ p, size_t n) {
   for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n; k += (size_t)gridDim.x * blockDim.x) p[k] = 0.0f;
 }
@@ -918,6 +1072,81 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
   }
 }
 
+// Chunks of the trace-recompute dW: 128 samples x tlen steps (tlen a multiple of K), about as
+// many as plan_dw's row chunks.
+struct SpikesPlan {
+  DwPlan base;
+  int tlen, n_tblk, n_bblk, n_chunks;
+};
+
+SpikesPlan plan_dw_spikes(int T, int B, int N_in, int N_out, int K) {
+  SpikesPlan q{};
+  q.base = plan_dw(T, B, N_in, N_out);
+  q.n_bblk = (B + kSamplesPerChunk - 1) / kSamplesPerChunk;
+  const int want = std::max(1, q.base.n_chunks / q.n_bblk);  // chunks along time
+  int tlen = (T + want - 1) / want;
+  tlen = ((tlen + K - 1) / K) * K;
+  q.tlen = tlen;
+  q.n_tblk = (T + tlen - 1) / tlen;
+  q.n_chunks = q.n_tblk * q.n_bblk;
+  return q;
+}
+
+size_t dw_spikes_workspace(int T, int B, int N_in, int N_out, int64_t out_cap, int K) {
+  const SpikesPlan q = plan_dw_spikes(T, B, N_in, N_out, K);
+  const int nsp = q.base.n_slabs * T * B;
+  Carve c(nullptr);
+  if (q.n_chunks > 1) c.take<float>((size_t)q.n_chunks * N_in * N_out);
+  c.take<int32_t>((size_t)nsp + 1);
+  c.take<int32_t>((size_t)nsp);
+  c.take<int32_t>(scan_temp_elems(nsp));
+  c.take<SlabRec>((size_t)std::max<int64_t>(out_cap, 1));
+  return c.off;
+}
+
+void enqueue_dw_spikes(const uint8_t* s_in, const float* ck, int K, float alpha, int T, int B, int N_in, int N_out,
+                       const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
+                       const float* eps_out, int64_t out_cap, float* dW, void* workspace, hipStream_t s) {
+  if (out_cap == 0) {
+    fill_zero_async(dW, (size_t)N_in * N_out, s);
+    return;
+  }
+  const int TB = T * B;
+  const SpikesPlan q = plan_dw_spikes(T, B, N_in, N_out, K);
+  const DwPlan& p = q.base;
+  Carve ws(workspace);
+  float* part = q.n_chunks > 1 ? ws.take<float>((size_t)q.n_chunks * N_in * N_out) : dW;
+  const int nsp = p.n_slabs * TB;
+  int32_t* sp = ws.take<int32_t>((size_t)nsp + 1);
+  int32_t* scnt = ws.take<int32_t>((size_t)nsp);
+  int32_t* stmp = ws.take<int32_t>(scan_temp_elems(nsp));
+  SlabRec* rec = ws.take<SlabRec>((size_t)std::max<int64_t>(out_cap, 1));
+  const int R = std::max(1, std::min(8, kWave / p.n_slabs));
+  const int nwaves = (TB + R - 1) / R;
+  const dim3 rgrid((unsigned)((nwaves + kRowWaves - 1) / kRowWaves));
+  const dim3 rblock(kRowWaves * kWave);
+  const int64_t nrec = std::max<int64_t>(out_cap, 1);
+  hipLaunchKernelGGL(slab_count, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr, out_col_idx,
+                     out_cap, scnt);
+  launch_exclusive_scan(scnt, nsp, sp, nullptr, stmp, s);
+  if (out_g)
+    hipLaunchKernelGGL(slab_fill<true>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
+                       out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
+  else
+    hipLaunchKernelGGL(slab_fill<false>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
+                       out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
+  const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * q.n_chunks));
+  (void)hipFuncSetAttribute((const void*)dw_slab_spikes_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)p.lds);
+  hipLaunchKernelGGL(dw_slab_spikes_kernel, dgrid, dim3(kDwThreads), p.lds, s, s_in, ck, K, alpha, T, B, N_in, N_out,
+                     sp, rec, nrec, part, q.tlen, q.n_bblk, p.n_itiles, p.n_slabs, p.slab);
+  if (q.n_chunks > 1) {
+    const size_t n = (size_t)N_in * N_out;
+    const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(reduce_chunks, dim3(blocks), dim3(256), 0, s, part, q.n_chunks, n, dW);
+  }
+}
+
 // Spike gradient of one layer: chunk sums, carries, the walk. share_cu keeps the walk to two
 // blocks per CU so that a kernel running beside it (dW) finds room. Arguments already validated.
 void enqueue_grad_in(const float* W, int T, int B, int N_in, int N_out, float alpha, const int32_t* out_row_ptr,
@@ -1002,6 +1231,42 @@ extern "C" snn_status snn_sparse_dw(const float* trace_in, int T, int B, int N_i
   if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
   enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, workspace,
              static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" int64_t snn_trace_checkpoint_count(int T, int K) {
+  if (bad_dim(T) || bad_dim(K)) return 0;
+  return (T + K - 1) / K;
+}
+
+extern "C" snn_status snn_trace_checkpoints(const uint8_t* s_in, int T, int B, int N_in, float alpha, int K, float* ck,
+                                            void* stream) {
+  if (!s_in || !ck || bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(K) || too_big(T, B, N_in))
+    return SNN_ERR_INVALID_ARG;
+  if (bad_alpha(alpha)) return SNN_ERR_INVALID_ARG;
+  const int64_t n = (int64_t)B * N_in;
+  hipLaunchKernelGGL(trace_checkpoints_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), s_in, T, B, N_in, alpha, K, ck);
+  return launch_status();
+}
+
+extern "C" size_t snn_sparse_dw_spikes_workspace(int T, int B, int N_in, int N_out, int64_t out_cap, int K) {
+  if (!dims_ok(T, B, N_in, N_out) || out_cap < 0 || bad_dim(K)) return 0;
+  return dw_spikes_workspace(T, B, N_in, N_out, out_cap, K);
+}
+
+extern "C" snn_status snn_sparse_dw_spikes(const uint8_t* s_in, const float* ck, int K, float alpha, int T, int B,
+                                           int N_in, int N_out, const int32_t* out_row_ptr,
+                                           const int32_t* out_col_idx, const float* out_g, const float* eps_out,
+                                           int64_t out_cap, float* dW, void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+  if (!s_in || !ck || !dW || !dims_ok(T, B, N_in, N_out) || bad_dim(K) || bad_alpha(alpha))
+    return SNN_ERR_INVALID_ARG;
+  if (!out_csr_ok(out_row_ptr, out_col_idx, eps_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < dw_spikes_workspace(T, B, N_in, N_out, out_cap, K)) return SNN_ERR_INVALID_ARG;
+  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+  enqueue_dw_spikes(s_in, ck, K, alpha, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW,
+                    workspace, static_cast<hipStream_t>(stream));
   return launch_status();
 }
 

@@ -38,6 +38,11 @@ class Network:
     trace_out: Optional[torch.Tensor] = None
     bits: List[torch.Tensor] = field(default_factory=list)  # active bitsets of the LIF layers
     bits_bth: Optional[float] = None
+    # trace recompute: with recompute_k = K > 0 the LIF layers' input traces are not stored; the
+    # forward keeps the trace at every K-th step (ck) and the sparse dW rebuilds the rest from the
+    # input spikes (snn_sparse_dw_spikes). The dense baseline needs the stored traces.
+    recompute_k: int = 0
+    ck: List[torch.Tensor] = field(default_factory=list)
 
     @property
     def T(self):
@@ -58,7 +63,12 @@ class Network:
         sizes = [self.X.shape[2]] + [W.shape[1] for W in self.Ws]
         self.V = [torch.empty((T, B, n), dtype=torch.float32, device=dev) for n in sizes[1:]]
         self.S = [torch.empty((T, B, n), dtype=torch.uint8, device=dev) for n in sizes[1:]]
-        self.trace = [torch.empty((T, B, n), dtype=torch.float32, device=dev) for n in sizes[:-1]]
+        if self.recompute_k > 0:
+            nck = snn.snn_trace_checkpoint_count(T, self.recompute_k)
+            self.trace = [None] * self.L
+            self.ck = [torch.empty((nck, B, n), dtype=torch.float32, device=dev) for n in sizes[:-1]]
+        else:
+            self.trace = [torch.empty((T, B, n), dtype=torch.float32, device=dev) for n in sizes[:-1]]
         C = self.W_out.shape[1]
         self.V_out = torch.empty((T, B, C), dtype=torch.float32, device=dev)
         self.S_out = torch.empty((T, B, C), dtype=torch.uint8, device=dev)
@@ -77,6 +87,8 @@ class Network:
                                      device=self.X.device) for W in self.Ws]
         self.bits_bth = b_th
         for l, W in enumerate(self.Ws):
+            if self.recompute_k > 0:
+                snn.trace_checkpoints(x, self.alphas[l], self.recompute_k, ck=self.ck[l])
             if b_th is None:
                 snn.snn_lif_forward(x, W, T, B, W.shape[0], W.shape[1], self.alphas[l], self.theta, self.V[l],
                                     self.S[l], self.trace[l])
@@ -122,13 +134,39 @@ class Network:
             if reg_coefs is not None:
                 snn.activity_reg_grad(reg_coefs[l], self.T, eps, csrs[l])
             epss[l] = eps
-            dWs[l], eps = snn.sparse_backward(self.Ws[l], self.trace[l], self.alphas[l], csrs[l], eps,
-                                              inp=csrs[l - 1] if l > 0 else None, ws=ws[l], aux_stream=aux_stream)
+            if self.recompute_k > 0:
+                dWs[l], eps = self._layer_backward_recompute(l, csrs, eps, aux_stream)
+            else:
+                dWs[l], eps = snn.sparse_backward(self.Ws[l], self.trace[l], self.alphas[l], csrs[l], eps,
+                                                  inp=csrs[l - 1] if l > 0 else None, ws=ws[l],
+                                                  aux_stream=aux_stream)
         return dWs, dW_out, epss
+
+    def _layer_backward_recompute(self, l, csrs, eps, aux_stream=None):
+        """Layer l's sparse backward with the trace rebuilt from its input spikes: the spike
+        gradient (on aux_stream when given) beside dW from snn_sparse_dw_spikes."""
+        s_in = self.X if l == 0 else self.S[l - 1]
+        W = self.Ws[l]
+        main = torch.cuda.current_stream()
+        eps_in = None
+        if l > 0:
+            side = aux_stream if aux_stream is not None else main
+            side.wait_stream(main)
+            with torch.cuda.stream(side):
+                eps_in = snn.sparse_grad_in(W, self.alphas[l], self.T, self.B, csrs[l], eps, csrs[l - 1],
+                                            share_cu=aux_stream is not None, stream=side)
+        dW = snn.sparse_dw_spikes(s_in, self.ck[l], self.recompute_k, self.alphas[l], csrs[l], eps, W.shape[1],
+                                  stream=main)
+        if l > 0 and aux_stream is not None:
+            main.wait_stream(aux_stream)
+            eps_in.record_stream(main)
+        return dW, eps_in
 
     def dense_backward(self, b_th, ro=None, reg_coefs=None):
         """The dense baseline chain (b_th = inf: full-surrogate BPTT). Returns (dW list, dW_out,
         eps_dense list); reg_coefs as in sparse_backward."""
+        if self.recompute_k > 0:
+            raise ValueError("dense_backward needs the stored input traces (recompute_k = 0)")
         if ro is None or ro[3] is None:
             ro = self.readout(dense=True)
         dW_out, eps = snn.dense_backward_ref(self.W_out, self.trace_out, self.V_out, ro[3], self.alpha_out, INF,

@@ -41,6 +41,10 @@ _SIGNATURES = {
     "snn_active_compact_bits": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_dw": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_trace_checkpoint_count": (_I64, [_I, _I]),
+    "snn_trace_checkpoints": (_I, [_P, _I, _I, _I, _F, _I, _P, _P]),
+    "snn_sparse_dw_spikes_workspace": (_SZ, [_I, _I, _I, _I, _I64, _I]),
+    "snn_sparse_dw_spikes": (_I, [_P, _P, _I, _F, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_sparse_grad_in_workspace": (_SZ, [_I, _I, _I]),
     "snn_sparse_grad_in": (_I, [_P, _I, _I, _I, _I, _F, _P, _P, _P, _P, _I64, _P, _P, _I64, _P, _I, _P, _SZ, _P]),
     "snn_dense_backward_workspace": (_SZ, [_I, _I, _I, _I]),
@@ -191,6 +195,29 @@ def snn_sparse_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, 
         _ptr(out_col_idx, torch.int32, "out_col_idx"), _ptr(out_g, torch.float32, "out_g"),
         _ptr(eps_out, torch.float32, "eps_out"), int(out_cap), _ptr(dW, torch.float32, "dW"),
         _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_trace_checkpoint_count(T, K) -> int:
+    return int(lib().snn_trace_checkpoint_count(T, K))
+
+
+def snn_trace_checkpoints(s_in, T, B, N_in, alpha, K, ck, stream=None):
+    _check("snn_trace_checkpoints", lib().snn_trace_checkpoints(
+        _ptr(s_in, torch.uint8, "s_in"), T, B, N_in, float(alpha), K, _ptr(ck, torch.float32, "ck"), _stream(stream)))
+
+
+def snn_sparse_dw_spikes_workspace(T, B, N_in, N_out, out_cap, K) -> int:
+    return int(lib().snn_sparse_dw_spikes_workspace(T, B, N_in, N_out, int(out_cap), K))
+
+
+def snn_sparse_dw_spikes(s_in, ck, K, alpha, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW,
+                         ws, stream=None):
+    _check("snn_sparse_dw_spikes", lib().snn_sparse_dw_spikes(
+        _ptr(s_in, torch.uint8, "s_in"), _ptr(ck, torch.float32, "ck"), K, float(alpha), T, B, N_in, N_out,
+        _ptr(out_row_ptr, torch.int32, "out_row_ptr"), _ptr(out_col_idx, torch.int32, "out_col_idx"),
+        _ptr(out_g, torch.float32, "out_g"), _ptr(eps_out, torch.float32, "eps_out"), int(out_cap),
+        _ptr(dW, torch.float32, "dW"), _ptr(ws, None, "workspace"),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def snn_sparse_grad_in_workspace(T, B, N_out) -> int:
@@ -421,6 +448,28 @@ def sparse_dw(trace_in, out: Csr, eps_out, N_out, ws=None, stream=None, dW=None)
         ws = workspace(snn_sparse_dw_workspace(T, B, N_in, N_out, out.capacity), dev)
     snn_sparse_dw(trace_in, T, B, N_in, N_out, out.row_ptr, out.col_idx, out.g, eps_out, out.capacity, dW, ws,
                   stream)
+    return dW
+
+
+def trace_checkpoints(s_in: torch.Tensor, alpha, K: int, ck=None, stream=None):
+    """Run snn_trace_checkpoints on s_in [T, B, N_in]. Returns ck [ceil(T/K), B, N_in]."""
+    T, B, N_in = s_in.shape
+    if ck is None:
+        ck = torch.empty((snn_trace_checkpoint_count(T, K), B, N_in), dtype=torch.float32, device=s_in.device)
+    snn_trace_checkpoints(s_in, T, B, N_in, alpha, K, ck, stream)
+    return ck
+
+
+def sparse_dw_spikes(s_in, ck, K, alpha, out: Csr, eps_out, N_out, ws=None, stream=None, dW=None):
+    """Run snn_sparse_dw_spikes (dW with the trace rebuilt from s_in and checkpoints ck)."""
+    T, B, N_in = s_in.shape
+    dev = s_in.device
+    if dW is None:
+        dW = torch.empty((N_in, N_out), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = workspace(snn_sparse_dw_spikes_workspace(T, B, N_in, N_out, out.capacity, K), dev)
+    snn_sparse_dw_spikes(s_in, ck, K, alpha, T, B, N_in, N_out, out.row_ptr, out.col_idx, out.g, eps_out,
+                         out.capacity, dW, ws, stream)
     return dW
 
 

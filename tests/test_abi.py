@@ -158,6 +158,36 @@ def test_sparse_dw_unsupported_width(lib):
     assert _sdw(lib, N_out=5000) == snn.SNN_ERR_UNSUPPORTED
 
 
+def _sds(lib, **kw):
+    a = dict(s=FAKE, ck=FAKE, K=8, alpha=0.9, T=10, B=4, N_in=32, N_out=16, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE,
+             ocap=10, dW=FAKE, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    return lib.snn_sparse_dw_spikes(a["s"], a["ck"], a["K"], a["alpha"], a["T"], a["B"], a["N_in"], a["N_out"],
+                                    a["orp"], a["oci"], a["og"], a["oeps"], a["ocap"], a["dW"], a["ws"], a["ws_bytes"],
+                                    None)
+
+
+@pytest.mark.parametrize("kw", [dict(s=None), dict(ck=None), dict(K=0), dict(alpha=1.5), dict(alpha=NAN),
+                                dict(dW=None), dict(orp=None), dict(oeps=None), dict(ocap=-1), dict(ws=None),
+                                dict(ws_bytes=8), dict(T=0)])
+def test_sparse_dw_spikes_rejects(lib, kw):
+    assert _sds(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_sparse_dw_spikes_unsupported_width_and_sizes(lib):
+    assert _sds(lib, N_out=5000) == snn.SNN_ERR_UNSUPPORTED
+    assert lib.snn_trace_checkpoint_count(500, 32) == 16
+    assert lib.snn_trace_checkpoint_count(17, 1) == 17
+    assert lib.snn_trace_checkpoint_count(0, 4) == 0 and lib.snn_trace_checkpoint_count(10, 0) == 0
+    assert lib.snn_sparse_dw_spikes_workspace(500, 256, 1024, 1024, 10 ** 6, 32) > 0
+    assert lib.snn_sparse_dw_spikes_workspace(500, 256, 1024, 1024, 10 ** 6, 0) == 0
+    for kw in (dict(s=None), dict(ck=None), dict(K=0), dict(alpha=0.0), dict(B=0)):
+        a = dict(s=FAKE, T=10, B=4, N_in=32, alpha=0.9, K=4, ck=FAKE)
+        a.update(kw)
+        assert lib.snn_trace_checkpoints(a["s"], a["T"], a["B"], a["N_in"], a["alpha"], a["K"], a["ck"],
+                                         None) == snn.SNN_ERR_INVALID_ARG
+
+
 def _sgi(lib, **kw):
     a = dict(W=FAKE, T=10, B=4, N_in=32, N_out=16, alpha=0.9, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE, ocap=10,
              irp=FAKE, ici=FAKE, icap=10, eps_in=FAKE, share=1, ws=FAKE, ws_bytes=1 << 40)
