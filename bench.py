@@ -396,6 +396,13 @@ class Runner:
             max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
         self.ws_gi = snn.workspace(max(snn.snn_sparse_grad_in_workspace(T, B, sizes[l + 1]) for l in range(L + 1)))
         self.ro = net.readout(dense=not args.no_dense)
+        self.dW_out = torch.empty_like(net.W_out)
+        # dW calls on their own stream beside the spike-gradient chain when there is a chain to
+        # overlap (two or more LIF layers) and the layers are large enough to pay for the extra
+        # cross-stream waits; layer by layer otherwise
+        sched = args.schedule
+        self.pipelined = sched == "pipelined" or (
+            sched == "auto" and L >= 2 and T * B * max(sizes[1:L + 1]) >= (1 << 24))
         self.ws_ro = snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[L], sizes[L + 1],
                                                                      self.ro[0].capacity))
 
@@ -458,35 +465,10 @@ class Runner:
         cs = R("compact", main, lambda: net.compact(self.b_th, self.caps))
         E("cmp1").record(main)
         use_aux = not (self.args.serial or self.args.graph)
-        eps = R("ro_bwd", main, lambda: snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1],
-                                                             inp=cs[L - 1], ws=self.ws_ro,
-                                                             aux_stream=aux if use_aux else None)[1])
-        E("ro1").record(main)
-        for l in range(L - 1, -1, -1):
-            i = L - 1 - l  # top layer first
-            ev["lay0"][i].record(main)
-            if l > 0:
-                if aux is not main:
-                    aux.wait_stream(main)
-                ev["gi0"][i].record(aux)
-                R(f"gi{l}", aux, lambda l=l, eps=eps: snn.sparse_grad_in(
-                    net.Ws[l], net.alphas[l], T, B, cs[l], eps, cs[l - 1], share_cu=self.share[l] and aux is not main,
-                    ws=self.ws_gi, eps_in=self.eps[l - 1]))
-                ev["gi1"][i].record(aux)
-            ev["dw0"][i].record(main)
-            if K:
-                R(f"dw{l}", main, lambda l=l, eps=eps: snn.sparse_dw_spikes(
-                    net.X if l == 0 else net.S[l - 1], self.ck[l], K, net.alphas[l], cs[l], eps, net.Ws[l].shape[1],
-                    ws=self.ws_dw[l], dW=self.dW[l]))
-            else:
-                R(f"dw{l}", main, lambda l=l, eps=eps: snn.sparse_dw(net.trace[l], cs[l], eps, net.Ws[l].shape[1],
-                                                                    ws=self.ws_dw[l], dW=self.dW[l]))
-            ev["dw1"][i].record(main)
-            if l > 0:
-                if aux is not main:
-                    main.wait_stream(aux)
-                eps = self.eps[l - 1]
-            ev["lay1"][i].record(main)
+        if self.pipelined and use_aux:
+            self._layers_pipelined(ev, r, cs, K)
+        else:
+            self._layers_layerwise(ev, r, cs, K, use_aux)
         if with_dense:
             def dense_chain():
                 _, e = snn.dense_backward_ref(net.W_out, net.trace_out, net.V_out, r[3], net.alpha_out, math.inf,
@@ -504,6 +486,77 @@ class Runner:
             R("dense", main, dense_layers)
             E("dn1").record(main)
         return cs
+
+    def _dw_call(self, l, eps, K):
+        snn, net = self.snn, self.net
+        if K:
+            return lambda: snn.sparse_dw_spikes(net.X if l == 0 else net.S[l - 1], self.ck[l], K, net.alphas[l],
+                                                self.cs[l], eps, net.Ws[l].shape[1], ws=self.ws_dw[l], dW=self.dW[l])
+        return lambda: snn.sparse_dw(net.trace[l], self.cs[l], eps, net.Ws[l].shape[1], ws=self.ws_dw[l],
+                                     dW=self.dW[l])
+
+    def _gi_call(self, l, eps, share):
+        snn, net = self.snn, self.net
+        return lambda: snn.sparse_grad_in(net.Ws[l], net.alphas[l], self.T, self.B, self.cs[l], eps, self.cs[l - 1],
+                                          share_cu=share, ws=self.ws_gi, eps_in=self.eps[l - 1])
+
+    def _layers_pipelined(self, ev, r, cs, K):
+        """The spike gradients form a chain (each layer's needs the one above); a layer's dW needs only
+        its own eps. The chain runs on main and every dW on the second stream as soon as its eps is
+        there, so the dW calls (the longer job) run back to back beside the chain."""
+        snn, net, main, dws, R = self.snn, self.net, self.main, self.aux, self.region
+        T, B, L = self.T, self.B, self.L
+        self.cs = cs
+        eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
+                                                         share_cu=True, ws=self.ws_gi, eps_in=self.eps[L - 1]))
+        ev["ro1"].record(main)
+        for l in range(L - 1, -1, -1):
+            i = L - 1 - l  # top layer first
+            dws.wait_stream(main)  # eps of layer l is ready
+            ev["lay0"][i].record(dws)
+            ev["dw0"][i].record(dws)
+            R(f"dw{l}", dws, self._dw_call(l, eps, K))
+            ev["dw1"][i].record(dws)
+            ev["lay1"][i].record(dws)
+            if l > 0:
+                ev["gi0"][i].record(main)
+                R(f"gi{l}", main, self._gi_call(l, eps, True))
+                ev["gi1"][i].record(main)
+                eps = self.eps[l - 1]
+        main.wait_stream(dws)
+        ev["bw1"].record(main)  # end of the LIF layers' backward
+        # the readout's dW, outside the measured chain (as the readout's loss and forward are)
+        R("ro_dw", main, lambda: snn.sparse_dw(net.trace_out, r[0], r[1], net.W_out.shape[1], ws=self.ws_ro,
+                                              dW=self.dW_out))
+
+    def _layers_layerwise(self, ev, r, cs, K, use_aux):
+        """Layer by layer: the readout's backward, then each LIF layer's spike gradient (on the second
+        stream) beside its dW, the next layer starting when both are done."""
+        snn, net, main, aux, R = self.snn, self.net, self.main, self.aux, self.region
+        L = self.L
+        self.cs = cs
+        eps = R("ro_bwd", main, lambda: snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1],
+                                                             inp=cs[L - 1], ws=self.ws_ro,
+                                                             aux_stream=aux if use_aux else None)[1])
+        ev["ro1"].record(main)
+        for l in range(L - 1, -1, -1):
+            i = L - 1 - l
+            ev["lay0"][i].record(main)
+            if l > 0:
+                if aux is not main:
+                    aux.wait_stream(main)
+                ev["gi0"][i].record(aux)
+                R(f"gi{l}", aux, self._gi_call(l, eps, self.share[l] and aux is not main))
+                ev["gi1"][i].record(aux)
+            ev["dw0"][i].record(main)
+            R(f"dw{l}", main, self._dw_call(l, eps, K))
+            ev["dw1"][i].record(main)
+            if l > 0:
+                if aux is not main:
+                    main.wait_stream(aux)
+                eps = self.eps[l - 1]
+            ev["lay1"][i].record(main)
+        ev["bw1"].record(main)
 
     def memory(self, nnz):
         """Per LIF layer: bytes each backward chain allocates beyond the shared forward state, and
@@ -524,7 +577,7 @@ class Runner:
 
     def events(self):
         mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
-        ev = {k: mk() for k in ("fwd0", "fwd1", "ck1", "cmp0", "cmp1", "ro1", "dn0", "dn1")}
+        ev = {k: mk() for k in ("fwd0", "fwd1", "ck1", "cmp0", "cmp1", "ro1", "bw1", "dn0", "dn1")}
         for k in ("lay0", "lay1", "gi0", "gi1", "dw0", "dw1"):
             ev[k] = [mk() for _ in range(self.L)]
         return ev
@@ -557,7 +610,7 @@ class Runner:
         t_dw = [span("dw0", "dw1", i) for i in range(L)]
         t_gi = [np.array([e["gi0"][i].elapsed_time(e["gi1"][i]) for e in evs]) for i in range(L - 1)]
         t_cmp = span("cmp0", "cmp1")
-        t_sparse = t_cmp + sum(t_layers)
+        t_sparse = t_cmp + span("ro1", "bw1")  # compaction + the LIF layers (readout excluded, as in the dense chain)
         t_step = np.array([e["fwd0"].elapsed_time(e["dn1"] if dense and not self.args.no_dense else e["lay1"][L - 1])
                            for e in evs])
 
@@ -661,6 +714,9 @@ def main():
                     help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
+    ap.add_argument("--schedule", choices=("auto", "pipelined", "layerwise"), default="auto",
+                    help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
+                         "or layer by layer (auto: pipelined for two or more large layers)")
     ap.add_argument("--recompute", type=int, default=0, metavar="K",
                     help="trace recompute: dW rebuilds the input trace from the spikes and checkpoints every K steps")
     ap.add_argument("--graph", action="store_true",

@@ -126,6 +126,8 @@ class Network:
             ro = self.readout()
         ro_csr, ro_eps = ro[0], ro[1]
         ws = workspaces or [None] * (self.L + 1)
+        if aux_stream is not None and self.L >= 2 and self.recompute_k == 0 and workspaces is None:
+            return self._sparse_backward_pipelined(csrs, ro_csr, ro_eps, aux_stream, reg_coefs)
         dW_out, eps = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro_csr, ro_eps,
                                           inp=csrs[self.L - 1], ws=ws[self.L], aux_stream=aux_stream)
         dWs: List[Optional[torch.Tensor]] = [None] * self.L
@@ -140,6 +142,34 @@ class Network:
                 dWs[l], eps = snn.sparse_backward(self.Ws[l], self.trace[l], self.alphas[l], csrs[l], eps,
                                                   inp=csrs[l - 1] if l > 0 else None, ws=ws[l],
                                                   aux_stream=aux_stream)
+        return dWs, dW_out, epss
+
+    def _sparse_backward_pipelined(self, csrs, ro_csr, ro_eps, aux, reg_coefs=None):
+        """The spike gradients form a chain down the layers (each needs the one above), while a
+        layer's dW needs only its own eps: the chain runs on the current stream and every dW on
+        aux as soon as its eps is there, so the dW calls run back to back beside the chain."""
+        main = torch.cuda.current_stream()
+        T, B, L = self.T, self.B, self.L
+        eps = snn.sparse_grad_in(self.W_out, self.alpha_out, T, B, ro_csr, ro_eps, csrs[L - 1], share_cu=True,
+                                 stream=main)
+        aux.wait_stream(main)
+        with torch.cuda.stream(aux):
+            dW_out = snn.sparse_dw(self.trace_out, ro_csr, ro_eps, self.W_out.shape[1], stream=aux)
+        dWs: List[Optional[torch.Tensor]] = [None] * L
+        epss: List[Optional[torch.Tensor]] = [None] * L
+        for l in range(L - 1, -1, -1):
+            if reg_coefs is not None:
+                snn.activity_reg_grad(reg_coefs[l], T, eps, csrs[l])
+            epss[l] = eps
+            aux.wait_stream(main)  # eps of layer l is ready
+            with torch.cuda.stream(aux):
+                dWs[l] = snn.sparse_dw(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], stream=aux)
+            if l > 0:
+                eps = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=True,
+                                         stream=main)
+        main.wait_stream(aux)
+        for t in dWs + [dW_out]:
+            t.record_stream(main)
         return dWs, dW_out, epss
 
     def _layer_backward_recompute(self, l, csrs, eps, aux_stream=None):

@@ -243,6 +243,23 @@ def test_aux_stream_overlap(name, batch, b_th):
         assert torch.equal(a["eps"][l][:n], b["eps"][l][:n])  # fixed summation order on either stream
 
 
+@pytest.mark.parametrize("maker,b_th", [(_ragged, 0.3), (lambda: _case("deep", list(range(6))), 0.2)])
+def test_pipelined_schedule_matches_layerwise(maker, b_th):
+    """With an auxiliary stream and two or more LIF layers, Network.sparse_backward runs the
+    spike-gradient chain on the current stream and every dW on the auxiliary stream: the same
+    dW, readout dW and spike gradients, bit for bit, as the layer-by-layer schedule."""
+    inp = maker()
+    print(f"\n[case] pipelined schedule {inp.cfg.name} b_th={b_th}", flush=True)
+    a = _gpu(inp, b_th, dense=False, aux=torch.cuda.Stream())
+    b = _gpu(inp, b_th, dense=False)
+    assert torch.equal(a["dW_out"], b["dW_out"])
+    for l in range(len(inp.Ws)):
+        assert torch.equal(a["dW"][l], b["dW"][l]), f"dW[{l}]"
+        n = a["csrs"][l].nnz()
+        assert torch.equal(a["eps"][l][:n], b["eps"][l][:n]), f"eps[{l}]"
+    check_all(inp, b_th, a, _oracle(inp, b_th), dense=False)
+
+
 @pytest.mark.parametrize("name,batch,b_th", [("latency", list(range(16)), math.inf), ("stress", [0, 1], 0.8),
                                              ("ragged_sum", None, math.inf)])
 def test_compaction_long_rows(name, batch, b_th):
