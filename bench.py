@@ -398,11 +398,9 @@ class Runner:
         self.ro = net.readout(dense=not args.no_dense)
         self.dW_out = torch.empty_like(net.W_out)
         # dW calls on their own stream beside the spike-gradient chain when there is a chain to
-        # overlap (two or more LIF layers) and the layers are large enough to pay for the extra
-        # cross-stream waits; layer by layer otherwise
+        # overlap (two or more LIF layers); layer by layer otherwise
         sched = args.schedule
-        self.pipelined = sched == "pipelined" or (
-            sched == "auto" and L >= 2 and T * B * max(sizes[1:L + 1]) >= (1 << 24))
+        self.pipelined = sched == "pipelined" or (sched == "auto" and L >= 2)
         self.ws_ro = snn.workspace(snn.snn_sparse_backward_workspace(T, B, sizes[L], sizes[L + 1],
                                                                      self.ro[0].capacity))
 
@@ -487,8 +485,11 @@ class Runner:
             E("dn1").record(main)
         return cs
 
-    def _dw_call(self, l, eps, K):
+    def _dw_call(self, l, eps, K, prepared=False):
         snn, net = self.snn, self.net
+        if prepared:
+            return lambda: snn.sparse_dw_prepared(net.trace[l], self.cs[l], eps, net.Ws[l].shape[1], self.ws_dw[l],
+                                                  dW=self.dW[l])
         if K:
             return lambda: snn.sparse_dw_spikes(net.X if l == 0 else net.S[l - 1], self.ck[l], K, net.alphas[l],
                                                 self.cs[l], eps, net.Ws[l].shape[1], ws=self.ws_dw[l], dW=self.dW[l])
@@ -507,15 +508,20 @@ class Runner:
         snn, net, main, dws, R = self.snn, self.net, self.main, self.aux, self.region
         T, B, L = self.T, self.B, self.L
         self.cs = cs
+        if not K:  # the dW parts that need only the active sets run on the dW stream right away
+            dws.wait_stream(main)
+            for l in range(L - 1, -1, -1):
+                R(f"lay{l}", dws, lambda l=l: snn.sparse_dw_layout((T, B, self.sizes[l]), cs[l], self.sizes[l + 1],
+                                                                    self.ws_dw[l]))
         eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
-                                                         share_cu=True, ws=self.ws_gi, eps_in=self.eps[L - 1]))
+                                                         share_cu=False, ws=self.ws_gi, eps_in=self.eps[L - 1]))
         ev["ro1"].record(main)
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
             dws.wait_stream(main)  # eps of layer l is ready
             ev["lay0"][i].record(dws)
             ev["dw0"][i].record(dws)
-            R(f"dw{l}", dws, self._dw_call(l, eps, K))
+            R(f"dw{l}", dws, self._dw_call(l, eps, K, prepared=not K))
             ev["dw1"][i].record(dws)
             ev["lay1"][i].record(dws)
             if l > 0:
@@ -716,7 +722,7 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
     ap.add_argument("--schedule", choices=("auto", "pipelined", "layerwise"), default="auto",
                     help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
-                         "or layer by layer (auto: pipelined for two or more large layers)")
+                         "or layer by layer (auto: pipelined for two or more LIF layers)")
     ap.add_argument("--recompute", type=int, default=0, metavar="K",
                     help="trace recompute: dW rebuilds the input trace from the spikes and checkpoints every K steps")
     ap.add_argument("--graph", action="store_true",

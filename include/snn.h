@@ -173,6 +173,23 @@ snn_status snn_sparse_dw(const float* trace_in, int T, int B, int N_in, int N_ou
                          const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
                          const float* eps_out, int64_t out_cap, float* dW, void* workspace,
                          size_t workspace_bytes, void* stream);
+/*
+ * snn_sparse_dw in two parts, so that the part that needs only the active set's structure can
+ * run early (right after compaction, before any eps exists) and off the critical path:
+ * snn_sparse_dw_layout reads out_row_ptr and out_col_idx only and writes the per-(row, column
+ * slab) entry counts and offsets (or, for N_out <= 32, the bitset of rows with an entry) into the
+ * workspace; snn_sparse_dw_prepared then does the rest of snn_sparse_dw (arguments as there) and
+ * gives the same dW bit for bit, provided the layout ran on the same workspace with a CSR of the
+ * same structure (row pointers and columns) and out_cap, and the workspace was not used in
+ * between. Workspace from snn_sparse_dw_workspace. Errors as snn_sparse_dw.
+ */
+snn_status snn_sparse_dw_layout(int T, int B, int N_in, int N_out, const int32_t* out_row_ptr,
+                                const int32_t* out_col_idx, int64_t out_cap, void* workspace,
+                                size_t workspace_bytes, void* stream);
+snn_status snn_sparse_dw_prepared(const float* trace_in, int T, int B, int N_in, int N_out,
+                                  const int32_t* out_row_ptr, const int32_t* out_col_idx, const float* out_g,
+                                  const float* eps_out, int64_t out_cap, float* dW, void* workspace,
+                                  size_t workspace_bytes, void* stream);
 size_t snn_sparse_grad_in_workspace(int T, int B, int N_out);
 snn_status snn_sparse_grad_in(const float* W, int T, int B, int N_in, int N_out, float alpha,
                               const int32_t* out_row_ptr, const int32_t* out_col_idx,

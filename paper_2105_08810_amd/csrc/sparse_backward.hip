@@ -1004,11 +1004,16 @@ void enqueue_narrow_g(int TB, int N_out, const int32_t* out_row_ptr, const int32
 
 // dW of one layer. For a narrow layer the dense G goes to the front of the workspace; g_ready
 // says it is there already (written by enqueue_narrow_g on this stream).
+// The parts of a dW call: the layout depends only on the output CSR's structure (row pointers,
+// columns); the rest needs eps too. kAll runs both.
+enum DwPhase { kDwAll, kDwLayout, kDwRest };
+
 void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const int32_t* out_row_ptr,
                 const int32_t* out_col_idx, const float* out_g, const float* eps_out, int64_t out_cap, float* dW,
-                void* workspace, hipStream_t s, bool g_ready = false) {
+                void* workspace, hipStream_t s, bool g_ready = false, DwPhase phase = kDwAll) {
+  const bool layout = phase != kDwRest, rest = phase != kDwLayout;
   if (out_cap == 0) {  // no active output entry: dW = 0 and no entry array is read
-    fill_zero_async(dW, (size_t)N_in * N_out, s);
+    if (rest) fill_zero_async(dW, (size_t)N_in * N_out, s);
     return;
   }
   if (N_out <= kNarrowOut) {
@@ -1018,9 +1023,11 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
     float* Gd = ws.take<float>((size_t)TB * narrow_ld(N_out));
     uint64_t* busy = ws.take<uint64_t>(((size_t)TB + kWave - 1) / kWave);
     float* part = q.n_chunks > 1 ? ws.take<float>((size_t)q.n_chunks * N_in * N_out) : dW;
+    if (layout)
+      hipLaunchKernelGGL(narrow_busy_rows, dim3((unsigned)((TB + 255) / 256)), dim3(256), 0, s, TB, out_row_ptr,
+                         out_cap, busy);
+    if (!rest) return;
     if (!g_ready) enqueue_narrow_g(TB, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, Gd, s);
-    hipLaunchKernelGGL(narrow_busy_rows, dim3((unsigned)((TB + 255) / 256)), dim3(256), 0, s, TB, out_row_ptr, out_cap,
-                       busy);
     // columns in blocks of 8 (N_out <= 8) or 16 (grid y: one or two blocks)
     const int ld = narrow_ld(N_out);
     const unsigned blocks = (unsigned)(((int64_t)q.n_chunks * q.n_iw * kWave + 255) / 256);
@@ -1052,9 +1059,12 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
   const dim3 rgrid((unsigned)((nwaves + kRowWaves - 1) / kRowWaves));
   const dim3 rblock(kRowWaves * kWave);
   const int64_t nrec = std::max<int64_t>(out_cap, 1);
-  hipLaunchKernelGGL(slab_count, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr, out_col_idx,
-                     out_cap, scnt);
-  launch_exclusive_scan(scnt, nsp, sp, nullptr, stmp, s);
+  if (layout) {
+    hipLaunchKernelGGL(slab_count, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr, out_col_idx,
+                       out_cap, scnt);
+    launch_exclusive_scan(scnt, nsp, sp, nullptr, stmp, s);
+  }
+  if (!rest) return;
   if (out_g)
     hipLaunchKernelGGL(slab_fill<true>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
                        out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
@@ -1231,6 +1241,31 @@ extern "C" snn_status snn_sparse_dw(const float* trace_in, int T, int B, int N_i
   if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
   enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, workspace,
              static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+extern "C" snn_status snn_sparse_dw_layout(int T, int B, int N_in, int N_out, const int32_t* out_row_ptr,
+                                           const int32_t* out_col_idx, int64_t out_cap, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  if (!dims_ok(T, B, N_in, N_out) || !out_row_ptr || out_cap < 0 || (out_cap > 0 && !out_col_idx))
+    return SNN_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < dw_workspace(T, B, N_in, N_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+  enqueue_dw(nullptr, T, B, N_in, N_out, out_row_ptr, out_col_idx, nullptr, nullptr, out_cap, nullptr, workspace,
+             static_cast<hipStream_t>(stream), false, kDwLayout);
+  return launch_status();
+}
+
+extern "C" snn_status snn_sparse_dw_prepared(const float* trace_in, int T, int B, int N_in, int N_out,
+                                             const int32_t* out_row_ptr, const int32_t* out_col_idx,
+                                             const float* out_g, const float* eps_out, int64_t out_cap, float* dW,
+                                             void* workspace, size_t workspace_bytes, void* stream) {
+  if (!trace_in || !dW || !dims_ok(T, B, N_in, N_out)) return SNN_ERR_INVALID_ARG;
+  if (!out_csr_ok(out_row_ptr, out_col_idx, eps_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < dw_workspace(T, B, N_in, N_out, out_cap)) return SNN_ERR_INVALID_ARG;
+  if (N_out > 4096) return SNN_ERR_UNSUPPORTED;
+  enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, workspace,
+             static_cast<hipStream_t>(stream), false, kDwRest);
   return launch_status();
 }
 

@@ -150,11 +150,16 @@ class Network:
         aux as soon as its eps is there, so the dW calls run back to back beside the chain."""
         main = torch.cuda.current_stream()
         T, B, L = self.T, self.B, self.L
+        aux.wait_stream(main)  # the active sets are ready: the dW parts that need only them start on aux
+        wss = []
+        with torch.cuda.stream(aux):
+            for l in range(L):
+                n_in, n_out = self.Ws[l].shape
+                ws = snn.workspace(snn.snn_sparse_dw_workspace(T, B, n_in, n_out, csrs[l].capacity), self.X.device)
+                snn.sparse_dw_layout((T, B, n_in), csrs[l], n_out, ws, stream=aux)
+                wss.append(ws)
         eps = snn.sparse_grad_in(self.W_out, self.alpha_out, T, B, ro_csr, ro_eps, csrs[L - 1], share_cu=True,
                                  stream=main)
-        aux.wait_stream(main)
-        with torch.cuda.stream(aux):
-            dW_out = snn.sparse_dw(self.trace_out, ro_csr, ro_eps, self.W_out.shape[1], stream=aux)
         dWs: List[Optional[torch.Tensor]] = [None] * L
         epss: List[Optional[torch.Tensor]] = [None] * L
         for l in range(L - 1, -1, -1):
@@ -163,10 +168,12 @@ class Network:
             epss[l] = eps
             aux.wait_stream(main)  # eps of layer l is ready
             with torch.cuda.stream(aux):
-                dWs[l] = snn.sparse_dw(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], stream=aux)
+                dWs[l] = snn.sparse_dw_prepared(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], wss[l], stream=aux)
             if l > 0:
                 eps = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=True,
                                          stream=main)
+        with torch.cuda.stream(aux):  # the readout's dW last: nothing below waits for it
+            dW_out = snn.sparse_dw(self.trace_out, ro_csr, ro_eps, self.W_out.shape[1], stream=aux)
         main.wait_stream(aux)
         for t in dWs + [dW_out]:
             t.record_stream(main)

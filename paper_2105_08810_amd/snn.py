@@ -41,6 +41,8 @@ _SIGNATURES = {
     "snn_active_compact_bits": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_dw": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_sparse_dw_layout": (_I, [_I, _I, _I, _I, _P, _P, _I64, _P, _SZ, _P]),
+    "snn_sparse_dw_prepared": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_trace_checkpoint_count": (_I64, [_I, _I]),
     "snn_trace_checkpoints": (_I, [_P, _I, _I, _I, _F, _I, _P, _P]),
     "snn_sparse_dw_spikes_workspace": (_SZ, [_I, _I, _I, _I, _I64, _I]),
@@ -195,6 +197,38 @@ def snn_sparse_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, 
         _ptr(out_col_idx, torch.int32, "out_col_idx"), _ptr(out_g, torch.float32, "out_g"),
         _ptr(eps_out, torch.float32, "eps_out"), int(out_cap), _ptr(dW, torch.float32, "dW"),
         _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_sparse_dw_layout(T, B, N_in, N_out, out_row_ptr, out_col_idx, out_cap, ws, stream=None):
+    _check("snn_sparse_dw_layout", lib().snn_sparse_dw_layout(
+        T, B, N_in, N_out, _ptr(out_row_ptr, torch.int32, "out_row_ptr"), _ptr(out_col_idx, torch.int32, "out_col_idx"),
+        int(out_cap), _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def snn_sparse_dw_prepared(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, ws,
+                           stream=None):
+    _check("snn_sparse_dw_prepared", lib().snn_sparse_dw_prepared(
+        _ptr(trace_in, torch.float32, "trace_in"), T, B, N_in, N_out, _ptr(out_row_ptr, torch.int32, "out_row_ptr"),
+        _ptr(out_col_idx, torch.int32, "out_col_idx"), _ptr(out_g, torch.float32, "out_g"),
+        _ptr(eps_out, torch.float32, "eps_out"), int(out_cap), _ptr(dW, torch.float32, "dW"),
+        _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def sparse_dw_layout(trace_shape, out: "Csr", N_out, ws, stream=None):
+    """Run snn_sparse_dw_layout for a layer whose input trace has shape [T, B, N_in] into ws."""
+    T, B, N_in = trace_shape
+    snn_sparse_dw_layout(T, B, N_in, N_out, out.row_ptr, out.col_idx, out.capacity, ws, stream)
+
+
+def sparse_dw_prepared(trace_in, out: "Csr", eps_out, N_out, ws, stream=None, dW=None):
+    """Run snn_sparse_dw_prepared (after sparse_dw_layout on ws). Returns dW [N_in, N_out]."""
+    T, B, N_in = trace_in.shape
+    if dW is None:
+        dW = torch.empty((N_in, N_out), dtype=torch.float32, device=trace_in.device)
+    snn_sparse_dw_prepared(trace_in, T, B, N_in, N_out, out.row_ptr, out.col_idx, out.g, eps_out, out.capacity, dW,
+                           ws, stream)
+    return dW
 
 
 def snn_trace_checkpoint_count(T, K) -> int:

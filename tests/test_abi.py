@@ -188,6 +188,25 @@ def test_sparse_dw_spikes_unsupported_width_and_sizes(lib):
                                          None) == snn.SNN_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("kw", [dict(orp=None), dict(oci=None), dict(ocap=-1), dict(ws=None), dict(ws_bytes=8),
+                                dict(T=0), dict(N_in=-2)])
+def test_sparse_dw_layout_rejects(lib, kw):
+    a = dict(T=10, B=4, N_in=32, N_out=16, orp=FAKE, oci=FAKE, ocap=10, ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    assert lib.snn_sparse_dw_layout(a["T"], a["B"], a["N_in"], a["N_out"], a["orp"], a["oci"], a["ocap"], a["ws"],
+                                    a["ws_bytes"], None) == snn.SNN_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [dict(tr=None), dict(dW=None), dict(orp=None), dict(oeps=None), dict(ws_bytes=8)])
+def test_sparse_dw_prepared_rejects(lib, kw):
+    a = dict(tr=FAKE, T=10, B=4, N_in=32, N_out=16, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE, ocap=10, dW=FAKE,
+             ws=FAKE, ws_bytes=1 << 40)
+    a.update(kw)
+    assert lib.snn_sparse_dw_prepared(a["tr"], a["T"], a["B"], a["N_in"], a["N_out"], a["orp"], a["oci"], a["og"],
+                                      a["oeps"], a["ocap"], a["dW"], a["ws"], a["ws_bytes"],
+                                      None) == snn.SNN_ERR_INVALID_ARG
+
+
 def _sgi(lib, **kw):
     a = dict(W=FAKE, T=10, B=4, N_in=32, N_out=16, alpha=0.9, orp=FAKE, oci=FAKE, og=FAKE, oeps=FAKE, ocap=10,
              irp=FAKE, ici=FAKE, icap=10, eps_in=FAKE, share=1, ws=FAKE, ws_bytes=1 << 40)

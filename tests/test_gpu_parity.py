@@ -491,3 +491,24 @@ def test_graph_replays_match_eager():
             d = (snap["dW"][l] - dW_e[l]).abs().max().item()
             assert d <= 1e-6 * dW_e[l].abs().max().item() + 1e-30, (l, d)
         assert (snap["dWo"] - dWo_e).abs().max().item() <= 1e-6 * dWo_e.abs().max().item() + 1e-30
+
+
+@pytest.mark.parametrize("maker", [_ragged, lambda: _case("stress", [0, 1, 2])])
+def test_dw_layout_then_prepared_equals_one_call(maker):
+    """snn_sparse_dw_layout (structure only, run before eps exists) followed by
+    snn_sparse_dw_prepared gives snn_sparse_dw's dW bit for bit, for narrow (<= 32 outputs) and
+    slab layers alike; the layout can be reused with a second eps."""
+    inp = maker()
+    print(f"\n[case] dW layout + prepared {inp.cfg.name}", flush=True)
+    g = _gpu(inp, 0.3, dense=False)
+    net, csrs = g["net"], g["csrs"]
+    T, B = net.T, net.B
+    for l in range(net.L):
+        n_in, n_out = net.Ws[l].shape
+        ws = snn.workspace(snn.snn_sparse_dw_workspace(T, B, n_in, n_out, csrs[l].capacity))
+        snn.sparse_dw_layout((T, B, n_in), csrs[l], n_out, ws)
+        for eps in (g["eps"][l], 2.0 * g["eps"][l]):
+            got = snn.sparse_dw_prepared(net.trace[l], csrs[l], eps, n_out, ws)
+            ref = snn.sparse_dw(net.trace[l], csrs[l], eps, n_out)
+            torch.cuda.synchronize()
+            assert torch.equal(got, ref), f"dW[{l}]"
