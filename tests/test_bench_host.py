@@ -33,6 +33,12 @@ def test_more_than_one_gpu_is_refused(args, env):
     assert "one GPU" in r.stderr
 
 
+def test_recompute_is_refused_for_conv():
+    r = _run(["--workload", "conv", "--recompute", "8"])
+    assert r.returncode == 2
+    assert "fully connected" in r.stderr
+
+
 def test_algorithmic_counts_by_hand():
     # T=2, B=3, 5 inputs, 4 outputs; 7 active outputs on 4 rows, 6 input-active entries
     by_dw, fl_dw, by_gi, fl_gi = bench.algorithmic(2, 3, 5, 4, nnz_out=7, r_out=4, nnz_in=6)
