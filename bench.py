@@ -391,6 +391,7 @@ class Runner:
         net.forward()
         self.main = torch.cuda.current_stream()
         self.aux = self.main if args.serial else torch.cuda.Stream()  # default priority
+        self.dw_extra = [] if args.serial else [torch.cuda.Stream() for _ in range(args.dw_streams - 1)]
         T, B, L, sizes = self.T, self.B, self.L, self.sizes
         self.ws_dn = None if args.no_dense else snn.workspace(
             max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
@@ -508,28 +509,35 @@ class Runner:
         snn, net, main, dws, R = self.snn, self.net, self.main, self.aux, self.region
         T, B, L = self.T, self.B, self.L
         self.cs = cs
+        # dW streams taken in turn by layer: a layer's dW starts as soon as its eps is there, not
+        # after the previous layer's dW (its final chunk reduction, or a small layer's whole call)
+        dw_streams = [dws] + self.dw_extra
+        dws.wait_stream(main)
         if not K:  # the dW parts that need only the active sets run on the dW stream right away
-            dws.wait_stream(main)
             for l in range(L - 1, -1, -1):
                 R(f"lay{l}", dws, lambda l=l: snn.sparse_dw_layout((T, B, self.sizes[l]), cs[l], self.sizes[l + 1],
                                                                     self.ws_dw[l]))
+        for s2 in dw_streams[1:]:
+            s2.wait_stream(dws)
         eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
                                                          share_cu=False, ws=self.ws_gi, eps_in=self.eps[L - 1]))
         ev["ro1"].record(main)
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
-            dws.wait_stream(main)  # eps of layer l is ready
-            ev["lay0"][i].record(dws)
-            ev["dw0"][i].record(dws)
-            R(f"dw{l}", dws, self._dw_call(l, eps, K, prepared=not K))
-            ev["dw1"][i].record(dws)
-            ev["lay1"][i].record(dws)
+            sd = dw_streams[i % len(dw_streams)]
+            sd.wait_stream(main)  # eps of layer l is ready
+            ev["lay0"][i].record(sd)
+            ev["dw0"][i].record(sd)
+            R(f"dw{l}", sd, self._dw_call(l, eps, K, prepared=not K))
+            ev["dw1"][i].record(sd)
+            ev["lay1"][i].record(sd)
             if l > 0:
                 ev["gi0"][i].record(main)
                 R(f"gi{l}", main, self._gi_call(l, eps, True))
                 ev["gi1"][i].record(main)
                 eps = self.eps[l - 1]
-        main.wait_stream(dws)
+        for sd in dw_streams:
+            main.wait_stream(sd)
         ev["bw1"].record(main)  # end of the LIF layers' backward
         # the readout's dW, outside the measured chain (as the readout's loss and forward are)
         R("ro_dw", main, lambda: snn.sparse_dw(net.trace_out, r[0], r[1], net.W_out.shape[1], ws=self.ws_ro,
@@ -723,6 +731,8 @@ def main():
     ap.add_argument("--schedule", choices=("auto", "pipelined", "layerwise"), default="auto",
                     help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
                          "or layer by layer (auto: pipelined for two or more LIF layers)")
+    ap.add_argument("--dw-streams", type=int, default=2, metavar="N",
+                    help="pipelined schedule: streams the dW calls take in turn, layer by layer (default 2)")
     ap.add_argument("--recompute", type=int, default=0, metavar="K",
                     help="trace recompute: dW rebuilds the input trace from the spikes and checkpoints every K steps")
     ap.add_argument("--graph", action="store_true",

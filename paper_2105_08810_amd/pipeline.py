@@ -43,6 +43,7 @@ class Network:
     # input spikes (snn_sparse_dw_spikes). The dense baseline needs the stored traces.
     recompute_k: int = 0
     ck: List[torch.Tensor] = field(default_factory=list)
+    _aux2: Optional[torch.cuda.Stream] = None  # second dW stream of the pipelined schedule
 
     @property
     def T(self):
@@ -150,6 +151,11 @@ class Network:
         aux as soon as its eps is there, so the dW calls run back to back beside the chain."""
         main = torch.cuda.current_stream()
         T, B, L = self.T, self.B, self.L
+        if self._aux2 is None:
+            self._aux2 = torch.cuda.Stream()  # default priority
+        # dW streams taken in turn by layer: a layer's dW starts as soon as its eps is there, not
+        # after the previous layer's dW
+        streams = [aux, self._aux2]
         aux.wait_stream(main)  # the active sets are ready: the dW parts that need only them start on aux
         wss = []
         with torch.cuda.stream(aux):
@@ -158,6 +164,7 @@ class Network:
                 ws = snn.workspace(snn.snn_sparse_dw_workspace(T, B, n_in, n_out, csrs[l].capacity), self.X.device)
                 snn.sparse_dw_layout((T, B, n_in), csrs[l], n_out, ws, stream=aux)
                 wss.append(ws)
+        self._aux2.wait_stream(aux)
         eps = snn.sparse_grad_in(self.W_out, self.alpha_out, T, B, ro_csr, ro_eps, csrs[L - 1], share_cu=True,
                                  stream=main)
         dWs: List[Optional[torch.Tensor]] = [None] * L
@@ -166,16 +173,18 @@ class Network:
             if reg_coefs is not None:
                 snn.activity_reg_grad(reg_coefs[l], T, eps, csrs[l])
             epss[l] = eps
-            aux.wait_stream(main)  # eps of layer l is ready
-            with torch.cuda.stream(aux):
-                dWs[l] = snn.sparse_dw_prepared(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], wss[l], stream=aux)
+            sd = streams[(L - 1 - l) % 2]
+            sd.wait_stream(main)  # eps of layer l is ready
+            with torch.cuda.stream(sd):
+                dWs[l] = snn.sparse_dw_prepared(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], wss[l], stream=sd)
             if l > 0:
                 eps = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=True,
                                          stream=main)
         with torch.cuda.stream(aux):  # the readout's dW last: nothing below waits for it
             dW_out = snn.sparse_dw(self.trace_out, ro_csr, ro_eps, self.W_out.shape[1], stream=aux)
-        main.wait_stream(aux)
-        for t in dWs + [dW_out]:
+        for sd in streams:
+            main.wait_stream(sd)
+        for t in dWs + [dW_out] + wss:
             t.record_stream(main)
         return dWs, dW_out, epss
 
