@@ -504,27 +504,27 @@ class Runner:
 
     def _layers_pipelined(self, ev, r, cs, K):
         """The spike gradients form a chain (each layer's needs the one above); a layer's dW needs only
-        its own eps. The chain runs on main and every dW on the second stream as soon as its eps is
-        there, so the dW calls (the longer job) run back to back beside the chain."""
+        its own eps. The chain runs on main and every dW on a dW stream as soon as its eps is there,
+        so the dW calls (the longer job) run back to back beside the chain."""
         snn, net, main, dws, R = self.snn, self.net, self.main, self.aux, self.region
         T, B, L = self.T, self.B, self.L
         self.cs = cs
         # dW streams taken in turn by layer: a layer's dW starts as soon as its eps is there, not
         # after the previous layer's dW (its final chunk reduction, or a small layer's whole call)
         dw_streams = [dws] + self.dw_extra
-        dws.wait_stream(main)
-        if not K:  # the dW parts that need only the active sets run on the dW stream right away
-            for l in range(L - 1, -1, -1):
-                R(f"lay{l}", dws, lambda l=l: snn.sparse_dw_layout((T, B, self.sizes[l]), cs[l], self.sizes[l + 1],
-                                                                    self.ws_dw[l]))
-        for s2 in dw_streams[1:]:
-            s2.wait_stream(dws)
         eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
                                                          share_cu=False, ws=self.ws_gi, eps_in=self.eps[L - 1]))
         ev["ro1"].record(main)
+        # From here on every kernel is LIF-layer work (timed). A layer's structure-only dW part goes
+        # first on its dW stream (it needs no eps), where it overlaps the work of the layer above.
+        for sd in dw_streams:
+            sd.wait_stream(main)
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
             sd = dw_streams[i % len(dw_streams)]
+            if not K:
+                R(f"lay{l}", sd, lambda l=l: snn.sparse_dw_layout((T, B, self.sizes[l]), cs[l], self.sizes[l + 1],
+                                                                   self.ws_dw[l]))
             sd.wait_stream(main)  # eps of layer l is ready
             ev["lay0"][i].record(sd)
             ev["dw0"][i].record(sd)
