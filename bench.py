@@ -391,8 +391,13 @@ class Runner:
         net.forward()
         self.main = torch.cuda.current_stream()
         self.aux = self.main if args.serial else torch.cuda.Stream()  # default priority
-        self.dw_extra = [] if args.serial else [torch.cuda.Stream() for _ in range(args.dw_streams - 1)]
         T, B, L, sizes = self.T, self.B, self.L, self.sizes
+        # dW streams of the pipelined schedule: two for small layers (a dW call does not fill the
+        # GPU, so the next layer's can run beside it); one when every dW call fills the GPU by itself
+        # (a second gains ~1.5% at the stress size, and overlapping dW calls blur their per-call
+        # timing)
+        n_dw = args.dw_streams or (1 if T * B * max(sizes[1:L + 1]) >= (1 << 24) else 2)
+        self.dw_extra = [] if args.serial else [torch.cuda.Stream() for _ in range(n_dw - 1)]
         self.ws_dn = None if args.no_dense else snn.workspace(
             max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
         self.ws_gi = snn.workspace(max(snn.snn_sparse_grad_in_workspace(T, B, sizes[l + 1]) for l in range(L + 1)))
@@ -731,8 +736,9 @@ def main():
     ap.add_argument("--schedule", choices=("auto", "pipelined", "layerwise"), default="auto",
                     help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
                          "or layer by layer (auto: pipelined for two or more LIF layers)")
-    ap.add_argument("--dw-streams", type=int, default=2, metavar="N",
-                    help="pipelined schedule: streams the dW calls take in turn, layer by layer (default 2)")
+    ap.add_argument("--dw-streams", type=int, default=0, metavar="N",
+                    help="pipelined schedule: streams the dW calls take in turn, layer by layer (default: 2 for "
+                         "small layers, 1 when a dW call fills the GPU)")
     ap.add_argument("--recompute", type=int, default=0, metavar="K",
                     help="trace recompute: dW rebuilds the input trace from the spikes and checkpoints every K steps")
     ap.add_argument("--graph", action="store_true",

@@ -151,11 +151,12 @@ class Network:
         aux as soon as its eps is there, so the dW calls run back to back beside the chain."""
         main = torch.cuda.current_stream()
         T, B, L = self.T, self.B, self.L
-        if self._aux2 is None:
+        # dW streams taken in turn by layer, so that a layer's dW can start beside the previous
+        # layer's: two for small layers; one when each dW call fills the GPU by itself
+        big = T * B * max(W.shape[1] for W in self.Ws) >= (1 << 24)
+        if not big and self._aux2 is None:
             self._aux2 = torch.cuda.Stream()  # default priority
-        # dW streams taken in turn by layer: a layer's dW starts as soon as its eps is there, not
-        # after the previous layer's dW
-        streams = [aux, self._aux2]
+        streams = [aux] if big else [aux, self._aux2]
         aux.wait_stream(main)  # the active sets are ready: the dW parts that need only them start on aux
         wss = []
         with torch.cuda.stream(aux):
@@ -164,7 +165,8 @@ class Network:
                 ws = snn.workspace(snn.snn_sparse_dw_workspace(T, B, n_in, n_out, csrs[l].capacity), self.X.device)
                 snn.sparse_dw_layout((T, B, n_in), csrs[l], n_out, ws, stream=aux)
                 wss.append(ws)
-        self._aux2.wait_stream(aux)
+        for sd in streams[1:]:
+            sd.wait_stream(aux)
         eps = snn.sparse_grad_in(self.W_out, self.alpha_out, T, B, ro_csr, ro_eps, csrs[L - 1], share_cu=True,
                                  stream=main)
         dWs: List[Optional[torch.Tensor]] = [None] * L
@@ -173,7 +175,7 @@ class Network:
             if reg_coefs is not None:
                 snn.activity_reg_grad(reg_coefs[l], T, eps, csrs[l])
             epss[l] = eps
-            sd = streams[(L - 1 - l) % 2]
+            sd = streams[(L - 1 - l) % len(streams)]
             sd.wait_stream(main)  # eps of layer l is ready
             with torch.cuda.stream(sd):
                 dWs[l] = snn.sparse_dw_prepared(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], wss[l], stream=sd)
