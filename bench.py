@@ -392,12 +392,9 @@ class Runner:
         self.main = torch.cuda.current_stream()
         self.aux = self.main if args.serial else torch.cuda.Stream()  # default priority
         T, B, L, sizes = self.T, self.B, self.L, self.sizes
-        # dW streams of the pipelined schedule: two for small layers (a dW call does not fill the
-        # GPU, so the next layer's can run beside it); one when every dW call fills the GPU by itself
-        # (a second gains ~1.5% at the stress size, and overlapping dW calls blur their per-call
-        # timing)
-        n_dw = args.dw_streams or (1 if T * B * max(sizes[1:L + 1]) >= (1 << 24) else 2)
-        self.dw_extra = [] if args.serial else [torch.cuda.Stream() for _ in range(n_dw - 1)]
+        n_extra = max(1, args.dw_streams - 1)  # extra dW streams the pipelined schedule may take
+        self.dw_extra = [] if args.serial else [torch.cuda.Stream() for _ in range(n_extra)]
+        self.n_dw = 1
         self.ws_dn = None if args.no_dense else snn.workspace(
             max(snn.snn_dense_backward_workspace(T, B, sizes[l], sizes[l + 1]) for l in range(L + 1)))
         self.ws_gi = snn.workspace(max(snn.snn_sparse_grad_in_workspace(T, B, sizes[l + 1]) for l in range(L + 1)))
@@ -418,6 +415,12 @@ class Runner:
         self.net.forward(None if self.args.unfused else b_th)
         csrs = self.net.compact(b_th)
         self.caps = [c.capacity for c in csrs]
+        # dW streams of the pipelined schedule: two when the dW calls are small (one does not fill
+        # the GPU, so the next layer's can run beside it); one when a dW call fills the GPU by itself
+        # (more than ~1e9 multiply-adds: a second stream gains ~1.5% at the stress size at B_th = 0.2
+        # and overlapping dW calls blur their per-call timing)
+        big = max(self.caps[l] * sizes[l] for l in range(L)) >= 10 ** 9
+        self.n_dw = min(1 + len(self.dw_extra), self.args.dw_streams or (1 if big else 2))
         K = self.args.recompute
         if K:  # trace recompute: dW from the input spikes and checkpoints of the trace every K steps
             self.ws_dw = [snn.workspace(snn.snn_sparse_dw_spikes_workspace(T, B, sizes[l], sizes[l + 1],
@@ -516,7 +519,7 @@ class Runner:
         self.cs = cs
         # dW streams taken in turn by layer: a layer's dW starts as soon as its eps is there, not
         # after the previous layer's dW (its final chunk reduction, or a small layer's whole call)
-        dw_streams = [dws] + self.dw_extra
+        dw_streams = ([dws] + self.dw_extra)[:self.n_dw]
         eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
                                                          share_cu=False, ws=self.ws_gi, eps_in=self.eps[L - 1]))
         ev["ro1"].record(main)

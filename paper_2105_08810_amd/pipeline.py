@@ -153,7 +153,7 @@ class Network:
         T, B, L = self.T, self.B, self.L
         # dW streams taken in turn by layer, so that a layer's dW can start beside the previous
         # layer's: two for small layers; one when each dW call fills the GPU by itself
-        big = T * B * max(W.shape[1] for W in self.Ws) >= (1 << 24)
+        big = max(csrs[l].capacity * self.Ws[l].shape[0] for l in range(L)) >= 10 ** 9  # multiply-adds
         if not big and self._aux2 is None:
             self._aux2 = torch.cuda.Stream()  # default priority
         streams = [aux] if big else [aux, self._aux2]
