@@ -109,10 +109,13 @@ class Network:
         """CSR of every LIF layer's active set: from the forward's bitsets when they were marked
         with this b_th, else from V."""
         caps = capacities or [None] * self.L
+        return [self.compact_layer(l, b_th, caps[l]) for l in range(self.L)]
+
+    def compact_layer(self, l, b_th, capacity: Optional[int] = None) -> snn.Csr:
+        """CSR of layer l's active set (as compact())."""
         if self.bits and self.bits_bth == b_th:
-            return [snn.active_compact_bits(self.bits[l], self.V[l], self.theta, self.beta, caps[l])
-                    for l in range(self.L)]
-        return [snn.active_compact(self.V[l], self.theta, b_th, self.beta, caps[l]) for l in range(self.L)]
+            return snn.active_compact_bits(self.bits[l], self.V[l], self.theta, self.beta, capacity)
+        return snn.active_compact(self.V[l], self.theta, b_th, self.beta, capacity)
 
     def activity(self, reg: "Penalty", want_zeta=False):
         """Activity penalties of every LIF layer (App. E) on the forward's spikes.
@@ -394,8 +397,46 @@ class ConvNetwork:
         if ro is None:
             ro = self.readout()
         conv, pool = csrs
-        T, B, H, W, C, F = self.dims
         dW_out, eps_pool = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro[0], ro[1], inp=pool)
+        dWc, eps = self._route_and_filter(conv, pool, eps_pool, ws, reg_coef)
+        return dWc, dW_out, eps
+
+    def compact_and_backward(self, b_th, ro=None, capacities: Optional[List[int]] = None, ws=None, reg_coef=None,
+                             aux_stream=None, events=None):
+        """compact() then sparse_backward(), with the conv layer's compaction on aux_stream beside
+        the pooled entries' compaction and the readout's backward, which need only the pooled
+        entries; the routing to the conv entries waits for both. events: optional dict of timing
+        events, "conv0"/"conv1" recorded around the conv layer's compaction (on its stream) and
+        "pool0"/"pool1" around the pooled entries' compaction. Returns (csrs, (dWc, dW_out, eps))."""
+        mark = (lambda k, st: events[k].record(st)) if events is not None else (lambda k, st: None)
+        if self.bits_bth != b_th:
+            raise ValueError("compact_and_backward(b_th): run forward(b_th) first")
+        if ro is None:
+            ro = self.readout()
+        T, B, H, W, C, F = self.dims
+        caps = capacities or [None, None]
+        main = torch.cuda.current_stream()
+        side = aux_stream if aux_stream is not None else main
+        side.wait_stream(main)
+        with torch.cuda.stream(side):
+            mark("conv0", side)
+            conv = snn.active_compact_bits(self.bits, self.V, self.theta, self.beta, caps[0])
+            mark("conv1", side)
+        mark("pool0", main)
+        snn.snn_pool_route_bits(self.bits, self.arg, T, B, H, W, F, self.pbits)
+        pool = snn.active_compact_bits(self.pbits, None, self.theta, self.beta, caps[1], with_g=False,
+                                       shape=(T, B, self.Np))
+        mark("pool1", main)
+        dW_out, eps_pool = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro[0], ro[1], inp=pool)
+        if side is not main:
+            main.wait_stream(side)
+            conv.record_stream(main)
+        dWc, eps = self._route_and_filter(conv, pool, eps_pool, ws, reg_coef)
+        return [conv, pool], (dWc, dW_out, eps)
+
+    def _route_and_filter(self, conv, pool, eps_pool, ws, reg_coef):
+        """The pooled gradient routed to the conv entries, the penalty term, the filter gradient."""
+        T, B, H, W, C, F = self.dims
         eps = torch.empty(conv.capacity, dtype=torch.float32, device=self.X.device)
         snn.snn_pool_scatter_eps(T, B, H, W, F, pool.row_ptr, pool.col_idx, pool.capacity, eps_pool, self.arg,
                                  conv.row_ptr, conv.col_idx, conv.capacity, eps)
@@ -406,7 +447,7 @@ class ConvNetwork:
             ws = snn.workspace(snn.snn_conv_sparse_dw_workspace(T, B, H, W, C, F), self.X.device)
         snn.snn_conv_sparse_dw(self.trace, T, B, H, W, C, F, conv.row_ptr, conv.col_idx, conv.g, eps, conv.capacity,
                                dWc, ws)
-        return dWc, dW_out, eps
+        return dWc, eps
 
     def dense_backward(self, b_th, ro=None, ws=None, reg_coef=None):
         """The dense chain: dense readout backward, dense routing, dense filter gradient (b_th =

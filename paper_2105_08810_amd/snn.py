@@ -403,6 +403,13 @@ class Csr:
     def nnz(self) -> int:
         return int(self.nnz_dev.item())
 
+    def record_stream(self, stream) -> None:
+        """Mark every buffer as used on stream (for the caching allocator, when the CSR was made on
+        another stream)."""
+        for t in (self.row_ptr, self.col_idx, self.g, self.nnz_dev):
+            if t is not None:
+                t.record_stream(stream)
+
 
 def active_compact(V: torch.Tensor, theta, b_th, beta, capacity: Optional[int] = None, with_g=True) -> Csr:
     """Allocate and run snn_active_compact. Without a capacity it first counts (one host sync)."""

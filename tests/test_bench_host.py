@@ -94,3 +94,32 @@ def test_bench_train_mode_short():
         assert len(line[run]["ce"]) == 20 and all(np.isfinite(line[run]["ce"]))
         assert line[run]["ce"][-1] < line[run]["ce"][0]  # 20 Adam steps lower the loss
     assert len(line["grad_difference_init"]) == 3
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("extra", [[], ["--dw-streams", "1"]])
+def test_bench_pipelined_schedule_matches_layerwise(extra):
+    """The bench's pipelined schedule (dW layouts and calls on dW streams beside the spike-gradient
+    chain) computes the active sets, dW and spike gradients of the layer-by-layer schedule, bit for
+    bit (deep workload: five LIF layers)."""
+    import torch
+    from synth import CONFIGS
+    print(f"\n[case] bench schedules, deep, {extra}", flush=True)
+    runs = []
+    for sched in ("pipelined", "layerwise"):
+        args = bench.build_parser().parse_args(["--workload", "deep", "--no-dense", "--no-cpu", "--schedule", sched]
+                                               + extra)
+        r = bench.Runner(CONFIGS["deep"], args)
+        r.prepare(0.2)
+        cs = r.step(r.events(), dense=False)
+        torch.cuda.synchronize()
+        runs.append((r, cs))
+    (a, ca), (b, cb) = runs
+    assert a.pipelined and not b.pipelined
+    for l in range(a.L):
+        n = cb[l].nnz()
+        assert n > 0 and ca[l].nnz() == n
+        assert torch.equal(ca[l].row_ptr, cb[l].row_ptr) and torch.equal(ca[l].col_idx[:n], cb[l].col_idx[:n])
+        assert torch.equal(a.dW[l], b.dW[l]), f"dW[{l}]"
+        if l < a.L - 1:
+            assert torch.equal(a.eps[l][:n], b.eps[l][:n]), f"eps[{l}]"

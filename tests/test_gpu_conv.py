@@ -193,3 +193,40 @@ def test_conv_train_step(sparse, b_th):
         w_ref, m_ref, v_ref = oracle.adam_update(before[j], g, z, z, 1, *L)
         _, _, bw = _adam_bound(before[j].astype(np.float64), g, z, z, 1, *L, m_ref, v_ref, w_ref)
         assert (np.abs(_np(p) - w_ref) <= bw).all(), j
+
+
+@pytest.mark.parametrize("aux", [True, False])
+def test_conv_overlapped_chain_matches(aux):
+    """compact_and_backward (the conv layer's compaction on a second stream beside the pooled
+    entries' compaction and the readout's backward) gives the active sets and spike gradients of
+    compact() + sparse_backward() bit for bit, and the same weight gradients (float64 sums whose
+    order may differ, rounded to float32)."""
+    print(f"\n[case] conv overlapped chain aux={aux}", flush=True)
+    inp = make_conv_inputs(CONFIGS["conv"], [0, 1, 2, 3])
+    a = float(F32(math.exp(-0.1)))
+    dev = torch.device("cuda")
+    net = pipeline.ConvNetwork(X=torch.from_numpy(inp.X).to(dev), Wc=torch.from_numpy(inp.Wc).to(dev),
+                               W_out=torch.from_numpy(inp.W_out).to(dev), alpha=a, alpha_out=a,
+                               labels=torch.from_numpy(inp.labels).to(dev), loss_mode=0)
+    net.forward(0.2)
+    ro = net.readout()
+    ref_cs = net.compact(0.2)
+    ref = net.sparse_backward(ref_cs, ro)
+    caps = [c.capacity for c in ref_cs]
+    side = torch.cuda.Stream() if aux else None
+    cs, got = net.compact_and_backward(0.2, ro, caps, aux_stream=side)
+    torch.cuda.synchronize()
+    for c, rc, what in ((cs[0], ref_cs[0], "conv"), (cs[1], ref_cs[1], "pool")):
+        n = rc.nnz()
+        assert c.nnz() == n, what
+        assert torch.equal(c.row_ptr, rc.row_ptr), what
+        assert torch.equal(c.col_idx[:n], rc.col_idx[:n]), what
+        if rc.g is not None:
+            assert torch.equal(c.g[:n], rc.g[:n]), what
+    n = ref_cs[0].nnz()
+    assert n > 0
+    assert torch.equal(got[2][:n], ref[2][:n])
+    for x, y, what in ((got[0], ref[0], "dWc"), (got[1], ref[1], "dW_out")):
+        scale = float(y.abs().max())
+        assert scale > 0, what
+        assert torch.allclose(x, y, rtol=1e-6, atol=1e-7 * scale), what
