@@ -376,6 +376,57 @@ def test_full_size_stress_sampled():
         assert not bad.any(), f"dW[{l}]: {int(bad.sum())} elements differ from the dense path"
 
 
+@pytest.mark.parametrize("name,b_th", [("latency", 0.2), ("event", 0.05), ("event", 0.5), ("audio", 0.2),
+                                        ("deep", 0.2)])
+def test_full_size_sampled(name, b_th):
+    """Every other fully connected workload at its full size (B = 256, its own T and widths),
+    through Network.sparse_backward with an auxiliary stream: the launch configuration of the
+    bench (the pipelined schedule for the five-layer network, the readout's spike gradient beside
+    its dW for one LIF layer). Sampled b checked against the oracle run on sample b alone, as for
+    the stress workload: V, spikes, traces, CSR rows and g bit-exact or to float32 rounding, eps
+    of every layer within the envelope; dW, a sum over all samples, against the dense chain."""
+    cfg = CONFIGS[name]
+    print(f"\n[case] full-size {name} b_th={b_th}", flush=True)
+    inp = make_inputs(cfg)
+    net = pipeline.from_inputs(inp).forward()
+    ro = net.readout(dense=True)
+    csrs = net.compact(b_th)
+    dW, dW_out, eps_l = net.sparse_backward(csrs, ro, aux_stream=torch.cuda.Stream())
+    ddW, ddW_out, _ = net.dense_backward(b_th, ro)
+    torch.cuda.synchronize()
+    T, B, L = net.T, net.B, net.L
+    assert B == 256
+    for b in (0, 101, 255):
+        sub = make_inputs(cfg, [b])
+        f = oracle.network_forward(sub.X, sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, np.float32(cfg.theta))
+        args = (sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, sub.labels, cfg.loss_mode, cfg.theta, b_th, cfg.beta)
+        r = oracle.network_backward(f, *args)
+        env = oracle.network_backward(f, *args, absolute=True)
+        assert_bits(_np(net.V_out[:, b]), f["V_out"][:, 0], f"V_out b={b}")
+        for l in range(L):
+            assert_bits(_np(net.V[l][:, b]), f["V"][l][:, 0], f"V[{l}] b={b}")
+            assert_bits(_np(net.S[l][:, b]), f["S"][l][:, 0], f"S[{l}] b={b}")
+            assert_bits(_np(net.trace[l][:, b]), f["trace"][l][:, 0], f"trace[{l}] b={b}")
+            rp = _np(csrs[l].row_ptr).astype(np.int64)
+            rows = np.arange(T) * B + b
+            lo, hi = rp[rows], rp[rows + 1]
+            ref_rp, ref_ci, ref_g = oracle.active_csr(f["V"][l], cfg.theta, b_th, cfg.beta)
+            assert_bits(hi - lo, np.diff(ref_rp).astype(np.int64), f"row counts[{l}] b={b}")
+            idx = np.concatenate([np.arange(a, z) for a, z in zip(lo, hi)] + [np.zeros(0, np.int64)]).astype(np.int64)
+            col = _np(csrs[l].col_idx)[idx].astype(np.int64)
+            assert_bits(col, ref_ci.astype(np.int64), f"col_idx[{l}] b={b}")
+            g = _np(csrs[l].g)[idx].astype(F64)
+            assert np.allclose(g, ref_g, rtol=2e-6, atol=0), f"g[{l}] b={b}"
+            t_of = np.repeat(np.arange(T), hi - lo)
+            got = _np(eps_l[l])[idx].astype(F64)
+            assert_env(got, r["eps"][l][t_of, 0, col] / B, env["eps"][l][t_of, 0, col] / B, f"eps[{l}] b={b}")
+    for x, y, what in [(dW[l], ddW[l], f"dW[{l}]") for l in range(L)] + [(dW_out, ddW_out, "dW_out")]:
+        x, y = _np(x).astype(F64), _np(y).astype(F64)
+        assert np.abs(y).max() > 0, what
+        bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
+        assert not bad.any(), f"{what}: {int(bad.sum())} elements differ from the dense path"
+
+
 def _wide(hidden, n_in, n_ro, T=8, B=2):
     sizes = (n_in, *hidden, n_ro)
     cfg = Config(f"wide{'x'.join(map(str, hidden))}", 204, T=T, B=B, sizes=sizes, tau_ratio_hidden=0.1,
