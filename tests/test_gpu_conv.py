@@ -230,3 +230,59 @@ def test_conv_overlapped_chain_matches(aux):
         scale = float(y.abs().max())
         assert scale > 0, what
         assert torch.allclose(x, y, rtol=1e-6, atol=1e-7 * scale), what
+
+
+def test_conv_full_size_sampled():
+    """The conv workload at its full size (T=100, B=256, 28x28x1, 64 filters) in the bench's launch
+    configuration (the conv layer's compaction beside the readout's backward). Samples are
+    independent up to the weight gradients, so the oracle on sample b alone (its loss gradient
+    scaled by 1/B) fixes sample b's forward (bit for bit), its active entries and the spike
+    gradient at them; the weight gradients, sums over all samples, are checked against the dense
+    chain (itself checked against the oracle on the smaller cases)."""
+    cfg = CONFIGS["conv"]
+    b_th = cfg.b_th
+    print(f"\n[case] conv full size b_th={b_th}", flush=True)
+    inp = make_conv_inputs(cfg)
+    dev = torch.device("cuda")
+    net = pipeline.ConvNetwork(X=torch.from_numpy(inp.X).to(dev), Wc=torch.from_numpy(inp.Wc).to(dev),
+                               W_out=torch.from_numpy(inp.W_out).to(dev), alpha=float(cfg.alpha),
+                               alpha_out=float(cfg.alpha_out), labels=torch.from_numpy(inp.labels).to(dev),
+                               loss_mode=0 if cfg.loss_mode == "max" else 1, theta=float(cfg.theta),
+                               beta=float(cfg.beta))
+    net.forward(b_th)
+    ro = net.readout(dense=True)
+    cs, (dWc, dWo, eps) = net.compact_and_backward(b_th, ro, aux_stream=torch.cuda.Stream())
+    ddWc, ddWo, _ = net.dense_backward(b_th, ro)
+    torch.cuda.synchronize()
+    T, B, H, W, C, Fo = net.dims
+    N = H * W * Fo
+    assert B == 256
+    conv_csr = cs[0]
+    rp = _np(conv_csr.row_ptr).astype(np.int64)
+    for b in (0, 255):
+        sub = make_conv_inputs(cfg, [b])
+        assert np.array_equal(sub.X[:, 0], inp.X[:, b])
+        f = conv.conv_network_forward(sub.X, sub.Wc, sub.W_out, cfg.alpha, cfg.alpha_out, cfg.theta)
+        args = (sub.Wc, sub.W_out, cfg.alpha_out, sub.labels, cfg.loss_mode, cfg.theta, b_th, cfg.beta)
+        r = conv.conv_network_backward(f, *args)
+        env = conv.conv_network_backward(f, *args, absolute=True)
+        _bits_equal(_np(net.V[:, b]), f["V"].reshape(T, 1, N)[:, 0], f"V b={b}")
+        _bits_equal(_np(net.S[:, b]), f["S"].reshape(T, 1, N)[:, 0], f"S b={b}")
+        _bits_equal(_np(net.trace[:, b]), f["trace"].reshape(T, 1, -1)[:, 0], f"trace b={b}")
+        _bits_equal(_np(net.V_out[:, b]), f["V_out"][:, 0], f"V_out b={b}")
+        ref_rp, ref_ci = _csr_from_mask(r["mask"].reshape(T, 1, N))
+        rows = np.arange(T) * B + b
+        lo, hi = rp[rows], rp[rows + 1]
+        _bits_equal(hi - lo, np.diff(ref_rp), f"row counts b={b}")
+        idx = np.concatenate([np.arange(a, z) for a, z in zip(lo, hi)] + [np.zeros(0, np.int64)]).astype(np.int64)
+        col = _np(conv_csr.col_idx)[idx].astype(np.int64)
+        _bits_equal(col, ref_ci, f"col_idx b={b}")
+        t_of = np.repeat(np.arange(T), hi - lo)
+        ref = r["eps"].reshape(T, 1, N)[t_of, 0, col] / B
+        ref_env = env["eps"].reshape(T, 1, N)[t_of, 0, col] / B
+        _env_ok(_np(eps)[idx], ref, ref_env, f"eps at conv entries b={b}")
+    for x, y, what in ((dWc, ddWc, "dWc"), (dWo, ddWo, "dW_out")):
+        x, y = _np(x).astype(np.float64), _np(y).astype(np.float64)
+        assert np.abs(y).max() > 0, what
+        bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
+        assert not bad.any(), f"{what}: {int(bad.sum())} elements differ from the dense chain"
