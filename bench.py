@@ -285,14 +285,16 @@ class ConvRunner:
         T, B, H, W, C, F = self.net.dims
         self.ws_sp = snn.workspace(snn.snn_conv_sparse_dw_workspace(T, B, H, W, C, F))
         self.ws_dn = snn.workspace(snn.snn_conv_dense_dw_workspace(T, B, H, W, C, F))
-        # the conv layer's compaction runs on a second stream beside the pooled entries' compaction
-        # and the readout's backward (--serial: one stream)
+        # --conv-csr: the chain through the conv layer's CSR, its compaction on a second stream
+        # beside the pooled entries' compaction and the readout's backward (--serial: one stream)
         self.aux = None if args.serial else torch.cuda.Stream()  # default priority
 
     def prepare(self, b_th):
         self.b_th = b_th
         self.net.forward(b_th)
-        self.caps = [c.capacity for c in self.net.compact(b_th)]
+        cs = self.net.compact(b_th)
+        self.caps = [c.capacity for c in cs]
+        self.conv_nnz = cs[0].nnz()  # the conv layer's active entries (counted before the timed steps)
 
     def events(self):
         mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
@@ -305,8 +307,12 @@ class ConvRunner:
         net.forward(self.b_th)
         ev["fwd1"].record()
         ro = net.readout(dense=with_dense)
-        ev["cmp0"].record()  # the sparse chain: compaction (partly beside the readout's backward) to dWc
-        cs, _ = net.compact_and_backward(self.b_th, ro, self.caps, ws=self.ws_sp, aux_stream=self.aux, events=ev)
+        ev["cmp0"].record()  # the sparse chain: compaction to dWc
+        if self.args.conv_csr:
+            cs, _ = net.compact_and_backward(self.b_th, ro, self.caps, ws=self.ws_sp, aux_stream=self.aux, events=ev)
+        else:
+            pool, _ = net.pooled_backward(self.b_th, ro, self.caps[1], ws=self.ws_sp, events=ev)
+            cs = [None, pool]
         ev["bw1"].record()
         if with_dense:
             ev["dn0"].record()
@@ -330,18 +336,26 @@ class ConvRunner:
         med = lambda a: float(np.median(a))  # noqa: E731
         span = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in evs])  # noqa: E731
         T, B, H, W, C, F = self.net.dims
-        t_cmp = span("conv0", "conv1") + span("pool0", "pool1")  # the compaction kernels' own spans
+        csr_chain = self.args.conv_csr
+        # the compaction kernels' own spans
+        t_cmp = (span("conv0", "conv1") if csr_chain else 0.0) + span("pool0", "pool1")
         t_sparse = span("cmp0", "bw1")
         with_dense = dense and not self.args.no_dense
-        nnz = cs[0].nnz()
+        nnz = cs[0].nnz() if csr_chain else self.conv_nnz
         nnz_pool = cs[1].nnz()
         N = H * W * F
         TB = T * B
-        # gathered bytes: compaction (bitset, CSR, g, V at active entries), pooled bits and CSR,
-        # readout backward at the pooled entries, routing, the filter gradient (entries and the
-        # input patches of entries with a gradient)
-        sparse_bytes = (TB * ((B * N + 63) // 64) // B * 8 + 12 * nnz + 4 * (TB + 1) + 2 * TB * self.net.Np
-                        + 8 * nnz_pool + 4 * (TB + 1) + 12 * nnz)
+        Np = self.net.Np
+        bits = TB * ((B * N + 63) // 64) // B * 8
+        # gathered bytes: pooled bits (conv bitset and picks read, pooled bitset written) and CSR,
+        # the readout's backward at the pooled entries; then either the filter gradient from the
+        # pooled entries (their picks, V, eps and 3x3xC input patches) or the conv layer's
+        # compaction (bitset, CSR, g, V at active entries), routing and the filter gradient from it
+        sparse_bytes = bits + TB * Np + TB * Np // 8 + 4 * (TB + 1) + 4 * nnz_pool + 2 * TB * Np
+        if csr_chain:
+            sparse_bytes += bits + 12 * nnz + 4 * (TB + 1) + 4 * nnz_pool + 12 * nnz
+        else:
+            sparse_bytes += nnz_pool * (4 + 4 + 1 + 4 + 36 * C)
         out = {
             "metric": "sparse backward ms/batch + active neuron-steps/s, speedup vs dense BPTT",
             "value": nnz / (med(t_sparse) * 1e-3),
@@ -353,7 +367,9 @@ class ConvRunner:
             "sparse_backward_ms": med(t_sparse),
             "sparse_backward_ms_iqr": [float(np.percentile(t_sparse, 25)), float(np.percentile(t_sparse, 75))],
             "compaction_ms": med(t_cmp),
-            "compaction_overlapped": self.aux is not None,
+            "sparse_chain": ("conv-layer CSR (its compaction beside the readout's backward), routing, filter gradient"
+                             if csr_chain else "pooled entries only: readout backward, filter gradient of the picked "
+                             "conv neurons (no conv-layer compaction)"),
             "dense_backward_ms": med(span("dn0", "dn1")) if with_dense else None,
             "forward_ms": med(span("fwd0", "fwd1")),
             "active_fraction": [nnz / (TB * N)],
@@ -361,7 +377,7 @@ class ConvRunner:
             "nnz": [nnz],
             "sparse_backward_gathered_bytes": sparse_bytes,
             "sparse_backward_hbm_frac": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "memory_sparse_dense_bytes": [12 * nnz + 4 * (TB + 1) + 12 * nnz_pool + 4 * (TB + 1),
+            "memory_sparse_dense_bytes": [(12 * nnz + 4 * (TB + 1) if csr_chain else 0) + 8 * nnz_pool + 4 * (TB + 1),
                                           4 * TB * N + 4 * TB * self.net.Np],
             "wall_s_timed": wall,
         }
@@ -732,6 +748,9 @@ def build_parser() -> argparse.ArgumentParser:
     ap.add_argument("--cpu-samples", type=int, default=16)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--serial", action="store_true", help="everything on one stream")
+    ap.add_argument("--conv-csr", action="store_true",
+                    help="conv workload: the sparse chain through the conv layer's CSR and routing instead of the "
+                         "pooled entries alone")
     ap.add_argument("--unfused", action="store_true",
                     help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")

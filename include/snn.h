@@ -375,6 +375,25 @@ snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, int H, int W,
                               size_t workspace_bytes, void* stream);
 
 /*
+ * The same filter gradient from the pooled CSR alone, for a conv layer whose spikes reach the
+ * loss only through the 2x2 pooling (no other term on the conv spikes, such as the activity
+ * penalty): then an active conv neuron has a nonzero gradient only where its pooling picked it
+ * for an active pooled entry, and those are exactly the pooled CSR's entries (snn_pool_route_bits
+ * and compaction). Pooled entry (t,b,np) with gradient eps_pool stands for conv neuron
+ * (t,b,2 py + arg/2, 2 px + arg%2, f) (np = (py (W/2) + px) F + f, arg from snn_maxpool_spikes),
+ * G = eps_pool * g(V) there, g = 1/(beta |V - theta| + 1)^2 with the compaction's float32
+ * operations and G = 0 outside |V - theta| < b_th. No conv-layer CSR and no routing call are
+ * needed. V [T,B,H*W*F] float32, arg [T,B,(H/2)*(W/2)*F] uint8 (read). Workspace, dWc, errors
+ * and accumulation as snn_conv_sparse_dw (SNN_ERR_INVALID_ARG also for a NaN theta, b_th or
+ * beta, or a negative b_th or beta). Columns outside [0, (H/2)*(W/2)*F) are ignored.
+ */
+snn_status snn_conv_sparse_dw_pooled(const float* trace_in, const float* V, const uint8_t* arg, int T, int B, int H,
+                                     int W, int C, int F, float theta, float b_th, float beta,
+                                     const int32_t* pool_row_ptr, const int32_t* pool_col_idx, const float* eps_pool,
+                                     int64_t pool_cap, float* dWc, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
+/*
  * Dense filter gradient (the baseline): every neuron's G = eps_conv * g(V) * [|V - theta| < b_th]
  * (b_th = +INFINITY: full surrogate) with eps_conv dense [T,B,H*W*F], then the same sum.
  * SNN_ERR_UNSUPPORTED when C*F > 2^20.

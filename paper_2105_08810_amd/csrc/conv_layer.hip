@@ -300,15 +300,30 @@ __global__ void scatter_dense_kernel(const float* __restrict__ eps_p, const uint
   }
 }
 
+// Parameters of the pooled form of the sparse filter gradient.
+struct PooledArgs {
+  const float* V;      // conv layer's V [T*B][H*W*F]
+  const uint8_t* arg;  // pooling's pick [T*B][(H/2)*(W/2)*F]
+  float theta, b_th, beta;
+};
+
+// Surrogate derivative, with the float32 operations of the compaction (no contraction).
+__device__ __forceinline__ float surrogate_g(float v, float theta, float beta) {
+  const float x = __fadd_rn(__fmul_rn(beta, fabsf(v - theta)), 1.0f);
+  return 1.0f / __fmul_rn(x, x);
+}
+
 // Sparse filter gradient: blocks take contiguous row ranges, wavefronts rows, lanes the row's
 // entries; an entry with G = eps * g != 0 adds G * trace over its 3x3xC input patch into the
 // block's float64 accumulator [9 * C][F] in LDS. Each block writes its sums; a fixed-order
-// reduction over blocks gives dWc.
-template <int CT>  // CT > 0: C == CT and the patch's loads are issued together; 0: any C
+// reduction over blocks gives dWc. POOLED: the entries are the pooled CSR's, each standing for
+// the conv neuron its pooling picked (window position arg), with G = eps_pooled * g(V) there
+// (zero outside the band).
+template <int CT, bool POOLED>  // CT > 0: C == CT and the patch's loads are issued together; 0: any C
 __global__ __launch_bounds__(kCsdThreads) void conv_dw_sparse_kernel(
     const float* __restrict__ trace, int TB, int H, int W, int C, int F, const int32_t* __restrict__ rp,
     const int32_t* __restrict__ col, const float* __restrict__ g, const float* __restrict__ eps, int64_t cap,
-    int rows_per_block, double* __restrict__ part) {
+    int rows_per_block, double* __restrict__ part, PooledArgs pa) {
   extern __shared__ double cacc[];  // [9 * C * F]
   const int nacc = 9 * C * F;
   for (int i = threadIdx.x; i < nacc; i += kCsdThreads) cacc[i] = 0.0;
@@ -324,8 +339,24 @@ __global__ __launch_bounds__(kCsdThreads) void conv_dw_sparse_kernel(
     for (int64_t e = e0 + lane_id(); e < e1; e += kWave) {
       // the entry's column and gradient loads go out together; a bad column or a zero gradient
       // is masked, not branched on, so the patch loads below are not held back either
-      const int n = col[e];
-      const float G0 = g ? eps[e] * g[e] : eps[e];
+      int n;
+      float G0;
+      if (POOLED) {
+        const int Np = (H / 2) * (W / 2) * F;
+        const int p = col[e];
+        const bool pv = (unsigned)p < (unsigned)Np;
+        const int pc = pv ? p : 0;
+        const int a = pa.arg[(int64_t)r * Np + pc] & 3;
+        const int q = pc / F;
+        const int yy = 2 * (q / (W / 2)) + (a >> 1);
+        const int xx = 2 * (q % (W / 2)) + (a & 1);
+        n = pv ? (yy * W + xx) * F + (pc - q * F) : -1;
+        const float v = pa.V[(int64_t)r * N + (pv ? n : 0)];
+        G0 = fabsf(v - pa.theta) < pa.b_th ? eps[e] * surrogate_g(v, pa.theta, pa.beta) : 0.0f;
+      } else {
+        n = col[e];
+        G0 = g ? eps[e] * g[e] : eps[e];
+      }
       const bool ok = (unsigned)n < (unsigned)N && G0 != 0.0f;
       const int nc = ok ? n : 0;
       const double G = (double)G0;
@@ -624,14 +655,47 @@ extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, in
   const int nacc = 9 * C * F;
   double* part = static_cast<double*>(workspace);
   const size_t lds = (size_t)nacc * sizeof(double);
+  const PooledArgs none{nullptr, nullptr, 0.0f, 0.0f, 0.0f};
   auto launch = [&](auto kernel) {
     (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCsdThreads), lds, s, trace_in, TB, H, W, C, F, conv_row_ptr,
-                       conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part);
+                       conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part, none);
   };
-  if (C == 1) launch(conv_dw_sparse_kernel<1>);
-  else if (C == 2) launch(conv_dw_sparse_kernel<2>);
-  else launch(conv_dw_sparse_kernel<0>);
+  if (C == 1) launch(conv_dw_sparse_kernel<1, false>);
+  else if (C == 2) launch(conv_dw_sparse_kernel<2, false>);
+  else launch(conv_dw_sparse_kernel<0, false>);
+  hipLaunchKernelGGL(reduce_parts, dim3((unsigned)nacc), dim3(256), 0, s, part, nb, nacc, dWc);
+  return launch_status();
+}
+
+extern "C" snn_status snn_conv_sparse_dw_pooled(const float* trace_in, const float* V, const uint8_t* arg, int T,
+                                                int B, int H, int W, int C, int F, float theta, float b_th,
+                                                float beta, const int32_t* pool_row_ptr,
+                                                const int32_t* pool_col_idx, const float* eps_pool,
+                                                int64_t pool_cap, float* dWc, void* workspace,
+                                                size_t workspace_bytes, void* stream) {
+  if (!trace_in || !V || !arg || !pool_row_ptr || !dWc || !workspace) return SNN_ERR_INVALID_ARG;
+  if (pool_cap < 0 || (pool_cap > 0 && (!pool_col_idx || !eps_pool))) return SNN_ERR_INVALID_ARG;
+  if (!conv_dims_ok(T, B, H, W, F) || bad_dim(C) || too_big(T, B, H * W * C)) return SNN_ERR_INVALID_ARG;
+  if (isnan(theta) || isnan(b_th) || b_th < 0.0f || isnan(beta) || beta < 0.0f) return SNN_ERR_INVALID_ARG;
+  if (C * F > 2048) return SNN_ERR_UNSUPPORTED;
+  if (workspace_bytes < snn_conv_sparse_dw_workspace(T, B, H, W, C, F)) return SNN_ERR_INVALID_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int TB = T * B;
+  const int nb = cdw_blocks(TB, 9 * C * F);
+  const int rpb = (TB + nb - 1) / nb;
+  const int nacc = 9 * C * F;
+  double* part = static_cast<double*>(workspace);
+  const size_t lds = (size_t)nacc * sizeof(double);
+  const PooledArgs pa{V, arg, theta, b_th, beta};
+  auto launch = [&](auto kernel) {
+    (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCsdThreads), lds, s, trace_in, TB, H, W, C, F, pool_row_ptr,
+                       pool_col_idx, nullptr, eps_pool, pool_cap, rpb, part, pa);
+  };
+  if (C == 1) launch(conv_dw_sparse_kernel<1, true>);
+  else if (C == 2) launch(conv_dw_sparse_kernel<2, true>);
+  else launch(conv_dw_sparse_kernel<0, true>);
   hipLaunchKernelGGL(reduce_parts, dim3((unsigned)nacc), dim3(256), 0, s, part, nb, nacc, dWc);
   return launch_status();
 }

@@ -434,6 +434,33 @@ class ConvNetwork:
         dWc, eps = self._route_and_filter(conv, pool, eps_pool, ws, reg_coef)
         return [conv, pool], (dWc, dW_out, eps)
 
+    def pooled_backward(self, b_th, ro=None, pool_capacity: Optional[int] = None, ws=None, events=None):
+        """The sparse backward from the pooled entries alone, for a loss that reaches the conv
+        spikes only through the pooling (no activity penalty): the pooled entries' compaction, the
+        readout's backward at them, and the filter gradient of the conv neurons the pooling picked
+        (snn_conv_sparse_dw_pooled); every other conv neuron, active or not, has a zero gradient,
+        so no conv-layer compaction and no routing are needed. events: optional dict of timing
+        events, "pool0"/"pool1" recorded around the pooled entries' compaction. Returns
+        (pooled CSR, (dWc, dW_out, eps at the pooled entries))."""
+        if self.bits_bth != b_th:
+            raise ValueError("pooled_backward(b_th): run forward(b_th) first")
+        mark = (lambda k: events[k].record()) if events is not None else (lambda k: None)
+        if ro is None:
+            ro = self.readout()
+        T, B, H, W, C, F = self.dims
+        mark("pool0")
+        snn.snn_pool_route_bits(self.bits, self.arg, T, B, H, W, F, self.pbits)
+        pool = snn.active_compact_bits(self.pbits, None, self.theta, self.beta, pool_capacity, with_g=False,
+                                       shape=(T, B, self.Np))
+        mark("pool1")
+        dW_out, eps_pool = snn.sparse_backward(self.W_out, self.trace_out, self.alpha_out, ro[0], ro[1], inp=pool)
+        dWc = torch.empty_like(self.Wc)
+        if ws is None:
+            ws = snn.workspace(snn.snn_conv_sparse_dw_workspace(T, B, H, W, C, F), self.X.device)
+        snn.snn_conv_sparse_dw_pooled(self.trace, self.V, self.arg, T, B, H, W, C, F, self.theta, b_th, self.beta,
+                                      pool.row_ptr, pool.col_idx, eps_pool, pool.capacity, dWc, ws)
+        return pool, (dWc, dW_out, eps_pool)
+
     def _route_and_filter(self, conv, pool, eps_pool, ws, reg_coef):
         """The pooled gradient routed to the conv entries, the penalty term, the filter gradient."""
         T, B, H, W, C, F = self.dims

@@ -64,6 +64,8 @@ _SIGNATURES = {
     "snn_pool_scatter_eps_dense": (_I, [_P, _P, _I, _I, _I, _I, _I, _P, _P]),
     "snn_conv_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I, _I]),
     "snn_conv_sparse_dw": (_I, [_P, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_conv_sparse_dw_pooled": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ,
+                                       _P]),
     "snn_conv_dense_dw_workspace": (_SZ, [_I, _I, _I, _I, _I, _I]),
     "snn_conv_dense_dw": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _F, _F, _P, _P, _SZ, _P]),
 }
@@ -368,6 +370,15 @@ def snn_conv_sparse_dw(trace_in, T, B, H, W, C, F, conv_row_ptr, conv_col_idx, c
         _ptr(conv_col_idx, torch.int32, "conv_col_idx"), _ptr(conv_g, torch.float32, "conv_g"),
         _ptr(eps_conv, torch.float32, "eps_conv"), int(conv_cap), _ptr(dWc, torch.float32, "dWc"),
         _ptr(ws, None, "workspace"), _nbytes(ws), _stream(stream)))
+
+
+def snn_conv_sparse_dw_pooled(trace_in, V, arg, T, B, H, W, C, F, theta, b_th, beta, pool_row_ptr, pool_col_idx,
+                              eps_pool, pool_cap, dWc, ws, stream=None):
+    _check("snn_conv_sparse_dw_pooled", lib().snn_conv_sparse_dw_pooled(
+        _ptr(trace_in, torch.float32, "trace_in"), _ptr(V, torch.float32, "V"), _ptr(arg, torch.uint8, "arg"),
+        T, B, H, W, C, F, float(theta), float(b_th), float(beta), _ptr(pool_row_ptr, torch.int32, "pool_row_ptr"),
+        _ptr(pool_col_idx, torch.int32, "pool_col_idx"), _ptr(eps_pool, torch.float32, "eps_pool"), int(pool_cap),
+        _ptr(dWc, torch.float32, "dWc"), _ptr(ws, None, "workspace"), _nbytes(ws), _stream(stream)))
 
 
 def snn_conv_dense_dw_workspace(T, B, H, W, C, F) -> int:

@@ -329,6 +329,14 @@ def test_conv_entry_points_reject(lib):
     assert lib.snn_conv_sparse_dw(FAKE, 10, 4, 8, 8, 1, 64, FAKE, None, FAKE, FAKE, 100, FAKE, FAKE, ws, None) == E
     assert lib.snn_conv_sparse_dw(FAKE, 10, 4, 8, 8, 64, 64, FAKE, FAKE, FAKE, FAKE, 100, FAKE, FAKE, 1 << 40,
                                   None) == snn.SNN_ERR_UNSUPPORTED
+    pooled = lambda **kw: lib.snn_conv_sparse_dw_pooled(  # noqa: E731
+        FAKE, kw.get("v", FAKE), kw.get("arg", FAKE), 10, 4, kw.get("H", 8), 8, kw.get("C", 1), 64,
+        kw.get("theta", 1.0), kw.get("b_th", 0.2), kw.get("beta", 100.0), FAKE, kw.get("col", FAKE), FAKE,
+        kw.get("cap", 100), FAKE, FAKE, kw.get("ws", ws), None)
+    for kw in ({"v": None}, {"arg": None}, {"col": None}, {"cap": -1}, {"H": 7}, {"theta": math.nan},
+               {"b_th": -1.0}, {"b_th": math.nan}, {"beta": -1.0}, {"ws": 8}):
+        assert pooled(**kw) == E, kw
+    assert pooled(C=64, ws=1 << 40) == snn.SNN_ERR_UNSUPPORTED
     wd = lib.snn_conv_dense_dw_workspace(10, 4, 8, 8, 1, 64)
     assert wd > 0 and lib.snn_conv_dense_dw_workspace(10, 4, 7, 8, 1, 64) == 0
     assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 1, 64, 1.0, NAN, 100.0, FAKE, FAKE, wd, None) == E

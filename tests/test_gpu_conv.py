@@ -252,8 +252,10 @@ def test_conv_full_size_sampled():
     net.forward(b_th)
     ro = net.readout(dense=True)
     cs, (dWc, dWo, eps) = net.compact_and_backward(b_th, ro, aux_stream=torch.cuda.Stream())
+    pool, (pdWc, pdWo, peps) = net.pooled_backward(b_th, ro)
     ddWc, ddWo, _ = net.dense_backward(b_th, ro)
     torch.cuda.synchronize()
+    assert torch.equal(pool.row_ptr, cs[1].row_ptr) and torch.equal(pdWo, dWo)
     T, B, H, W, C, Fo = net.dims
     N = H * W * Fo
     assert B == 256
@@ -281,8 +283,50 @@ def test_conv_full_size_sampled():
         ref = r["eps"].reshape(T, 1, N)[t_of, 0, col] / B
         ref_env = env["eps"].reshape(T, 1, N)[t_of, 0, col] / B
         _env_ok(_np(eps)[idx], ref, ref_env, f"eps at conv entries b={b}")
-    for x, y, what in ((dWc, ddWc, "dWc"), (dWo, ddWo, "dW_out")):
+    for x, y, what in ((dWc, ddWc, "dWc"), (dWo, ddWo, "dW_out"), (pdWc, ddWc, "dWc from the pooled entries")):
         x, y = _np(x).astype(np.float64), _np(y).astype(np.float64)
         assert np.abs(y).max() > 0, what
         bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
         assert not bad.any(), f"{what}: {int(bad.sum())} elements differ from the dense chain"
+
+
+@pytest.mark.parametrize("case", ["small", "small_inf", "ragged", "degenerate", "workload"])
+def test_conv_pooled_chain(case):
+    """The filter gradient from the pooled entries alone (snn_conv_sparse_dw_pooled: no conv-layer
+    CSR, no routing) against the oracle, and against the conv-CSR chain: the same pooled CSR and
+    readout gradients bit for bit, dWc to float64 summation order."""
+    print(f"\n[case] conv pooled chain {case}", flush=True)
+    b_th = {"small_inf": math.inf, "ragged": 0.3, "degenerate": 0.4}.get(case, 0.2)
+    if case == "workload":
+        inp = make_conv_inputs(CONFIGS["conv"], [0, 1, 2, 3])
+        X, Wc, Wo, y = inp.X, inp.Wc, inp.W_out, inp.labels
+    elif case == "ragged":
+        X, Wc, Wo, y = _small(T=17, B=3, H=6, W=10, C=2, Fo=40, Cls=3, rate=0.1, sigma=0.7, seed=4)
+    elif case == "degenerate":
+        X, Wc, Wo, y = _small(T=5, B=2, H=2, W=4, C=3, Fo=8, Cls=2, rate=0.5, sigma=1.5, seed=13)
+    else:
+        X, Wc, Wo, y = _small()
+    a = F32(math.exp(-0.1))
+    f = conv.conv_network_forward(X, Wc, Wo, a, a)
+    r = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, b_th, 100.0)
+    env = conv.conv_network_backward(f, Wc, Wo, a, y, "max", 1.0, b_th, 100.0, absolute=True)
+    dev = torch.device("cuda")
+    net = pipeline.ConvNetwork(X=torch.from_numpy(X).to(dev), Wc=torch.from_numpy(Wc).to(dev),
+                               W_out=torch.from_numpy(Wo).to(dev), alpha=float(a), alpha_out=float(a),
+                               labels=torch.from_numpy(y).to(dev), loss_mode=0)
+    net.forward(b_th)
+    ro = net.readout()
+    csrs = net.compact(b_th)
+    dWc, dWo, _ = net.sparse_backward(csrs, ro)
+    pool, (pdWc, pdWo, peps) = net.pooled_backward(b_th, ro)
+    torch.cuda.synchronize()
+    n = csrs[1].nnz()
+    assert pool.nnz() == n and torch.equal(pool.row_ptr, csrs[1].row_ptr)
+    assert torch.equal(pool.col_idx[:n], csrs[1].col_idx[:n])
+    assert torch.equal(pdWo, dWo)
+    _env_ok(_np(pdWc), r["dWc"], env["dWc"], "dWc from the pooled entries")
+    _env_ok(_np(pdWo), r["dW_out"], env["dW_out"], "dW_out")
+    scale = float(dWc.abs().max())
+    assert torch.allclose(pdWc, dWc, rtol=1e-6, atol=1e-7 * scale)
+    if case != "degenerate":
+        assert np.abs(r["dWc"]).max() > 0
