@@ -41,10 +41,10 @@ struct DwPlan {
   size_t lds;
 };
 
-DwPlan plan_dw(int T, int B, int N_in, int N_out) {
+DwPlan plan_dw_slab(int T, int B, int N_in, int N_out, int slab_cap) {
   DwPlan p{};
   const int TB = T * B;
-  p.n_slabs = (N_out + kSlab - 1) / kSlab;
+  p.n_slabs = (N_out + slab_cap - 1) / slab_cap;
   p.slab = (N_out + p.n_slabs - 1) / p.n_slabs;
   p.lds = (size_t)p.slab * kLd * sizeof(double);
   p.n_itiles = (N_in + kItile - 1) / kItile;
@@ -57,6 +57,15 @@ DwPlan plan_dw(int T, int B, int N_in, int N_out) {
   nc = std::max(nc, 1);
   p.rows_per_chunk = (TB + nc - 1) / nc;
   p.n_chunks = (TB + p.rows_per_chunk - 1) / p.rows_per_chunk;
+  return p;
+}
+
+// Slabs of up to 128 outputs (one block per CU); a layer whose grid would then give fewer than
+// two blocks per CU (small T B or few tiles: latency-bound, not LDS-atomic-bound) takes slabs of
+// half that, two blocks per CU, twice the loads in flight.
+DwPlan plan_dw(int T, int B, int N_in, int N_out) {
+  const DwPlan p = plan_dw_slab(T, B, N_in, N_out, kSlab);
+  if ((int64_t)p.n_itiles * p.n_slabs * p.n_chunks < 2 * kAssumedCUs) return plan_dw_slab(T, B, N_in, N_out, kSlab / 2);
   return p;
 }
 
