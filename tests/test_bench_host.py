@@ -123,3 +123,23 @@ def test_bench_pipelined_schedule_matches_layerwise(extra):
         assert torch.equal(a.dW[l], b.dW[l]), f"dW[{l}]"
         if l < a.L - 1:
             assert torch.equal(a.eps[l][:n], b.eps[l][:n]), f"eps[{l}]"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("extra", [[], ["--conv-csr", "--no-dense"]])
+def test_bench_line_on_conv(extra):
+    """The conv workload's bench line (pooled-entry chain by default, the conv-CSR chain with
+    --conv-csr): the contract's keys, positive timings, the same active-entry counts either way."""
+    print(f"\n[case] bench conv {extra}", flush=True)
+    r = _run(["--workload", "conv", "--steps", "2", "--warmup", "1", "--no-cpu"] + extra)
+    assert r.returncode == 0, r.stderr[-2000:]
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "config", "sparse_backward_ms",
+              "compaction_ms", "sparse_chain", "nnz", "pooled_active_entries", "memory_saved_pct"):
+        assert k in line, k
+    assert line["config"]["workload"].startswith("conv")
+    assert line["value"] > 0 and line["sparse_backward_ms"] > 0 and line["compaction_ms"] > 0
+    assert line["nnz"][0] > line["pooled_active_entries"] > 0
+    assert ("conv-layer CSR" in line["sparse_chain"]) == ("--conv-csr" in extra)
+    if "--no-dense" not in extra:
+        assert line["dense_backward_ms"] > 0 and line["speedup_vs_dense"] > 1
