@@ -290,13 +290,13 @@ def test_conv_full_size_sampled():
         assert not bad.any(), f"{what}: {int(bad.sum())} elements differ from the dense chain"
 
 
-@pytest.mark.parametrize("case", ["small", "small_inf", "ragged", "degenerate", "workload"])
+@pytest.mark.parametrize("case", ["small", "small_inf", "ragged", "degenerate", "workload", "empty_band"])
 def test_conv_pooled_chain(case):
     """The filter gradient from the pooled entries alone (snn_conv_sparse_dw_pooled: no conv-layer
     CSR, no routing) against the oracle, and against the conv-CSR chain: the same pooled CSR and
     readout gradients bit for bit, dWc to float64 summation order."""
     print(f"\n[case] conv pooled chain {case}", flush=True)
-    b_th = {"small_inf": math.inf, "ragged": 0.3, "degenerate": 0.4}.get(case, 0.2)
+    b_th = {"small_inf": math.inf, "ragged": 0.3, "degenerate": 0.4, "empty_band": 0.0}.get(case, 0.2)
     if case == "workload":
         inp = make_conv_inputs(CONFIGS["conv"], [0, 1, 2, 3])
         X, Wc, Wo, y = inp.X, inp.Wc, inp.W_out, inp.labels
@@ -328,5 +328,7 @@ def test_conv_pooled_chain(case):
     _env_ok(_np(pdWo), r["dW_out"], env["dW_out"], "dW_out")
     scale = float(dWc.abs().max())
     assert torch.allclose(pdWc, dWc, rtol=1e-6, atol=1e-7 * scale)
-    if case != "degenerate":
+    if case == "empty_band":  # no active conv neuron: no pooled entry, a zero filter gradient
+        assert n == 0 and not pdWc.any()
+    elif case != "degenerate":
         assert np.abs(r["dWc"]).max() > 0
