@@ -135,11 +135,13 @@ def test_bench_line_on_conv(extra):
     assert r.returncode == 0, r.stderr[-2000:]
     line = json.loads(r.stdout.strip().splitlines()[-1])
     for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "config", "sparse_backward_ms",
-              "compaction_ms", "sparse_chain", "nnz", "pooled_active_entries", "memory_saved_pct"):
+              "compaction_ms", "sparse_chain", "nnz", "pooled_active_entries", "memory_saved_pct", "roofline"):
         assert k in line, k
     assert line["config"]["workload"].startswith("conv")
     assert line["value"] > 0 and line["sparse_backward_ms"] > 0 and line["compaction_ms"] > 0
     assert line["nnz"][0] > line["pooled_active_entries"] > 0
     assert ("conv-layer CSR" in line["sparse_chain"]) == ("--conv-csr" in extra)
+    rl = line["roofline"]
+    assert rl["bound"] == "hbm" and 0 < rl["frac"] < 1 and math.isclose(rl["frac"], rl["achieved"] / rl["peak"])
     if "--no-dense" not in extra:
         assert line["dense_backward_ms"] > 0 and line["speedup_vs_dense"] > 1
