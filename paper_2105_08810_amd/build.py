@@ -23,6 +23,7 @@ SOURCES = [
     "active_compact.hip",
     "lif_forward.hip",
     "sparse_backward.hip",
+    "dw_mfma.hip",
     "dense_backward.hip",
     "readout_ce.hip",
     "train_step.hip",

@@ -45,6 +45,20 @@ struct Carve {
 // Number of compute units of the current device (cached per process and device).
 int cu_count();
 
+// Sparse dW on the matrix cores (dw_mfma.hip), for 32 < N_out <= 1024 and N_in % 4 == 0.
+struct MdwPlan {
+  int n_win, n_itiles, n_chunks, wpc;  // windows of rows, input tiles, chunks of windows, windows per chunk
+};
+bool mdw_eligible(int T, int B, int N_in, int N_out);
+MdwPlan plan_mdw(int T, int B, int N_in, int N_out);
+size_t mdw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap);
+// Structure-only part: sorts each window's entries by column quad into the workspace.
+void mdw_enqueue_layout(int T, int B, int N_in, int N_out, const int32_t* out_row_ptr, const int32_t* out_col_idx,
+                        int64_t out_cap, void* workspace, hipStream_t s);
+// The rest (needs eps): G into the sorted entries, the accumulation, the chunk reduction into dW.
+void mdw_enqueue_rest(const float* trace_in, int T, int B, int N_in, int N_out, const float* out_g, const float* eps_out,
+                      int64_t out_cap, float* dW, void* workspace, hipStream_t s);
+
 // Exclusive scan of counts[0..n) into out[0..n] (out[n] = total) and *total64 = total.
 // temp must hold scan_temp_elems(n) int32 values.
 size_t scan_temp_elems(int n);

@@ -1,8 +1,9 @@
 """Trace recompute (snn_trace_checkpoints + snn_sparse_dw_spikes) on the GPU.
 
 The checkpoints equal the forward's stored input trace at every K-th step bit for bit; dW
-computed from the spikes and checkpoints equals dW computed from the stored trace (same CSR) up
-to the float64 accumulation order, and stays within the oracle's envelope. Cases cover sample
+computed from the spikes and checkpoints (float64 accumulation) equals dW computed from the stored
+trace (same CSR; float32 accumulation per chunk of rows on the matrix cores) within 3e-5 of the
+error envelope sum |G| trace, and stays within the oracle's envelope. Cases cover sample
 counts that are not multiples of 8 or 128, step counts that are not multiples of K, K = 1, K > T,
 narrow and wide layers, and the stress workload's layers at full size.
 """
@@ -42,7 +43,7 @@ def _layers(net, csrs, epss, K):
         n_out = net.Ws[l].shape[1]
         ref = snn.sparse_dw(net.trace[l], csrs[l], epss[l], n_out)
         got = snn.sparse_dw_spikes(s_in, ck, K, net.alphas[l], csrs[l], epss[l], n_out)
-        out.append((ref, got, ck))
+        out.append((ref, got, ck, _env(net.trace[l], csrs[l], epss[l], n_out)))
     torch.cuda.synchronize()
     return out
 
@@ -56,9 +57,16 @@ def _check_ck(net, ck, l, K):
     assert same.all(), f"checkpoints of layer {l}: {int((~same).sum())} differ"
 
 
-def _check_dw(ref, got, what):
+def _env(trace, csr, eps, n_out):
+    """The error envelope sum |G| trace of a dW (g >= 0 and traces >= 0: the same sparse dW of |eps|)."""
+    return snn.sparse_dw(trace, csr, eps.abs(), n_out)
+
+
+def _check_dw(ref, got, env, what):
+    """Two float32 sums of the same terms: within 3e-5 of the envelope (a float32 sum of n terms is
+    within about n 2^-24 of it; the stored-trace dW sums at most a few hundred terms per chunk)."""
     x, y = _np(got).astype(np.float64), _np(ref).astype(np.float64)
-    bad = np.abs(x - y) > 2e-6 * np.abs(y) + 1e-7 * np.abs(y).max() + 1e-30
+    bad = np.abs(x - y) > 3e-5 * _np(env).astype(np.float64) + 1e-30
     assert not bad.any(), f"{what}: {int(bad.sum())} of {bad.size} differ from the stored-trace dW"
 
 
@@ -76,9 +84,9 @@ def test_recompute_matches_stored_trace_and_oracle(T, B, sizes, K):
     args = (inp.Ws, inp.W_out, inp.alphas, inp.alpha_out, inp.labels, cfg.loss_mode, cfg.theta, 0.4, cfg.beta)
     r = oracle.network_backward(f, *args)
     env = oracle.network_backward(f, *args, absolute=True)
-    for l, (ref, got, ck) in enumerate(_layers(net, csrs, epss, K)):
+    for l, (ref, got, ck, e) in enumerate(_layers(net, csrs, epss, K)):
         _check_ck(net, ck, l, K)
-        _check_dw(ref, got, f"dW[{l}]")
+        _check_dw(ref, got, e, f"dW[{l}]")
         err = np.abs(_np(got).astype(np.float64) - r["dW"][l])
         assert not (err > TOL * env["dW"][l] + 1e-30).any(), f"dW[{l}] outside the oracle envelope"
         assert np.abs(r["dW"][l]).max() > 0
@@ -94,9 +102,9 @@ def test_recompute_full_size_stress(K):
     ro = net.readout(dense=True)
     csrs = net.compact(0.2)
     _, _, epss = net.sparse_backward(csrs, ro)
-    for l, (ref, got, ck) in enumerate(_layers(net, csrs, epss, K)):
+    for l, (ref, got, ck, e) in enumerate(_layers(net, csrs, epss, K)):
         _check_ck(net, ck, l, K)
-        _check_dw(ref, got, f"stress dW[{l}]")
+        _check_dw(ref, got, e, f"stress dW[{l}]")
 
 
 @pytest.mark.parametrize("aux", [False, True])
@@ -121,7 +129,8 @@ def test_network_recompute_mode(aux):
     (dW_a, dWo_a, eps_a, cs_a), (dW_b, dWo_b, eps_b, cs_b) = outs
     assert torch.equal(dWo_a, dWo_b)
     for l in range(net.L):
-        _check_dw(dW_a[l], dW_b[l], f"network dW[{l}]")
+        env = _env(ref.trace[l], cs_a[l], eps_a[l], ref.Ws[l].shape[1])
+        _check_dw(dW_a[l], dW_b[l], env, f"network dW[{l}]")
         n = cs_a[l].nnz()
         assert n == cs_b[l].nnz() and torch.equal(eps_a[l][:n], eps_b[l][:n]), f"eps[{l}]"
     with pytest.raises(ValueError):
