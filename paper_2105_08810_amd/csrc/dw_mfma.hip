@@ -25,6 +25,7 @@
 // Blocks: (input tile of 64 inputs) x (chunk of windows); each block writes a partial dW for its
 // chunk; the partials are summed in a fixed order in float64, so dW is bitwise reproducible.
 #include "common.h"
+#include <climits>
 
 namespace snn {
 namespace {
@@ -91,38 +92,55 @@ __global__ __launch_bounds__(256) void mdw_colcount(int TB, int N_out, const int
     if (h[k]) atomicAdd(&cnt[k], h[k]);
 }
 
-// One block: column c's rank (descending count, ties by index) gives its slot v in the quad layout
-// (snake dealing over nq = ceil(N_out / 4) quads); perm[c] = v, inv[v] = c (-1 for slots without a
-// column when N_out is not a multiple of 4).
+// Column c's rank (descending count, ties by index) gives its slot v in the quad layout (snake
+// dealing over nq = ceil(N_out / 4) quads): perm[c] = v, inv[v] = c, and inv[v] = -1 for the slots
+// of ranks N_out .. 4 nq - 1 (no column). Each block ranks 64 columns; its 16 wavefronts split the
+// comparisons and add their partial ranks in LDS.
 __global__ __launch_bounds__(kMQ * 4) void mdw_perm(int N_out, const int32_t* __restrict__ cnt,
                                                     int32_t* __restrict__ perm, int32_t* __restrict__ inv) {
-  __shared__ int cs[kMQ * 4];
-  const int c = threadIdx.x;
+  __shared__ __attribute__((aligned(16))) int cs[kMQ * 4];
+  __shared__ int part[16][kWave];
+  const int t = threadIdx.x;
   const int nq = (N_out + 3) / 4;
-  if (c < N_out) cs[c] = cnt[c];
-  if (c < 4 * nq) inv[c] = -1;
+  for (int k = t; k < kMQ * 4; k += blockDim.x) cs[k] = k < N_out ? cnt[k] : INT_MIN;
   __syncthreads();
-  if (c < N_out) {
-    const int mine = cs[c];
-    int rank = 0;
-    for (int k = 0; k < N_out; ++k) {
-      const int o = cs[k];
-      rank += (o > mine) || (o == mine && k < c);
-    }
-    const int round = rank / nq, idx = rank - round * nq;
-    const int q = (round & 1) ? nq - 1 - idx : idx;
-    const int v = 4 * q + round;
+  const int l = t & (kWave - 1), w = t / kWave;
+  const int c = blockIdx.x * kWave + l;
+  const int mine = c < N_out ? cs[c] : 0;
+  int rank = 0;
+  const int k0 = w * kWave;  // this wavefront's 64 comparisons (entries past N_out hold INT_MIN)
+#pragma unroll 4
+  for (int k = k0; k < k0 + kWave; k += 4) {
+    const int4 o = *reinterpret_cast<const int4*>(cs + k);
+    rank += (o.x > mine) || (o.x == mine && k < c);
+    rank += (o.y > mine) || (o.y == mine && k + 1 < c);
+    rank += (o.z > mine) || (o.z == mine && k + 2 < c);
+    rank += (o.w > mine) || (o.w == mine && k + 3 < c);
+  }
+  part[w][l] = rank;
+  __syncthreads();
+  auto slot_of = [nq](int r) {
+    const int round = r / nq, idx = r - round * nq;
+    return 4 * ((round & 1) ? nq - 1 - idx : idx) + round;
+  };
+  if (w == 0 && c < N_out) {
+    int r = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) r += part[k][l];
+    const int v = slot_of(r);
     perm[c] = v;
     inv[v] = c;
   }
+  if (blockIdx.x == 0 && t >= N_out && t < 4 * nq) inv[slot_of(t)] = -1;
 }
 
-// Layout: one block per window. Pass 1 counts each wavefront's entries per quad (its 32 rows);
-// pass 2 gives each entry its slot: the quad's start, the entries of the quad in earlier rows (the
-// other wavefronts' counts, then this wavefront's running count) and its place in the row's run of
-// that quad (lanes of the row with the same quad before it). Writes
-// rec[slot].x = row offset in the trace tile | (column % 4) << 20, src[slot] = entry index, and the
-// window's qoff row (absolute entry positions; qoff[256] = end of the window's valid entries).
+// Layout: one block per window. The window's entries (its CSR range) are split into four contiguous
+// parts, one per wavefront. Pass 1 counts each part's entries per quad; pass 2 gives each entry its
+// slot: the quad's start, the quad's entries in earlier parts, this part's running count and the
+// entry's place among the same quad's entries of its 64-entry piece (a match mask from one ballot
+// per bit of the quad). CSR order is kept inside a quad. Writes rec[slot].x = row offset in the
+// trace tile | (column slot % 4) << 20, src[slot] = entry index, and the window's qoff row
+// (absolute entry positions; qoff[256] = end of the window's valid entries).
 __global__ __launch_bounds__(kLayWaves * kWave) void mdw_layout(int TB, int N_out, const int32_t* __restrict__ row_ptr,
                                                                 const int32_t* __restrict__ col_idx, int64_t cap,
                                                                 const int32_t* __restrict__ perm,
@@ -130,6 +148,7 @@ __global__ __launch_bounds__(kLayWaves * kWave) void mdw_layout(int TB, int N_ou
                                                                 int32_t* __restrict__ src) {
   __shared__ int cnt[kLayWaves][kMQ];
   __shared__ int rp[kMRW + 1];
+  __shared__ int pm[kMQ * 4];
   const int w = threadIdx.x / kWave;
   const int l = lane_id();
   const int win = blockIdx.x;
@@ -137,17 +156,18 @@ __global__ __launch_bounds__(kLayWaves * kWave) void mdw_layout(int TB, int N_ou
   const int nr = min(kMRW, TB - r0);
   for (int k = threadIdx.x; k <= nr; k += blockDim.x) rp[k] = clampi(row_ptr[r0 + k], cap);
   for (int k = threadIdx.x; k < kLayWaves * kMQ; k += blockDim.x) (&cnt[0][0])[k] = 0;
+  for (int k = threadIdx.x; k < N_out; k += blockDim.x) pm[k] = perm[k];
   __syncthreads();
-  const int ra = min(w * kLayRows, nr), rb = min(ra + kLayRows, nr);
-  for (int r = ra; r < rb; ++r) {
-    const int e_end = rp[r + 1];
-    for (int e = rp[r] + l; e < e_end; e += kWave) {
-      const int c = col_idx[e];
-      if ((unsigned)c < (unsigned)N_out) atomicAdd(&cnt[w][perm[c] >> 2], 1);  // counts only: order does not matter
-    }
+  const int e_a = rp[0];
+  const int len = max(rp[nr] - e_a, 0);
+  const int pa = e_a + (int)((int64_t)len * w / kLayWaves);
+  const int pb = e_a + (int)((int64_t)len * (w + 1) / kLayWaves);
+  for (int e = pa + l; e < pb; e += kWave) {
+    const int c = col_idx[e];
+    if ((unsigned)c < (unsigned)N_out) atomicAdd(&cnt[w][pm[c] >> 2], 1);  // counts only: order does not matter
   }
   __syncthreads();
-  if (w == 0) {  // exclusive scan over quads (lane: quads 4l..4l+3), then the per-wavefront starts
+  if (w == 0) {  // exclusive scan over quads (lane: quads 4l..4l+3), then the per-part starts
     int tot[4], s = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -156,7 +176,7 @@ __global__ __launch_bounds__(kLayWaves * kWave) void mdw_layout(int TB, int N_ou
       for (int q = 0; q < kLayWaves; ++q) tot[k] += cnt[q][4 * l + k];
       s += tot[k];
     }
-    int run = rp[0] + wave_incl_scan(s) - s;
+    int run = e_a + wave_incl_scan(s) - s;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int quad = 4 * l + k;
@@ -173,32 +193,35 @@ __global__ __launch_bounds__(kLayWaves * kWave) void mdw_layout(int TB, int N_ou
     if (l == kWave - 1) qoff[(size_t)win * kMQLd + kMQ] = run;
   }
   __syncthreads();
-  for (int r = ra; r < rb; ++r) {
-    const int e_end = rp[r + 1];
-    for (int e0 = rp[r]; e0 < e_end; e0 += kWave) {
-      const int e = e0 + l;
-      const int c = e < e_end ? col_idx[e] : -1;
-      const bool valid = (unsigned)c < (unsigned)N_out;
-      const int v = valid ? perm[c] : 0;  // the column's slot in the quad layout
-      const int quad = valid ? (v >> 2) : -1;
-      // place among the chunk's entries of the same quad (earlier lanes) and whether a later lane has it
-      const int n = min(kWave, e_end - e0);
-      int before = 0, after = 0;
-      for (int k = 0; k < n; ++k) {
-        const int qk = __builtin_amdgcn_readlane(quad, k);
-        before += (k < l && qk == quad);
-        after += (k > l && qk == quad);
-      }
-      const int base = valid ? cnt[w][quad] : 0;
-      const int slot = base + before;
-      if (valid && slot < cap) {  // a malformed CSR cannot write past the arrays
-        rec[slot].x = (r * kMStride) | ((v & 3) << 20);
-        src[slot] = e;
-      }
-      __builtin_amdgcn_wave_barrier();
-      const bool tail = valid && after == 0;
-      if (tail) cnt[w][quad] = slot + 1;
+  const uint64_t below = (1ull << l) - 1ull;
+  for (int e0 = pa; e0 < pb; e0 += kWave) {
+    const int e = e0 + l;
+    const int c = e < pb ? col_idx[e] : -1;
+    const bool valid = (unsigned)c < (unsigned)N_out;
+    const int v = valid ? pm[c] : 0;           // the column's slot in the quad layout
+    const int key = valid ? (v >> 2) : 511;    // quads < 256; 511 marks lanes without an entry
+    uint64_t match = ~0ull;
+#pragma unroll
+    for (int bit = 0; bit < 9; ++bit) {
+      const uint64_t bal = __ballot((key >> bit) & 1);
+      match &= ((key >> bit) & 1) ? bal : ~bal;
     }
+    const int before = __popcll(match & below);
+    const int after = __popcll(match & ~below & ~(1ull << l));
+    // the entry's row: last r with rp[r] <= e (rows of the window only)
+    int lo = 0, hi = nr - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (rp[mid] <= e) lo = mid; else hi = mid - 1;
+    }
+    const int base = valid ? cnt[w][key] : 0;
+    const int slot = base + before;
+    if (valid && slot < cap) {  // a malformed CSR cannot write past the arrays
+      rec[slot].x = (lo * kMStride) | ((v & 3) << 20);
+      src[slot] = e;
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (valid && after == 0) cnt[w][key] = slot + 1;
   }
 }
 
@@ -442,7 +465,8 @@ void mdw_enqueue_layout(int T, int B, int N_in, int N_out, const int32_t* out_ro
   const int cblocks = std::max(1, std::min(cu_count(), (int)((out_cap + 4095) / 4096)));
   hipLaunchKernelGGL(mdw_colcount, dim3((unsigned)cblocks), dim3(256), 0, s, T * B, N_out, out_row_ptr, out_col_idx,
                      out_cap, b.cnt);
-  hipLaunchKernelGGL(mdw_perm, dim3(1), dim3(kMQ * 4), 0, s, N_out, b.cnt, b.perm, b.inv);
+  hipLaunchKernelGGL(mdw_perm, dim3((unsigned)((N_out + kWave - 1) / kWave)), dim3(kMQ * 4), 0, s, N_out, b.cnt,
+                     b.perm, b.inv);
   hipLaunchKernelGGL(mdw_layout, dim3((unsigned)p.n_win), dim3(kLayWaves * kWave), 0, s, T * B, N_out, out_row_ptr,
                      out_col_idx, out_cap, b.perm, b.qoff, b.rec, b.src);
 }
