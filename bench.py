@@ -38,14 +38,11 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_TFLOPS = 157.3  # dense fp32 matrix-core peak
 CPU_TARGET_S = 10.0  # seconds of oracle work timed for the CPU baseline
-# float64 LDS read-modify-write adds: 256 CUs x 2.4 GHz x 128 B/clk of LDS, 16 B per lane
-# update (8 read, 8 written) -> 4.915e12 lane updates/s; 2 flops each (multiply, add)
-LDS_F64_RMW_TFLOPS = 2 * 256 * 2.4e9 * 128 / 16 / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_dw_stress.json")
 CSRC = os.path.join(ROOT, "paper_2105_08810_amd", "csrc")
 
 
-DW_SOURCES = ("common.h", "runtime.hip", "sparse_backward.hip")  # the sources of the dW call's kernels
+DW_SOURCES = ("common.h", "runtime.hip", "sparse_backward.hip", "dw_mfma.hip")  # the dW call's kernels
 
 
 def csrc_digest() -> str:
@@ -73,6 +70,19 @@ def algorithmic(T, B, n_in, n_out, nnz_out, r_out, nnz_in=None):
         by_gi = 4 * n_in * n_out + 8 * nnz_in + 4 * (TB + 1)
         fl_gi = 2 * nnz_in * n_out + 2 * TB * n_out
     return by_dw, fl_dw, by_gi, fl_gi
+
+
+def forward_bytes(T, B, sizes, bits):
+    """Bytes the forward moves once each: per LIF layer the input spikes (u8) and W read, V (f32),
+    spikes (u8) and the input trace (f32) written, and the active bitset when the forward marks it;
+    the readout (infinite threshold) the same without the bitset."""
+    TB, total = T * B, 0
+    for l in range(len(sizes) - 1):
+        n_in, n_out = sizes[l], sizes[l + 1]
+        total += TB * n_in + 4 * n_in * n_out + 4 * TB * n_out + TB * n_out + 4 * TB * n_in
+        if bits and l < len(sizes) - 2:
+            total += T * ((B * n_out + 63) // 64) * 8
+    return total
 
 
 def cpu_baseline(cfg, b_th, n_samples):
@@ -296,6 +306,36 @@ class ConvRunner:
         self.caps = [c.capacity for c in cs]
         self.conv_nnz = cs[0].nnz()  # the conv layer's active entries (counted before the timed steps)
 
+    def measured_memory(self):
+        """Eq. (memory_saved) from the allocator: the peak bytes allocated while each chain's backward
+        runs (from the readout's gradient at its read entries to the filter gradient), above what
+        was allocated before it, plus the per-entry record of the forward that the chain reads: V
+        [T, B, H W F] (float32) for the dense chain, the conv and pooled active bitsets for the
+        sparse one. Returns [(sparse, dense, saved %)] for the conv layer."""
+        torch, net = self.torch, self.net
+        T, B, H, W, C, F = net.dims
+        dev = net.X.device
+        ro = net.readout(dense=True)
+        TB, N = T * B, H * W * F
+
+        def peak(fn):
+            torch.cuda.synchronize()
+            base = torch.cuda.memory_allocated(dev)
+            torch.cuda.reset_peak_memory_stats(dev)
+            keep = fn()
+            torch.cuda.synchronize()
+            used = torch.cuda.max_memory_allocated(dev) - base
+            del keep
+            return used
+
+        if self.args.conv_csr:
+            sparse = peak(lambda: net.compact_and_backward(self.b_th, ro, self.caps))
+        else:
+            sparse = peak(lambda: net.pooled_backward(self.b_th, ro, self.caps[1]))
+        sparse += net.bits.numel() * net.bits.element_size() + net.pbits.numel() * net.pbits.element_size()
+        dense = peak(lambda: net.dense_backward(self.b_th, ro)) + 4 * TB * N
+        return [(sparse, dense, 100.0 * (dense - sparse) / dense)]
+
     def events(self):
         mk = lambda: self.torch.cuda.Event(enable_timing=True)  # noqa: E731
         return {k: mk() for k in ("fwd0", "fwd1", "cmp0", "conv0", "conv1", "pool0", "pool1", "bw1", "dn0", "dn1")}
@@ -388,12 +428,12 @@ class ConvRunner:
                 "kernel": "pooled active set: snn_pool_route_bits + snn_active_compact_bits (the chain's longest step)",
                 "algorithmic_bytes": pool_bytes, "launch_ms": med(t_pool),
             },
-            "memory_sparse_dense_bytes": [(12 * nnz + 4 * (TB + 1) if csr_chain else 0) + 8 * nnz_pool + 4 * (TB + 1),
-                                          4 * TB * N + 4 * TB * self.net.Np],
+            "memory_sparse_dense_bytes_analytic": [(12 * nnz + 4 * (TB + 1) if csr_chain else 0) + 8 * nnz_pool +
+                                                   4 * (TB + 1), 4 * TB * N + 4 * TB * self.net.Np],
             "wall_s_timed": wall,
         }
-        m = out["memory_sparse_dense_bytes"]
-        out["memory_saved_pct"] = [100.0 * (m[1] - m[0]) / m[1]]
+        m = out["memory_sparse_dense_bytes_analytic"]
+        out["memory_saved_pct_analytic"] = [100.0 * (m[1] - m[0]) / m[1]]
         if with_dense:
             out["speedup_vs_dense"] = out["dense_backward_ms"] / out["sparse_backward_ms"]
             out["overall_speedup_fwd_plus_bwd"] = (out["forward_ms"] + out["dense_backward_ms"]) / (
@@ -608,8 +648,9 @@ class Runner:
         ev["bw1"].record(main)
 
     def memory(self, nnz):
-        """Per LIF layer: bytes each backward chain allocates beyond the shared forward state, and
-        the memory saved, 100 (dense - sparse) / dense (Eq. (memory_saved))."""
+        """Per LIF layer, the analytic figure: bytes each backward chain allocates beyond the shared
+        forward state (CSR, eps, dW and workspaces against the dense gradient buffers), and the
+        memory saved, 100 (dense - sparse) / dense."""
         snn, T, B, L, sizes = self.snn, self.T, self.B, self.L, self.sizes
         TB = T * B
         out = []
@@ -621,6 +662,49 @@ class Runner:
             if l > 0:
                 sparse += 4 * nnz[l - 1] + snn.snn_sparse_grad_in_workspace(T, B, n_out)
                 dense += 4 * TB * n_in
+            out.append((sparse, dense, 100.0 * (dense - sparse) / dense))
+        return out
+
+    def measured_memory(self):
+        """Eq. (memory_saved) from the allocator, per LIF layer: the peak bytes allocated while the
+        layer's backward step runs in each chain, above what was allocated before it (the forward
+        state and the incoming spike gradient). The sparse step makes its active set (CSR, g), then
+        allocates dW, the spike gradient at the active entries of the layer below and its
+        workspaces; the dense step allocates dW, the dense spike gradient and its workspace. Each
+        step also reads one per-entry record the forward kept for it, counted too: V [T, B, N]
+        (float32) for the dense step, the active bitset (one bit per entry) for the sparse one
+        (V itself when the compaction reads V). Returns [(sparse, dense, saved %)] per layer."""
+        torch, snn, net = self.torch, self.snn, self.net
+        T, B, L, TB = self.T, self.B, self.L, self.T * self.B
+        b_th = self.b_th
+        dev = net.X.device
+        fused = not self.args.unfused
+        out = []
+
+        def peak(fn):
+            torch.cuda.synchronize()
+            base = torch.cuda.memory_allocated(dev)
+            torch.cuda.reset_peak_memory_stats(dev)
+            keep = fn()
+            torch.cuda.synchronize()
+            used = torch.cuda.max_memory_allocated(dev) - base
+            del keep
+            return used
+
+        for l in range(L):
+            n_in, n_out = net.Ws[l].shape
+            below = net.compact_layer(l - 1, b_th, self.caps[l - 1]) if l > 0 else None  # made by that layer's step
+            eps_s = torch.zeros(self.caps[l], dtype=torch.float32, device=dev)
+            sparse = peak(lambda: (lambda c: snn.sparse_backward(net.Ws[l], net.trace[l], net.alphas[l], c, eps_s,
+                                                                   inp=below) + (c,))(
+                net.compact_layer(l, b_th, self.caps[l])))
+            sparse += T * ((B * n_out + 63) // 64) * 8 if fused else 4 * TB * n_out
+            del eps_s, below
+            eps_d = torch.zeros((T, B, n_out), dtype=torch.float32, device=dev)
+            dense = peak(lambda: snn.dense_backward_ref(net.Ws[l], net.trace[l], net.V[l], eps_d, net.alphas[l],
+                                                        net.theta, b_th, net.beta, grad_in=l > 0))
+            dense += 4 * TB * n_out
+            del eps_d
             out.append((sparse, dense, 100.0 * (dense - sparse) / dense))
         return out
 
@@ -671,7 +755,7 @@ class Runner:
         dw_flops = sum(p[1] for p in per)
         dw_bytes = sum(p[0] for p in per)
         dw_s = sum(dw_ms) * 1e-3
-        achieved = dw_flops / dw_s / 1e12
+        dw_gbs = dw_bytes / dw_s / 1e9  # algorithmic bytes per launch / average launch time
         value = sum(nnz) / (med(t_sparse) * 1e-3)
         mem = self.memory(nnz)
         # whole sparse backward on its gathered bytes (compaction: V read... here the bitset, the
@@ -682,6 +766,8 @@ class Runner:
         sparse_bytes = cmp_bytes + sum(p[0] + p[2] for p in per)
         # dense chain: dW GEMM of every LIF layer and the spike-gradient GEMM of all but the first
         dense_flops = sum(2 * T * B * sizes[l] * sizes[l + 1] * (2 if l > 0 else 1) for l in range(L))
+        fwd_bytes = forward_bytes(T, B, sizes, not self.args.unfused)
+        use_aux = not (self.args.serial or self.args.graph)
         traffic = None
         if os.path.exists(TRAFFIC_FILE):
             with open(TRAFFIC_FILE) as f:
@@ -712,17 +798,24 @@ class Runner:
             "sparse_grad_in_ms": [med(t) for t in reversed(t_gi)],
             "dense_backward_ms": med(span("dn0", "dn1")) if dense and not self.args.no_dense else None,
             "forward_ms": med(t_fwd),
+            "forward_hbm_frac": fwd_bytes / (med(t_fwd) * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "forward_bytes": fwd_bytes,
             "active_fraction": [n / (T * B * sizes[l + 1]) for l, n in enumerate(nnz)],
-            "memory_saved_pct": [m[2] for m in mem],
-            "backward_bytes_sparse_dense": [[m[0], m[1]] for m in mem],
+            "memory_saved_pct_analytic": [m[2] for m in mem],
+            "backward_bytes_sparse_dense_analytic": [[m[0], m[1]] for m in mem],
             "nnz": nnz,
             "roofline": {
-                "bound": "alu", "achieved": achieved, "peak": LDS_F64_RMW_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / LDS_F64_RMW_TFLOPS, "traffic": traffic,
-                "kernel": "snn_sparse_dw (slab records + dw_slab_kernel + chunk reduction), LIF layers",
-                "resource": "float64 LDS read-modify-write adds (multiply on the VALU)",
-                "algorithmic_flops": dw_flops, "algorithmic_bytes": dw_bytes, "launch_ms": dw_ms,
-                "hbm_achieved_gbs": dw_bytes / dw_s / 1e9, "hbm_frac": dw_bytes / dw_s / 1e9 / HBM_PEAK_GBS,
+                "bound": "hbm", "achieved": dw_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": dw_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                "kernel": ("snn_sparse_dw_prepared (mdw_gate + mdw_kernel + mdw_reduce) of each LIF layer; its "
+                           "structure-only layout runs earlier, beside the layer above" if self.pipelined and use_aux
+                           else "snn_sparse_dw (layout + mdw_gate + mdw_kernel + mdw_reduce) of each LIF layer"),
+                "algorithmic_bytes_per_launch": dw_bytes / L, "algorithmic_flops_per_launch": dw_flops / L,
+                "launches": L, "launch_ms": dw_ms,
+                "alu_view": {"resource": "fp32 matrix cores (v_mfma_f32_4x4x1f32)", "achieved": dw_flops / dw_s / 1e12,
+                             "peak": MFMA_F32_TFLOPS, "unit": "TFLOP/s",
+                             "frac": dw_flops / dw_s / 1e12 / MFMA_F32_TFLOPS},
+                "chain_hbm_frac": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9 / HBM_PEAK_GBS,
             },
             "sparse_backward_gathered_bytes": sparse_bytes,
             "sparse_backward_hbm_gbs": sparse_bytes / (med(t_sparse) * 1e-3) / 1e9,
@@ -738,6 +831,7 @@ class Runner:
                 "checkpoint_bytes": sum(4 * nck * B * sizes[l] for l in range(L)),
                 "dw_kernel": "dw_slab_spikes_kernel (trace rebuilt in registers from the input spikes)"}
             out["roofline"]["kernel"] = "snn_sparse_dw_spikes (slab records + dw_slab_spikes_kernel + chunk reduction)"
+            out["roofline"]["alu_view"]["resource"] = "float64 LDS adds (multiply on the VALU)"
             out["roofline"]["traffic"] = None
         if out["dense_backward_ms"] is not None:
             out["dense_mfma_tflops"] = dense_flops / (out["dense_backward_ms"] * 1e-3) / 1e12
@@ -816,6 +910,9 @@ def main():
         dense = not args.no_dense and (k == 0 or not args.sweep)  # the dense chain's cost does not depend on B_th
         evs, cs, wall = run.run(args.steps, args.warmup, dense)
         out = run.summarize(evs, cs, wall, dense)
+        mem = run.measured_memory()
+        out["memory_saved_pct"] = [m[2] for m in mem]
+        out["backward_peak_bytes_sparse_dense"] = [[m[0], m[1]] for m in mem]
         if dense:
             dense_ms = out["dense_backward_ms"]
         elif dense_ms is not None:

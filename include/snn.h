@@ -143,7 +143,10 @@ snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, 
  *   aux_stream (may be NULL): a second hipStream_t. When given, the spike-gradient part runs on
  *   it beside the dW part on `stream`; the call makes aux_stream wait for the work already on
  *   `stream`, and `stream` wait for the aux work, so work enqueued on `stream` afterwards sees
- *   both results. Creates two HIP events per call.
+ *   both results. The fork and join use two HIP events per device and host thread, created by
+ *   the first such call and kept until the thread ends; no call creates or destroys events or
+ *   synchronises the host. SNN_ERR_HIP when the fork or the join cannot be enqueued (after a
+ *   failed join, work enqueued later on `stream` is not ordered after eps_in).
  * Supported: N_out <= 4096.
  */
 size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_out, int64_t out_cap);

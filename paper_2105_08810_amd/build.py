@@ -75,6 +75,47 @@ def build(verbose: bool = True) -> str:
     return LIB
 
 
+SAN_DIR = os.path.join(OBJDIR, "san")
+SAN_LIB = os.path.join(SAN_DIR, "libsnn_san.so")
+# AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (argument validation,
+# workspace sizing, planning); each -fsanitize= goes to the host pass alone
+SAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def asan_runtime() -> str:
+    """Path of the compiler's shared AddressSanitizer runtime (preloaded into a Python process
+    that loads the sanitized library)."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    r = subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    return r.stdout.strip()
+
+
+def build_sanitized() -> str:
+    """libsnn_san.so: the same sources with the host sanitizers (-O1 -g), for CPU tests of the
+    argument validation. The device code is built as usual (it does not run in those tests)."""
+    os.makedirs(SAN_DIR, exist_ok=True)
+    flags = [f for f in COMMON if f != "-O3"] + ["-O1", "-g"] + SAN_HOST
+
+    def one(src):
+        obj = os.path.join(SAN_DIR, os.path.splitext(src)[0] + ".o")
+        cmd = [hipcc(), *flags, "-c", os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed on {src}:\n{' '.join(cmd)}\n{r.stderr}")
+        return obj
+
+    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+        objs = list(ex.map(one, SOURCES))
+    cmd = [hipcc(), "-shared", f"--offload-arch={ARCH}", *SAN_HOST, "-shared-libasan", "-o", SAN_LIB, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stderr}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     build()
     sys.exit(0)

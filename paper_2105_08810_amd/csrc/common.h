@@ -45,6 +45,10 @@ struct Carve {
 // Number of compute units of the current device (cached per process and device).
 int cu_count();
 
+// Raises a kernel's dynamic-LDS limit on the current device to at least `bytes`. The attribute
+// is set once per device, kernel and size and remembered (thread-safe); later calls only look up.
+void ensure_dynamic_lds(const void* kernel, int bytes);
+
 // Sparse dW on the matrix cores (dw_mfma.hip), for 32 < N_out <= 1024 and N_in % 4 == 0.
 struct MdwPlan {
   int n_win, n_itiles, n_chunks, wpc;  // windows of rows, input tiles, chunks of windows, windows per chunk

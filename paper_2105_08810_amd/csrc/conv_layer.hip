@@ -657,7 +657,7 @@ extern "C" snn_status snn_conv_sparse_dw(const float* trace_in, int T, int B, in
   const size_t lds = (size_t)nacc * sizeof(double);
   const PooledArgs none{nullptr, nullptr, 0.0f, 0.0f, 0.0f};
   auto launch = [&](auto kernel) {
-    (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    ensure_dynamic_lds((const void*)kernel, (int)lds);
     hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCsdThreads), lds, s, trace_in, TB, H, W, C, F, conv_row_ptr,
                        conv_col_idx, conv_g, eps_conv, conv_cap, rpb, part, none);
   };
@@ -689,7 +689,7 @@ extern "C" snn_status snn_conv_sparse_dw_pooled(const float* trace_in, const flo
   const size_t lds = (size_t)nacc * sizeof(double);
   const PooledArgs pa{V, arg, theta, b_th, beta};
   auto launch = [&](auto kernel) {
-    (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    ensure_dynamic_lds((const void*)kernel, (int)lds);
     hipLaunchKernelGGL(kernel, dim3((unsigned)nb), dim3(kCsdThreads), lds, s, trace_in, TB, H, W, C, F, pool_row_ptr,
                        pool_col_idx, nullptr, eps_pool, pool_cap, rpb, part, pa);
   };

@@ -15,7 +15,6 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128, BK = 16, PAD = 4;
 constexpr int kGemmThreads = 256;
-constexpr int kAssumedCUs = 256;
 
 __device__ __forceinline__ float gate(float e, float v, float theta, float bth, float beta, bool readout) {
   if (readout) return e;
@@ -212,15 +211,15 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_f32_mfma(int M, int N, int 
 
 __global__ void reduce_splits(const float* __restrict__ part, int n_split, size_t n, float* __restrict__ out) {
   for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n; k += (size_t)gridDim.x * blockDim.x) {
-    float s = 0.0f;
-    for (int c = 0; c < n_split; ++c) s += part[(size_t)c * n + k];
-    out[k] = s;
+    double s = 0.0;  // fixed order, rounded once
+    for (int c = 0; c < n_split; ++c) s += (double)part[(size_t)c * n + k];
+    out[k] = (float)s;
   }
 }
 
 int dw_splits(int TB, int N_in, int N_out) {
   const int tiles = ((N_in + BM - 1) / BM) * ((N_out + BN - 1) / BN);
-  int s = (2 * kAssumedCUs + tiles - 1) / tiles;
+  int s = (2 * cu_count() + tiles - 1) / tiles;
   s = std::min(s, std::max(1, TB / 256));
   return std::max(1, std::min(s, 64));
 }

@@ -476,13 +476,7 @@ void mdw_enqueue_rest(const float* trace_in, int T, int B, int N_in, int N_out, 
   const MdwPlan p = plan_mdw(T, B, N_in, N_out);
   const MdwBufs b = mdw_bufs(p, N_in, N_out, out_cap, workspace, dW);
   hipLaunchKernelGGL(mdw_gate, dim3((unsigned)p.n_win), dim3(256), 0, s, b.qoff, out_cap, b.src, out_g, eps_out, b.rec);
-  static bool attr_set[64] = {};
-  int dev = 0;
-  (void)hipGetDevice(&dev);
-  if (dev >= 0 && dev < 64 && !attr_set[dev]) {
-    (void)hipFuncSetAttribute((const void*)mdw_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * kMBuf);
-    attr_set[dev] = true;
-  }
+  ensure_dynamic_lds((const void*)mdw_kernel, 2 * kMBuf);
   hipLaunchKernelGGL(mdw_kernel, dim3((unsigned)(p.n_itiles * p.n_chunks)), dim3(kMThreads), 2 * kMBuf, s, trace_in,
                      T * B, N_in, N_out, b.qoff, b.rec, b.inv, out_cap, p.n_win, p.wpc, p.n_itiles, b.part);
   if (p.n_chunks > 1) {

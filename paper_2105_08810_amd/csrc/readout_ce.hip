@@ -36,9 +36,9 @@ __global__ __launch_bounds__(kThreads) void ce_sample(const float* __restrict__ 
       a[c] = best;
       tstar[(size_t)b * C + c] = bt;
     } else {
-      float s = 0.0f;
-      for (int t = 0; t < T; ++t) s += V[((size_t)t * B + b) * C + c];
-      a[c] = s;
+      double s = 0.0;  // the logit of a sum over time, rounded once
+      for (int t = 0; t < T; ++t) s += (double)V[((size_t)t * B + b) * C + c];
+      a[c] = (float)s;
     }
   }
   __syncthreads();

@@ -2,6 +2,9 @@
 // counts into CSR row pointers.
 #include "common.h"
 
+#include <mutex>
+#include <vector>
+
 extern "C" const char* snn_status_string(int status) {
   switch (status) {
     case SNN_OK: return "SNN_OK";
@@ -26,6 +29,23 @@ int cu_count() {
     cached_dev = dev;
   }
   return cached;
+}
+
+void ensure_dynamic_lds(const void* kernel, int bytes) {
+  struct Done {
+    int dev;
+    const void* kernel;
+    int bytes;
+  };
+  static std::mutex mu;
+  static std::vector<Done> done;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const Done& d : done)
+    if (d.dev == dev && d.kernel == kernel && d.bytes >= bytes) return;
+  if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess)
+    done.push_back({dev, kernel, bytes});
 }
 
 namespace {

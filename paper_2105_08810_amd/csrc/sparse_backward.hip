@@ -33,7 +33,6 @@ constexpr size_t kLdsBudget = 150 * 1024;
 constexpr int kWalkThreads = 256;
 constexpr int kWalkWaves = kWalkThreads / kWave;
 constexpr int kGinBatch = 4;
-constexpr int kAssumedCUs = 256;
 constexpr int kBufWord3 = 0x00020000;  // buffer descriptor word 3 on gfx9: 32-bit data format
 
 struct DwPlan {
@@ -49,7 +48,7 @@ DwPlan plan_dw_slab(int T, int B, int N_in, int N_out, int slab_cap) {
   p.lds = (size_t)p.slab * kLd * sizeof(double);
   p.n_itiles = (N_in + kItile - 1) / kItile;
   const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(2, (160 * 1024) / p.lds));
-  const int target = kAssumedCUs * per_cu * 8;  // short chunks: the slab blocks of a tile stay close (L2 reuse)
+  const int target = cu_count() * per_cu * 8;  // short chunks: the slab blocks of a tile stay close (L2 reuse)
   const int tiles = p.n_itiles * p.n_slabs;
   int nc = (target + tiles - 1) / tiles;
   nc = std::min(nc, std::max(1, TB / (4 * N_out)));  // partial slabs stay small next to the trace
@@ -65,7 +64,7 @@ DwPlan plan_dw_slab(int T, int B, int N_in, int N_out, int slab_cap) {
 // half that, two blocks per CU, twice the loads in flight.
 DwPlan plan_dw(int T, int B, int N_in, int N_out) {
   const DwPlan p = plan_dw_slab(T, B, N_in, N_out, kSlab);
-  if ((int64_t)p.n_itiles * p.n_slabs * p.n_chunks < 2 * kAssumedCUs) return plan_dw_slab(T, B, N_in, N_out, kSlab / 2);
+  if ((int64_t)p.n_itiles * p.n_slabs * p.n_chunks < 2 * cu_count()) return plan_dw_slab(T, B, N_in, N_out, kSlab / 2);
   return p;
 }
 
@@ -469,9 +468,9 @@ __global__ void fill_zero(float* __restrict__ p, size_t n) {
 
 __global__ void reduce_chunks(const float* __restrict__ part, int n_chunks, size_t n, float* __restrict__ out) {
   for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n; k += (size_t)gridDim.x * blockDim.x) {
-    float s = 0.0f;
-    for (int c = 0; c < n_chunks; ++c) s += part[(size_t)c * n + k];
-    out[k] = s;
+    double s = 0.0;  // fixed order, rounded once
+    for (int c = 0; c < n_chunks; ++c) s += (double)part[(size_t)c * n + k];
+    out[k] = (float)s;
   }
 }
 
@@ -590,7 +589,7 @@ NarrowDwPlan plan_narrow_dw(int T, int B, int N_in) {
   p.n_iw = (N_in + kWave - 1) / kWave;
   constexpr int kMaxRows = 63 * kWave;  // a chunk (starting at a multiple of 8) spans <= 64 bitset words
   const int units = (TB + kNarrowBatch - 1) / kNarrowBatch;
-  int nc = (32 * kAssumedCUs + p.n_iw - 1) / p.n_iw;  // about 32 wavefronts per CU
+  int nc = (32 * cu_count() + p.n_iw - 1) / p.n_iw;  // about 32 wavefronts per CU
   nc = std::min(nc, std::min(units, 1024));
   nc = std::max(nc, (TB + kMaxRows - 1) / kMaxRows);
   p.rows_per_chunk = std::min(kMaxRows, ((units + nc - 1) / nc) * kNarrowBatch);
@@ -1087,7 +1086,7 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
     hipLaunchKernelGGL(slab_fill<false>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
                        out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
   const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
-  (void)hipFuncSetAttribute((const void*)dw_slab_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+  ensure_dynamic_lds((const void*)dw_slab_kernel, (int)p.lds);
   hipLaunchKernelGGL(dw_slab_kernel, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out, sp, rec, nrec,
                      part, p.rows_per_chunk, p.n_itiles, p.n_slabs, p.slab);
   if (p.n_chunks > 1) {
@@ -1161,8 +1160,7 @@ void enqueue_dw_spikes(const uint8_t* s_in, const float* ck, int K, float alpha,
     hipLaunchKernelGGL(slab_fill<false>, rgrid, rblock, 0, s, TB, N_out, p.n_slabs, p.slab, R, out_row_ptr,
                        out_col_idx, out_g, eps_out, out_cap, sp, nrec, rec);
   const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * q.n_chunks));
-  (void)hipFuncSetAttribute((const void*)dw_slab_spikes_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)p.lds);
+  ensure_dynamic_lds((const void*)dw_slab_spikes_kernel, (int)p.lds);
   hipLaunchKernelGGL(dw_slab_spikes_kernel, dgrid, dim3(kDwThreads), p.lds, s, s_in, ck, K, alpha, T, B, N_in, N_out,
                      sp, rec, nrec, part, q.tlen, q.n_bblk, p.n_itiles, p.n_slabs, p.slab);
   if (q.n_chunks > 1) {
@@ -1218,7 +1216,7 @@ void enqueue_grad_in(const float* W, int T, int B, int N_in, int N_out, float al
   hipLaunchKernelGGL(gin_carries, dim3((unsigned)((BN + 255) / 256)), dim3(256), 0, s, T, B, N_out, alpha, wp.P, wp.C,
                      Lbuf);
   const int nj = (N_out + kWave - 1) / kWave;
-  const dim3 walk_grid(share_cu ? std::min<unsigned>(wgrid.x, 2 * kAssumedCUs) : wgrid.x);
+  const dim3 walk_grid(share_cu ? std::min<unsigned>(wgrid.x, 2u * (unsigned)cu_count()) : wgrid.x);
 #define SNN_WALK(NJ_)                                                                                             \
   launch_walk<NJ_>(walk_grid, 0, s, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, eps_out, \
                    out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)
@@ -1345,6 +1343,27 @@ extern "C" size_t snn_sparse_backward_workspace(int T, int B, int N_in, int N_ou
   return align256(dw_workspace(T, B, N_in, N_out, out_cap)) + gin_workspace(T, B, N_out);
 }
 
+namespace {
+// The fork and join events of snn_sparse_backward's auxiliary stream: two per device and host
+// thread, created on first use and kept for the life of the thread, so that a call creates and
+// destroys nothing. A stream wait takes the event's state when it is enqueued, so reusing the
+// pair call after call on one thread is safe.
+bool fork_join_events(hipEvent_t* in, hipEvent_t* out) {
+  constexpr int kMaxDevices = 64;
+  thread_local hipEvent_t ev[kMaxDevices][2] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return false;
+  for (int k = 0; k < 2; ++k)
+    if (!ev[dev][k] && hipEventCreateWithFlags(&ev[dev][k], hipEventDisableTiming) != hipSuccess) {
+      ev[dev][k] = nullptr;
+      return false;
+    }
+  *in = ev[dev][0];
+  *out = ev[dev][1];
+  return true;
+}
+}  // namespace
+
 extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in, int T, int B, int N_in, int N_out,
                                           float alpha, const int32_t* out_row_ptr, const int32_t* out_col_idx,
                                           const float* out_g, const float* eps_out, int64_t out_cap,
@@ -1370,15 +1389,15 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
   if (narrow_g)
     enqueue_narrow_g(T * B, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, reinterpret_cast<float*>(dw_ws),
                      s);
-  // The spike gradient (L1/L2-gather bound) and dW (LDS-atomic bound) lean on different parts of
-  // a CU; with an auxiliary stream they run side by side. aux waits for what is already on s,
-  // and s waits for aux before anything enqueued after this call.
+  // The spike gradient (a gather of W rows) and dW (matrix cores on LDS tiles) lean on different
+  // parts of a CU; with an auxiliary stream they run side by side. aux waits for what is already
+  // on s, and s waits for aux before anything enqueued after this call.
   hipStream_t sa = s;
   hipEvent_t ev_in = nullptr, ev_out = nullptr;
-  if (do_gin && aux_stream && aux_stream != stream &&
-      hipEventCreateWithFlags(&ev_in, hipEventDisableTiming) == hipSuccess &&
-      hipEventCreateWithFlags(&ev_out, hipEventDisableTiming) == hipSuccess && hipEventRecord(ev_in, s) == hipSuccess &&
-      hipStreamWaitEvent(static_cast<hipStream_t>(aux_stream), ev_in, 0) == hipSuccess) {
+  if (do_gin && aux_stream && aux_stream != stream && fork_join_events(&ev_in, &ev_out)) {
+    if (hipEventRecord(ev_in, s) != hipSuccess ||
+        hipStreamWaitEvent(static_cast<hipStream_t>(aux_stream), ev_in, 0) != hipSuccess)
+      return SNN_ERR_HIP;  // nothing enqueued yet
     sa = static_cast<hipStream_t>(aux_stream);
   }
   if (do_gin) {
@@ -1390,11 +1409,7 @@ extern "C" snn_status snn_sparse_backward(const float* W, const float* trace_in,
                     narrow_g ? reinterpret_cast<const float*>(dw_ws) : nullptr);
   }
   enqueue_dw(trace_in, T, B, N_in, N_out, out_row_ptr, out_col_idx, out_g, eps_out, out_cap, dW, dw_ws, s, narrow_g);
-  if (sa != s) {
-    if (hipEventRecord(ev_out, sa) != hipSuccess || hipStreamWaitEvent(s, ev_out, 0) != hipSuccess)
-      (void)hipStreamSynchronize(sa);  // never leave aux work unordered with later work on s
-  }
-  if (ev_in) (void)hipEventDestroy(ev_in);
-  if (ev_out) (void)hipEventDestroy(ev_out);
+  if (sa != s && (hipEventRecord(ev_out, sa) != hipSuccess || hipStreamWaitEvent(s, ev_out, 0) != hipSuccess))
+    return SNN_ERR_HIP;  // the join failed: later work on stream is not ordered after eps_in
   return launch_status();
 }

@@ -1,13 +1,20 @@
 """The C ABI on the CPU: the library loads, exports every symbol the header declares, and
-rejects bad arguments before any HIP call (so these run without a GPU)."""
+rejects bad arguments before any HIP call (so these run without a GPU). The same tests run a
+second time, in a child process, against a build of the library with AddressSanitizer and
+UndefinedBehaviorSanitizer on its host code."""
 import ctypes
 import math
 import os
 import re
+import subprocess
+import sys
 
 import pytest
 
 from paper_2105_08810_amd import snn
+
+# set in the child process of test_validation_under_sanitizers: the sanitized library
+SAN_LIB = os.environ.get("SNN_ABI_SANITIZED_LIB")
 
 NAN = float("nan")
 INF = math.inf
@@ -16,6 +23,12 @@ FAKE = 0x1000  # never dereferenced: every call below must fail validation first
 
 @pytest.fixture(scope="module")
 def lib():
+    if SAN_LIB:
+        l = ctypes.CDLL(SAN_LIB)
+        for name, (res, args) in snn._SIGNATURES.items():
+            getattr(l, name).restype = res
+            getattr(l, name).argtypes = args
+        return l
     if not os.path.exists(snn.LIB_PATH):
         from paper_2105_08810_amd import build
         build.build(verbose=False)
@@ -27,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
         text = f.read()
     declared = set(re.findall(r"\b(snn_[a-z_]+)\s*\(", text))
     assert {"snn_lif_forward", "snn_active_compact", "snn_sparse_backward", "snn_dense_backward_ref"} <= declared
-    raw = ctypes.CDLL(snn.LIB_PATH)
+    raw = ctypes.CDLL(SAN_LIB or snn.LIB_PATH)
     for name in sorted(declared):
         assert hasattr(raw, name), name
     assert declared == set(snn._SIGNATURES), "binding and header disagree"
@@ -343,3 +356,22 @@ def test_conv_entry_points_reject(lib):
     assert lib.snn_conv_dense_dw(FAKE, None, FAKE, 10, 4, 8, 8, 1, 64, 1.0, 0.2, 100.0, FAKE, FAKE, wd, None) == E
     assert lib.snn_conv_dense_dw(FAKE, FAKE, FAKE, 10, 4, 8, 8, 4096, 512, 1.0, 0.2, 100.0, FAKE, FAKE, 1 << 40,
                                  None) == snn.SNN_ERR_UNSUPPORTED
+
+
+@pytest.mark.skipif(SAN_LIB is not None, reason="runs in the parent process only")
+def test_validation_under_sanitizers():
+    """Every test above, in a child process, against libsnn_san.so (host code built with
+    -fsanitize=address,undefined, no recovery): any out-of-bounds access, overflow or other
+    undefined behaviour in the argument checks, workspace queries or plans ends the child."""
+    from paper_2105_08810_amd import build
+    path = build.build_sanitized()
+    env = dict(os.environ)
+    env.update(SNN_ABI_SANITIZED_LIB=path, LD_PRELOAD=build.asan_runtime(),
+               ASAN_OPTIONS="detect_leaks=0:halt_on_error=1:abort_on_error=0",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", __file__],
+                       capture_output=True, text=True, env=env, timeout=600)
+    out = r.stdout + r.stderr
+    assert r.returncode == 0, out[-4000:]
+    assert "runtime error" not in out and "AddressSanitizer" not in out, out[-4000:]
+    assert " passed" in out

@@ -60,10 +60,19 @@ def test_grad_difference_matches_oracle():
         assert a[k] == pytest.approx(b[k], rel=1e-12)
 
 
-def test_roofline_peaks_from_unit_counts():
-    assert bench.LDS_F64_RMW_TFLOPS == pytest.approx(2 * 256 * 2.4e9 * 128 / 16 / 1e12)
+def test_roofline_peaks():
     assert bench.HBM_PEAK_GBS == 8000.0
     assert bench.MFMA_F32_TFLOPS == 157.3
+
+
+def test_forward_bytes_by_hand():
+    # T=2, B=3; 5 inputs, one LIF layer of 4, readout of 2; bitsets marked for the LIF layer only
+    TB = 6
+    lif = TB * 5 + 4 * 5 * 4 + 4 * TB * 4 + TB * 4 + 4 * TB * 5
+    ro = TB * 4 + 4 * 4 * 2 + 4 * TB * 2 + TB * 2 + 4 * TB * 4
+    bits = 2 * ((3 * 4 + 63) // 64) * 8
+    assert bench.forward_bytes(2, 3, [5, 4, 2], bits=False) == lif + ro
+    assert bench.forward_bytes(2, 3, [5, 4, 2], bits=True) == lif + ro + bits
 
 
 @pytest.mark.gpu
@@ -77,8 +86,19 @@ def test_bench_line_on_tiny():
     assert line["n_gpus"] == 1 and line["steps"] == 3 and line["warmup"] == 1
     assert line["config"]["workload"].startswith("tiny")
     rl = line["roofline"]
-    assert rl["bound"] in ("hbm", "mfma", "alu") and rl["peak"] > 0 and 0 < rl["frac"] < 1
+    assert rl["bound"] == "hbm" and rl["peak"] == bench.HBM_PEAK_GBS and rl["unit"] == "GB/s" and 0 < rl["frac"] < 1
     assert math.isclose(rl["frac"], rl["achieved"] / rl["peak"], rel_tol=1e-9)
+    # achieved = algorithmic bytes per launch / average launch time
+    per_launch_s = sum(rl["launch_ms"]) * 1e-3 / rl["launches"]
+    assert math.isclose(rl["achieved"], rl["algorithmic_bytes_per_launch"] / per_launch_s / 1e9, rel_tol=1e-9)
+    av = rl["alu_view"]
+    assert av["peak"] == bench.MFMA_F32_TFLOPS and math.isclose(av["frac"], av["achieved"] / av["peak"])
+    assert 0 < rl["chain_hbm_frac"] < 1 and 0 < line["forward_hbm_frac"] < 1
+    # memory from the allocator's peaks, beside the analytic figure
+    peaks = line["backward_peak_bytes_sparse_dense"]
+    assert len(peaks) == len(line["memory_saved_pct"]) == len(line["memory_saved_pct_analytic"])
+    for (sp, dn), pct in zip(peaks, line["memory_saved_pct"]):
+        assert sp > 0 and dn > 0 and math.isclose(pct, 100.0 * (dn - sp) / dn)
     cb = line["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0
     assert line["value"] > 0 and line["sparse_backward_ms"] > 0 and line["dense_backward_ms"] > 0

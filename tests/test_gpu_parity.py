@@ -96,9 +96,10 @@ def check_all(inp, b_th, g, ref, dense=True):
     assert abs(float(loss.item()) - rro["loss"]) <= 1e-5 * max(1.0, abs(rro["loss"]))
     assert_bits(_np(ro_csr.row_ptr).astype(np.int64), rro["row_ptr"], "readout row_ptr")
     assert_bits(_np(ro_csr.col_idx).astype(np.int64), rro["col_idx"], "readout col_idx")
-    # dL/da = (softmax(a) - y)/B: float32 logits (a sum over T steps in mode 'sum') move p by a
-    # relative amount of the logits' rounding, so the bar is the gradient bar relative to max |dL/da|
-    assert np.abs(_np(ro_eps) - rro["eps"]).max() <= TOL * np.abs(rro["eps"]).max()
+    # dL/da = (softmax(a) - y)/B at the read entries, against its envelope (p + y)/B
+    n_ro = int(rro["row_ptr"][-1])
+    env_ro = oracle.csr_values(rro["G_abs"], rro["row_ptr"], rro["col_idx"])
+    assert_env(_np(ro_eps)[:n_ro], rro["eps"], env_ro, "readout eps")
     # sparse gradients
     assert_env(_np(g["dW_out"]), r["dW_out"], env["dW_out"], "dW_out")
     for l in range(net.L):
@@ -146,8 +147,13 @@ def _ragged_sum():
     ("event", None, 0.2),
     ("event", None, 0.5),
     ("stress", list(range(8)), 0.02),
+    ("stress", list(range(8)), 0.05),
+    ("stress", list(range(8)), 0.1),
     ("stress", list(range(8)), 0.2),
+    ("stress", list(range(8)), 0.35),
+    ("stress", list(range(8)), 0.5),
     ("stress", list(range(8)), 0.8),
+    ("stress", list(range(8)), 1.2),
     ("deep", list(range(32)), 0.2),
     ("deep", list(range(16)), 0.95),
     ("latency_train", list(range(32)), 0.2),
@@ -314,63 +320,96 @@ def test_split_calls_match_combined(name, batch, b_th):
             eps = eps_in
 
 
-def test_full_size_stress_sampled():
-    """The stress workload at full size (T=500, B=256, 3 x 1024) in the bench's launch
-    configuration (spike gradient on an auxiliary stream beside dW). Samples are independent in
-    the forward, compaction and spike gradient, so for sampled b the oracle run on sample b alone
-    (its loss gradient scaled by 1/B) is exact: V, spikes, traces and CSR rows bit-exact, eps of
-    every layer within the envelope. dW sums over all samples: checked against the dense matrix-core
-    path of the same truncated gradient (validated against the oracle on the smaller cases)."""
-    cfg = CONFIGS["stress"]
-    b_th = cfg.b_th
-    print(f"\n[case] full-size stress b_th={b_th}", flush=True)
-    inp = make_inputs(cfg)
-    net = pipeline.from_inputs(inp).forward()
-    ro = net.readout(dense=True)
-    csrs = net.compact(b_th)
-    T, B, L = net.T, net.B, net.L
-    main = torch.cuda.current_stream()
-    aux = torch.cuda.Stream()
-    _, eps = snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, ro[0], ro[1], inp=csrs[L - 1],
-                                 aux_stream=aux)
-    eps_l, dW = [None] * L, [None] * L
-    for l in range(L - 1, -1, -1):
-        eps_l[l] = eps
-        n_in, n_out = net.Ws[l].shape
-        if l > 0:
-            share = 3.0 * csrs[l].capacity * n_in >= 2.0 * csrs[l - 1].capacity * n_out
-            aux.wait_stream(main)
-            eps_in = snn.sparse_grad_in(net.Ws[l], net.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=share,
-                                        stream=aux)
-        dW[l] = snn.sparse_dw(net.trace[l], csrs[l], eps, n_out, stream=main)
-        if l > 0:
-            main.wait_stream(aux)
-            eps = eps_in
-    ddW, _, _ = net.dense_backward(b_th, ro)
-    torch.cuda.synchronize()
+def _sample_entries(csr, T, B, b):
+    """CSR positions, times and columns of sample b's entries (rows t*B + b), in CSR order."""
+    rp = _np(csr.row_ptr).astype(np.int64)
+    rows = np.arange(T) * B + b
+    lo, hi = rp[rows], rp[rows + 1]
+    idx = np.concatenate([np.arange(x, z) for x, z in zip(lo, hi)] + [np.zeros(0, np.int64)]).astype(np.int64)
+    col = _np(csr.col_idx)[idx].astype(np.int64)
+    return idx, np.repeat(np.arange(T), hi - lo), col, hi - lo
 
-    for b in (0, 137, 255):
+
+def _pin_dw(trace, csr, n_out, picks, what):
+    """The dW call of the bench (structure-only layout, then the call with the gradients) on the
+    full-size trace and CSR, with eps zero at every entry but the sampled ones, which carry eps
+    from the oracle. Samples add up in dW, so the result is the sum of the oracle's per-sample dW,
+    checked element by element within the summed envelope.
+    picks: list of (idx, eps, dW, env) per sample: CSR positions and the oracle's eps there, and the
+    oracle's dW and its envelope for that sample alone, all scaled to the batch mean."""
+    T, B, n_in = trace.shape
+    eps = torch.zeros(max(csr.capacity, 1), dtype=torch.float32, device=trace.device)
+    idx = np.concatenate([p[0] for p in picks])
+    val = np.concatenate([p[1] for p in picks]).astype(np.float32)
+    eps[torch.from_numpy(idx).to(trace.device)] = torch.from_numpy(val).to(trace.device)
+    ws = snn.workspace(snn.snn_sparse_dw_workspace(T, B, n_in, n_out, csr.capacity))
+    snn.sparse_dw_layout((T, B, n_in), csr, n_out, ws)
+    dW = snn.sparse_dw_prepared(trace, csr, eps, n_out, ws)
+    ref = sum(p[2] for p in picks)
+    env = sum(p[3] for p in picks)
+    assert np.abs(ref).max() > 0, what
+    assert_env(_np(dW), ref, env, what)
+
+
+def _full_size_check(cfg, b_th, net, ro, csrs, eps_l, samples):
+    """Per sampled b, against the oracle run on sample b alone (samples are independent in the
+    forward, the compaction and the spike gradient; its loss gradient scaled by 1/B): V, spikes,
+    traces, CSR rows and g bit-exact or to float32 rounding, eps of every layer within the
+    envelope. Then every dW (the readout's too) pinned to the oracle through _pin_dw."""
+    T, B, L = net.T, net.B, net.L
+    picks = [[] for _ in range(L + 1)]
+    for b in samples:
         sub = make_inputs(cfg, [b])
         f = oracle.network_forward(sub.X, sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, np.float32(cfg.theta))
         args = (sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, sub.labels, cfg.loss_mode, cfg.theta, b_th, cfg.beta)
         r = oracle.network_backward(f, *args)
         env = oracle.network_backward(f, *args, absolute=True)
+        assert_bits(_np(net.V_out[:, b]), f["V_out"][:, 0], f"V_out b={b}")
         for l in range(L):
             assert_bits(_np(net.V[l][:, b]), f["V"][l][:, 0], f"V[{l}] b={b}")
             assert_bits(_np(net.S[l][:, b]), f["S"][l][:, 0], f"S[{l}] b={b}")
             assert_bits(_np(net.trace[l][:, b]), f["trace"][l][:, 0], f"trace[{l}] b={b}")
-            rp = _np(csrs[l].row_ptr).astype(np.int64)
-            rows = np.arange(T) * B + b
-            lo, hi = rp[rows], rp[rows + 1]
-            ref_rp, ref_ci, _ = oracle.active_csr(f["V"][l], cfg.theta, b_th, cfg.beta)
-            assert_bits(hi - lo, np.diff(ref_rp).astype(np.int64), f"row counts[{l}] b={b}")
-            idx = np.concatenate([np.arange(a, z) for a, z in zip(lo, hi)]).astype(np.int64)
-            col = _np(csrs[l].col_idx)[idx].astype(np.int64)
+            idx, t_of, col, counts = _sample_entries(csrs[l], T, B, b)
+            ref_rp, ref_ci, ref_g = oracle.active_csr(f["V"][l], cfg.theta, b_th, cfg.beta)
+            assert_bits(counts, np.diff(ref_rp).astype(np.int64), f"row counts[{l}] b={b}")
             assert_bits(col, ref_ci.astype(np.int64), f"col_idx[{l}] b={b}")
-            t_of = np.repeat(np.arange(T), hi - lo)
-            got = _np(eps_l[l])[idx].astype(F64)
-            assert_env(got, r["eps"][l][t_of, 0, col] / B, env["eps"][l][t_of, 0, col] / B, f"eps[{l}] b={b}")
+            g = _np(csrs[l].g)[idx].astype(F64)
+            assert np.allclose(g, ref_g, rtol=2e-6, atol=0), f"g[{l}] b={b}"
+            ref_e = r["eps"][l][t_of, 0, col] / B
+            assert_env(_np(eps_l[l])[idx].astype(F64), ref_e, env["eps"][l][t_of, 0, col] / B, f"eps[{l}] b={b}")
+            picks[l].append((idx, ref_e, r["dW"][l] / B, env["dW"][l] / B))
+        # the readout's read entries of sample b and dL/da there
+        rro = r["readout"]
+        idx, t_of, col, counts = _sample_entries(ro[0], T, B, b)
+        assert_bits(counts, np.diff(rro["row_ptr"]).astype(np.int64), f"readout row counts b={b}")
+        assert_bits(col, rro["col_idx"], f"readout col_idx b={b}")
+        env_ro = oracle.csr_values(rro["G_abs"], rro["row_ptr"], rro["col_idx"])
+        assert_env(_np(ro[1])[idx].astype(F64), rro["eps"] / B, env_ro / B, f"readout eps b={b}")
+        picks[L].append((idx, rro["eps"] / B, r["dW_out"] / B, env["dW_out"] / B))
     for l in range(L):
+        _pin_dw(net.trace[l], csrs[l], net.Ws[l].shape[1], picks[l], f"dW[{l}] of samples {samples}")
+    _pin_dw(net.trace_out, ro[0], net.W_out.shape[1], picks[L], f"dW_out of samples {samples}")
+
+
+def test_full_size_stress_sampled():
+    """The stress workload at full size (T=500, B=256, 3 x 1024) in the bench's launch
+    configuration: the spike-gradient chain on one stream, every layer's dW (structure-only layout
+    first) on a second stream. Sampled b checked against the oracle run on sample b alone, and each
+    dW call of the bench's plan pinned to the oracle's dW of the sampled samples."""
+    cfg = CONFIGS["stress"]
+    b_th = cfg.b_th
+    print(f"\n[case] full-size stress b_th={b_th}", flush=True)
+    inp = make_inputs(cfg)
+    net = pipeline.from_inputs(inp).forward(b_th)
+    ro = net.readout(dense=True)
+    csrs = net.compact(b_th)
+    dW, dW_out, eps_l = net.sparse_backward(csrs, ro, aux_stream=torch.cuda.Stream())
+    ddW, _, _ = net.dense_backward(b_th, ro)
+    torch.cuda.synchronize()
+    assert (net.T, net.B) == (500, 256)
+    _full_size_check(cfg, b_th, net, ro, csrs, eps_l, (0, 137, 255))
+    # the full batch's dW against the dense matrix-core chain (itself pinned on the smaller cases)
+    for l in range(net.L):
         x, y = _np(dW[l]).astype(F64), _np(ddW[l]).astype(F64)
         bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
         assert not bad.any(), f"dW[{l}]: {int(bad.sum())} elements differ from the dense path"
@@ -382,45 +421,20 @@ def test_full_size_sampled(name, b_th):
     """Every other fully connected workload at its full size (B = 256, its own T and widths),
     through Network.sparse_backward with an auxiliary stream: the launch configuration of the
     bench (the pipelined schedule for the five-layer network, the readout's spike gradient beside
-    its dW for one LIF layer). Sampled b checked against the oracle run on sample b alone, as for
-    the stress workload: V, spikes, traces, CSR rows and g bit-exact or to float32 rounding, eps
-    of every layer within the envelope; dW, a sum over all samples, against the dense chain."""
+    its dW for one LIF layer). Sampled b checked against the oracle as for the stress workload,
+    each dW call pinned to the oracle's dW of the sampled samples."""
     cfg = CONFIGS[name]
     print(f"\n[case] full-size {name} b_th={b_th}", flush=True)
     inp = make_inputs(cfg)
-    net = pipeline.from_inputs(inp).forward()
+    net = pipeline.from_inputs(inp).forward(b_th)
     ro = net.readout(dense=True)
     csrs = net.compact(b_th)
     dW, dW_out, eps_l = net.sparse_backward(csrs, ro, aux_stream=torch.cuda.Stream())
     ddW, ddW_out, _ = net.dense_backward(b_th, ro)
     torch.cuda.synchronize()
-    T, B, L = net.T, net.B, net.L
-    assert B == 256
-    for b in (0, 101, 255):
-        sub = make_inputs(cfg, [b])
-        f = oracle.network_forward(sub.X, sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, np.float32(cfg.theta))
-        args = (sub.Ws, sub.W_out, sub.alphas, sub.alpha_out, sub.labels, cfg.loss_mode, cfg.theta, b_th, cfg.beta)
-        r = oracle.network_backward(f, *args)
-        env = oracle.network_backward(f, *args, absolute=True)
-        assert_bits(_np(net.V_out[:, b]), f["V_out"][:, 0], f"V_out b={b}")
-        for l in range(L):
-            assert_bits(_np(net.V[l][:, b]), f["V"][l][:, 0], f"V[{l}] b={b}")
-            assert_bits(_np(net.S[l][:, b]), f["S"][l][:, 0], f"S[{l}] b={b}")
-            assert_bits(_np(net.trace[l][:, b]), f["trace"][l][:, 0], f"trace[{l}] b={b}")
-            rp = _np(csrs[l].row_ptr).astype(np.int64)
-            rows = np.arange(T) * B + b
-            lo, hi = rp[rows], rp[rows + 1]
-            ref_rp, ref_ci, ref_g = oracle.active_csr(f["V"][l], cfg.theta, b_th, cfg.beta)
-            assert_bits(hi - lo, np.diff(ref_rp).astype(np.int64), f"row counts[{l}] b={b}")
-            idx = np.concatenate([np.arange(a, z) for a, z in zip(lo, hi)] + [np.zeros(0, np.int64)]).astype(np.int64)
-            col = _np(csrs[l].col_idx)[idx].astype(np.int64)
-            assert_bits(col, ref_ci.astype(np.int64), f"col_idx[{l}] b={b}")
-            g = _np(csrs[l].g)[idx].astype(F64)
-            assert np.allclose(g, ref_g, rtol=2e-6, atol=0), f"g[{l}] b={b}"
-            t_of = np.repeat(np.arange(T), hi - lo)
-            got = _np(eps_l[l])[idx].astype(F64)
-            assert_env(got, r["eps"][l][t_of, 0, col] / B, env["eps"][l][t_of, 0, col] / B, f"eps[{l}] b={b}")
-    for x, y, what in [(dW[l], ddW[l], f"dW[{l}]") for l in range(L)] + [(dW_out, ddW_out, "dW_out")]:
+    assert net.B == 256
+    _full_size_check(cfg, b_th, net, ro, csrs, eps_l, (0, 101, 255))
+    for x, y, what in [(dW[l], ddW[l], f"dW[{l}]") for l in range(net.L)] + [(dW_out, ddW_out, "dW_out")]:
         x, y = _np(x).astype(F64), _np(y).astype(F64)
         assert np.abs(y).max() > 0, what
         bad = np.abs(x - y) > 1e-4 * (np.abs(x) + np.abs(y)) + 1e-5 * np.abs(y).max()
