@@ -117,6 +117,21 @@ snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, 
                                    size_t workspace_bytes, void* stream);
 
 /*
+ * snn_active_compact_bits without a workspace argument and without any allocation, for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments (minus workspace) and results. The row
+ * counts and scan temporaries live in a device array of the library, 8 MiB, one per GPU, held
+ * until the process ends; its address is looked up on the first call on each device.
+ *   SNN_ERR_UNSUPPORTED when snn_active_compact_bits_workspace(T, B, N) exceeds 8 MiB (about
+ *   T*B > 2,000,000 rows); SNN_ERR_HIP when the array's address cannot be had.
+ * Every call on one GPU shares that array: calls that overlap on a GPU (on different streams or
+ * host threads) race and give wrong results; calls in order on one stream are safe.
+ */
+snn_status snn_active_compact_bits_noalloc(const uint64_t* active_bits, const float* V, int T, int B, int N,
+                                           float theta, float beta, int32_t* row_ptr, int32_t* col_idx,
+                                           float* g_act, int64_t capacity, int64_t* nnz_dev, void* stream);
+
+/*
  * Sparse backward of one layer (Sec. 2.2: sparse dW and sparse spike gradient, Proposition 1).
  *   W          [N_in,N_out] float32 (read)
  *   trace_in   [T,B,N_in]  float32 input trace from snn_lif_forward (read)

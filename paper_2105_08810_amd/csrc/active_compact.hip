@@ -14,6 +14,8 @@
 // subtraction, then fabs and a strict compare), so the integer outputs are bit-exact.
 #include "common.h"
 
+#include <mutex>
+
 namespace snn {
 namespace {
 
@@ -322,17 +324,26 @@ extern "C" size_t snn_active_compact_bits_workspace(int T, int B, int N) {
   return c.off;
 }
 
-extern "C" snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, int T, int B, int N,
-                                              float theta, float beta, int32_t* row_ptr, int32_t* col_idx,
-                                              float* g_act, int64_t capacity, int64_t* nnz_dev, void* workspace,
-                                              size_t workspace_bytes, void* stream) {
-  if (!active_bits || !row_ptr || !nnz_dev || !workspace) return SNN_ERR_INVALID_ARG;
-  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return SNN_ERR_INVALID_ARG;
-  if (isnan(theta) || isnan(beta) || beta < 0.0f) return SNN_ERR_INVALID_ARG;
-  if (capacity < 0 || (capacity > 0 && !col_idx) || (g_act && !V)) return SNN_ERR_INVALID_ARG;
-  if (workspace_bytes < snn_active_compact_bits_workspace(T, B, N)) return SNN_ERR_INVALID_ARG;
+namespace snn {
+namespace {
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
+// Validation shared by snn_active_compact_bits and its allocation-free form.
+bool compact_bits_args_ok(const uint64_t* active_bits, const float* V, int T, int B, int N, float theta, float beta,
+                          const int32_t* row_ptr, const int32_t* col_idx, const float* g_act, int64_t capacity,
+                          const int64_t* nnz_dev) {
+  if (!active_bits || !row_ptr || !nnz_dev) return false;
+  if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return false;
+  if (isnan(theta) || isnan(beta) || beta < 0.0f) return false;
+  if (capacity < 0 || (capacity > 0 && !col_idx) || (g_act && !V)) return false;
+  return true;
+}
+
+// The count, scan and fill passes, with the row counts and scan temporaries in `workspace`
+// (at least snn_active_compact_bits_workspace bytes; every byte used is written before it is
+// read, so it needs no clearing).
+snn_status enqueue_compact_bits(const uint64_t* active_bits, const float* V, int T, int B, int N, float theta,
+                                float beta, int32_t* row_ptr, int32_t* col_idx, float* g_act, int64_t capacity,
+                                int64_t* nnz_dev, void* workspace, hipStream_t s) {
   const int rows = T * B;
   Carve ws(workspace);
   int32_t* counts = ws.take<int32_t>(rows);
@@ -347,4 +358,64 @@ extern "C" snn_status snn_active_compact_bits(const uint64_t* active_bits, const
     hipLaunchKernelGGL(bits_fill, grid, dim3(kThreads), 0, s, active_bits, V, T, B, N, rpw, theta, beta, row_ptr,
                        col_idx, g_act, capacity);
   return launch_status();
+}
+
+}  // namespace
+}  // namespace snn
+
+extern "C" snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, int T, int B, int N,
+                                              float theta, float beta, int32_t* row_ptr, int32_t* col_idx,
+                                              float* g_act, int64_t capacity, int64_t* nnz_dev, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  if (!workspace) return SNN_ERR_INVALID_ARG;
+  if (!compact_bits_args_ok(active_bits, V, T, B, N, theta, beta, row_ptr, col_idx, g_act, capacity, nnz_dev))
+    return SNN_ERR_INVALID_ARG;
+  if (workspace_bytes < snn_active_compact_bits_workspace(T, B, N)) return SNN_ERR_INVALID_ARG;
+  return enqueue_compact_bits(active_bits, V, T, B, N, theta, beta, row_ptr, col_idx, g_act, capacity, nnz_dev,
+                              workspace, static_cast<hipStream_t>(stream));
+}
+
+// ------------------------------------------------------------------ allocation-free form
+//
+// The workspace of snn_active_compact_bits_noalloc is a file-scope device array: one copy per
+// GPU, part of the code object's memory, held until the process ends. Host code never passes the
+// array's name to a kernel (on the host it names a stand-in, not device memory): the device
+// address is looked up once per device, with that device current, and kept.
+namespace snn {
+namespace {
+
+constexpr size_t kNoAllocScratchBytes = size_t(8) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device (nullptr if it cannot be had).
+void* scratch_on_current_device() {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    addr[dev] = p;
+  }
+  return addr[dev];
+}
+
+}  // namespace
+}  // namespace snn
+
+extern "C" snn_status snn_active_compact_bits_noalloc(const uint64_t* active_bits, const float* V, int T, int B,
+                                                      int N, float theta, float beta, int32_t* row_ptr,
+                                                      int32_t* col_idx, float* g_act, int64_t capacity,
+                                                      int64_t* nnz_dev, void* stream) {
+  if (!compact_bits_args_ok(active_bits, V, T, B, N, theta, beta, row_ptr, col_idx, g_act, capacity, nnz_dev))
+    return SNN_ERR_INVALID_ARG;
+  if (snn_active_compact_bits_workspace(T, B, N) > kNoAllocScratchBytes) return SNN_ERR_UNSUPPORTED;
+  void* ws = scratch_on_current_device();
+  if (!ws) return SNN_ERR_HIP;
+  return enqueue_compact_bits(active_bits, V, T, B, N, theta, beta, row_ptr, col_idx, g_act, capacity, nnz_dev, ws,
+                              static_cast<hipStream_t>(stream));
 }

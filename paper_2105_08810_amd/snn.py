@@ -39,6 +39,7 @@ _SIGNATURES = {
     "snn_lif_forward_active": (_I, [_P, _P, _I, _I, _I, _I, _F, _F, _F, _P, _P, _P, _P, _P]),
     "snn_active_compact_bits_workspace": (_SZ, [_I, _I, _I]),
     "snn_active_compact_bits": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
+    "snn_active_compact_bits_noalloc": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P]),
     "snn_sparse_dw_workspace": (_SZ, [_I, _I, _I, _I, _I64]),
     "snn_sparse_dw": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_sparse_dw_layout": (_I, [_I, _I, _I, _I, _P, _P, _I64, _P, _SZ, _P]),
@@ -157,6 +158,14 @@ def snn_active_compact_bits(active_bits, V, T, B, N, theta, beta, row_ptr, col_i
         float(beta), _ptr(row_ptr, torch.int32, "row_ptr"), _ptr(col_idx, torch.int32, "col_idx"),
         _ptr(g_act, torch.float32, "g_act"), int(capacity), _ptr(nnz_dev, torch.int64, "nnz"),
         _ptr(ws, None, "workspace"), 0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def snn_active_compact_bits_noalloc(active_bits, V, T, B, N, theta, beta, row_ptr, col_idx, g_act, capacity,
+                                    nnz_dev, stream=None):
+    _check("snn_active_compact_bits_noalloc", lib().snn_active_compact_bits_noalloc(
+        _ptr(active_bits, torch.int64, "active_bits"), _ptr(V, torch.float32, "V"), T, B, N, float(theta),
+        float(beta), _ptr(row_ptr, torch.int32, "row_ptr"), _ptr(col_idx, torch.int32, "col_idx"),
+        _ptr(g_act, torch.float32, "g_act"), int(capacity), _ptr(nnz_dev, torch.int64, "nnz"), _stream(stream)))
 
 
 def snn_active_compact_workspace(T, B, N) -> int:

@@ -278,6 +278,29 @@ def test_compact_bits_v_optional_without_g(lib):
     assert lib.snn_active_compact_bits_workspace(10, 4, 16) > 0
 
 
+def _cbn(lib, **kw):
+    a = dict(bits=FAKE, V=FAKE, T=10, B=4, N=16, theta=1.0, beta=100.0, rp=FAKE, ci=FAKE, g=FAKE, cap=100, nnz=FAKE)
+    a.update(kw)
+    return lib.snn_active_compact_bits_noalloc(a["bits"], a["V"], a["T"], a["B"], a["N"], a["theta"], a["beta"],
+                                               a["rp"], a["ci"], a["g"], a["cap"], a["nnz"], None)
+
+
+@pytest.mark.parametrize("kw", [dict(bits=None), dict(rp=None), dict(nnz=None), dict(cap=-1), dict(ci=None),
+                                dict(V=None), dict(beta=NAN), dict(theta=NAN), dict(N=0), dict(T=-1)])
+def test_compact_bits_noalloc_rejects(lib, kw):
+    assert _cbn(lib, **kw) == snn.SNN_ERR_INVALID_ARG
+
+
+def test_compact_bits_noalloc_size_limit(lib):
+    # the library's device array holds 8 MiB: the row counts and scan temporaries of at most
+    # about 2e6 rows; larger inputs are refused before any HIP call
+    limit = 8 << 20
+    assert lib.snn_active_compact_bits_workspace(2000, 1000, 64) <= limit
+    assert lib.snn_active_compact_bits_workspace(3000, 1000, 64) > limit
+    assert _cbn(lib, T=3000, B=1000, N=64) == snn.SNN_ERR_UNSUPPORTED
+    assert _cbn(lib, T=100000, B=100000, N=64) == snn.SNN_ERR_INVALID_ARG  # T*B past int32, as for the other form
+
+
 def _reg(lib, **kw):
     a = dict(S=FAKE, T=10, B=4, N=16, ll=100.0, nl=0.001, lu=0.06, nu=1.0, zeta=FAKE, coef=FAKE, pen=FAKE, ws=FAKE,
              ws_bytes=1 << 30)
