@@ -579,28 +579,35 @@ class Runner:
 
     def _layers_pipelined(self, ev, r, cs, K):
         """The spike gradients form a chain (each layer's needs the one above); a layer's dW needs only
-        its own eps. The chain runs on main and every dW on a dW stream as soon as its eps is there,
-        so the dW calls (the longer job) run back to back beside the chain."""
-        snn, net, main, dws, R = self.snn, self.net, self.main, self.aux, self.region
+        its own eps, and its structure-only layout only the active sets. The layouts run on a side
+        stream from the start, beside the readout's spike gradient. When one dW call fills the GPU
+        (big layers), the dW calls then run on main between the spike gradients; for small layers
+        each dW runs on a dW stream as soon as its eps is there, beside the chain."""
+        snn, net, main, side, R = self.snn, self.net, self.main, self.aux, self.region
         T, B, L = self.T, self.B, self.L
         self.cs = cs
-        # dW streams taken in turn by layer: a layer's dW starts as soon as its eps is there, not
-        # after the previous layer's dW (its final chunk reduction, or a small layer's whole call)
-        dw_streams = ([dws] + self.dw_extra)[:self.n_dw]
+        inline = self.n_dw == 1  # one dW call fills the GPU
+        dw_streams = [main] if inline else ([side] + self.dw_extra)[:self.n_dw]
         eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
-                                                         share_cu=False, ws=self.ws_gi, eps_in=self.eps[L - 1]))
+                                                         share_cu=not inline, ws=self.ws_gi, eps_in=self.eps[L - 1]))
         ev["ro1"].record(main)
-        # From here on every kernel is LIF-layer work (timed). A layer's structure-only dW part goes
-        # first on its dW stream (it needs no eps), where it overlaps the work of the layer above.
-        for sd in dw_streams:
-            sd.wait_stream(main)
+        # From here on every kernel is LIF-layer work (timed); the layouts start here too, so that
+        # none of them hides behind the readout's spike gradient.
+        side.wait_stream(main)
+        laid = [None] * L
+        if not K:
+            for l in range(L - 1, -1, -1):  # top layer first: its dW comes first
+                R(f"lay{l}", side, lambda l=l: snn.sparse_dw_layout((T, B, self.sizes[l]), cs[l], self.sizes[l + 1],
+                                                                   self.ws_dw[l]))
+                laid[l] = self.torch.cuda.Event()
+                laid[l].record(side)
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
             sd = dw_streams[i % len(dw_streams)]
-            if not K:
-                R(f"lay{l}", sd, lambda l=l: snn.sparse_dw_layout((T, B, self.sizes[l]), cs[l], self.sizes[l + 1],
-                                                                   self.ws_dw[l]))
-            sd.wait_stream(main)  # eps of layer l is ready
+            if sd is not main:
+                sd.wait_stream(main)  # eps of layer l is ready
+            if laid[l] is not None:
+                sd.wait_event(laid[l])
             ev["lay0"][i].record(sd)
             ev["dw0"][i].record(sd)
             R(f"dw{l}", sd, self._dw_call(l, eps, K, prepared=not K))
@@ -608,11 +615,12 @@ class Runner:
             ev["lay1"][i].record(sd)
             if l > 0:
                 ev["gi0"][i].record(main)
-                R(f"gi{l}", main, self._gi_call(l, eps, True))
+                R(f"gi{l}", main, self._gi_call(l, eps, not inline))
                 ev["gi1"][i].record(main)
                 eps = self.eps[l - 1]
-        for sd in dw_streams:
-            main.wait_stream(sd)
+        for sd in [side] + dw_streams:
+            if sd is not main:
+                main.wait_stream(sd)
         ev["bw1"].record(main)  # end of the LIF layers' backward
         # the readout's dW, outside the measured chain (as the readout's loss and forward are)
         R("ro_dw", main, lambda: snn.sparse_dw(net.trace_out, r[0], r[1], net.W_out.shape[1], ws=self.ws_ro,
@@ -807,8 +815,9 @@ class Runner:
             "roofline": {
                 "bound": "hbm", "achieved": dw_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": dw_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                "kernel": ("snn_sparse_dw_prepared (mdw_gate + mdw_kernel + mdw_reduce) of each LIF layer; its "
-                           "structure-only layout runs earlier, beside the layer above" if self.pipelined and use_aux
+                "kernel": ("snn_sparse_dw_prepared (mdw_gate + mdw_kernel + mdw_reduce) of each LIF layer; the "
+                           "structure-only layouts run on a side stream inside the timed chain" if self.pipelined
+                           and use_aux
                            else "snn_sparse_dw (layout + mdw_gate + mdw_kernel + mdw_reduce) of each LIF layer"),
                 "algorithmic_bytes_per_launch": dw_bytes / L, "algorithmic_flops_per_launch": dw_flops / L,
                 "launches": L, "launch_ms": dw_ms,
@@ -860,6 +869,9 @@ def build_parser() -> argparse.ArgumentParser:
                     help="compaction reads V instead of the active bitsets the forward marks")
     ap.add_argument("--sweep", action="store_true", help="one JSON line per B_th of the workload's sweep")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB")
+    ap.add_argument("--no-memory", action="store_true",
+                    help="skip the allocator-peak memory measurement after the timed steps (for counter runs that "
+                         "should hold the timed step's dispatches only)")
     ap.add_argument("--schedule", choices=("auto", "pipelined", "layerwise"), default="auto",
                     help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
                          "or layer by layer (auto: pipelined for two or more LIF layers)")
@@ -910,9 +922,10 @@ def main():
         dense = not args.no_dense and (k == 0 or not args.sweep)  # the dense chain's cost does not depend on B_th
         evs, cs, wall = run.run(args.steps, args.warmup, dense)
         out = run.summarize(evs, cs, wall, dense)
-        mem = run.measured_memory()
-        out["memory_saved_pct"] = [m[2] for m in mem]
-        out["backward_peak_bytes_sparse_dense"] = [[m[0], m[1]] for m in mem]
+        if not args.no_memory:
+            mem = run.measured_memory()
+            out["memory_saved_pct"] = [m[2] for m in mem]
+            out["backward_peak_bytes_sparse_dense"] = [[m[0], m[1]] for m in mem]
         if dense:
             dense_ms = out["dense_backward_ms"]
         elif dense_ms is not None:

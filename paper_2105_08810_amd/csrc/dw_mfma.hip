@@ -23,7 +23,9 @@
 // record area is processed in several rounds of whole quads.
 //
 // Blocks: (input tile of 64 inputs) x (chunk of windows); each block writes a partial dW for its
-// chunk; the partials are summed in a fixed order in float64, so dW is bitwise reproducible.
+// chunk with columns in slot order (a wavefront's 64 slots are contiguous, so the stores coalesce);
+// mdw_reduce sums the partials in a fixed order in float64 and puts each column in its place, so
+// dW is bitwise reproducible.
 #include "common.h"
 #include <climits>
 
@@ -243,7 +245,8 @@ __global__ void mdw_gate(const int32_t* __restrict__ qoff, int64_t cap, const in
 __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict__ trace, int TB, int N_in, int N_out,
                                                         const int32_t* __restrict__ qoff, const int2* __restrict__ rec,
                                                         const int32_t* __restrict__ inv, int64_t cap, int n_win,
-                                                        int wpc, int n_itiles, float* __restrict__ part) {
+                                                        int wpc, int n_itiles, float* __restrict__ part,
+                                                        bool chunked) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int it, ch;
   if ((gridDim.x & 7) == 0 && ((gridDim.x >> 3) % n_itiles) == 0) {
@@ -268,10 +271,10 @@ __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict_
   // Direct loads of window win into buffer bi: its trace rows (input tile it; lanes past the row's
   // 64 inputs fill the padding), its first round of sorted entries and its qoff row. Every source
   // address is clamped into its array.
-  auto stage = [&](int bi, int win) {
+  // e_lo / e_hi: the window's entry range (read before the loads are issued: a later global read
+  // would wait for them too, vmcnt being in order).
+  auto stage = [&](int bi, int win, int e_lo, int e_hi) {
     const unsigned base = lds0 + (unsigned)(bi * kMBuf);
-    const int e_lo = clampi(qoff[(size_t)win * kMQLd], cap);
-    const int e_hi = max(e_lo, clampi(qoff[(size_t)win * kMQLd + kMQ], cap));
     if (e_hi == e_lo) return;
     const int r0 = win * kMRW;
     const int nrows = min(kMRW, TB - r0);
@@ -300,15 +303,38 @@ __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict_
     }
   };
 
-  if (wlo < whi) stage(0, wlo);
+  // Entry ranges of the chunk's windows, 64 at a time: lane l holds window wlo + 64 g + l. A group
+  // is loaded right after a barrier, before any staging load is in flight.
+  int rng_lo = 0, rng_hi = 0;
+  auto range_of = [&](int win, int& lo, int& hi) {
+    const int rel = win - wlo;
+    if ((rel & (kWave - 1)) == 0) {
+      const int wv = win + l;
+      const int a = wv < whi ? clampi(qoff[(size_t)wv * kMQLd], cap) : 0;
+      rng_lo = a;
+      rng_hi = wv < whi ? max(a, clampi(qoff[(size_t)wv * kMQLd + kMQ], cap)) : 0;
+    }
+    lo = __builtin_amdgcn_readlane(rng_lo, rel & (kWave - 1));
+    hi = __builtin_amdgcn_readlane(rng_hi, rel & (kWave - 1));
+  };
+  int cur_lo = 0, cur_hi = 0;
+  if (wlo < whi) {
+    range_of(wlo, cur_lo, cur_hi);
+    stage(0, wlo, cur_lo, cur_hi);
+  }
   for (int win = wlo; win < whi; ++win) {
     const int bi = (win - wlo) & 1;
     char* buf = smem + bi * kMBuf;
     mdw_wait_dma();
     __syncthreads();
-    if (win + 1 < whi) stage(bi ^ 1, win + 1);
-    const int e_lo = clampi(qoff[(size_t)win * kMQLd], cap);
-    const int e_hi = max(e_lo, clampi(qoff[(size_t)win * kMQLd + kMQ], cap));
+    int nxt_lo = 0, nxt_hi = 0;
+    if (win + 1 < whi) {
+      range_of(win + 1, nxt_lo, nxt_hi);
+      stage(bi ^ 1, win + 1, nxt_lo, nxt_hi);
+    }
+    const int e_lo = cur_lo, e_hi = cur_hi;
+    cur_lo = nxt_lo;
+    cur_hi = nxt_hi;
     if (e_hi > e_lo) {
       const int* qs = reinterpret_cast<const int*>(buf + kMTr + kMRecB);
       const char* lb = buf + 16 * t;
@@ -372,28 +398,48 @@ __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict_
   }
   // C[4q + u] register v, lane 4b + j: input i0 + 16q + 4v + u, column slot 64w + 4b + j (column inv[slot])
   const int slot = kWave * w + l;
-  const int col = slot < 4 * ((N_out + 3) / 4) ? inv[slot] : -1;
-  if (col >= 0 && col < N_out) {
-    float* dst = part + (size_t)ch * N_in * N_out;
+  const int S = 4 * ((N_out + 3) / 4);  // column slots per row
+  if (chunked) {  // partial of chunk ch, rows of S slots (mdw_reduce applies the column order)
+    float* dst = part + (size_t)ch * N_in * S;
+    if (slot < S) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int i = i0 + 16 * q + 4 * v + u;
-          if (i < N_in) dst[(size_t)i * N_out + col] = C[4 * q + u][v];
-        }
+          for (int v = 0; v < 4; ++v) {
+            const int i = i0 + 16 * q + 4 * v + u;
+            if (i < N_in) dst[(size_t)i * S + slot] = C[4 * q + u][v];
+          }
+    }
+  } else {  // one chunk: straight into dW, column inv[slot]
+    const int col = slot < S ? inv[slot] : -1;
+    if (col >= 0 && col < N_out) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int i = i0 + 16 * q + 4 * v + u;
+            if (i < N_in) part[(size_t)i * N_out + col] = C[4 * q + u][v];
+          }
+    }
   }
 }
 
 // dW = sum of the chunk partials in chunk order, float64 (deterministic); 256 outputs per block.
-__global__ __launch_bounds__(256) void mdw_reduce(const float* __restrict__ part, int n_chunks, int64_t n,
-                                                  float* __restrict__ out) {
+// Partials are rows of S column slots; output column c reads slot perm[c].
+__global__ __launch_bounds__(256) void mdw_reduce(const float* __restrict__ part, int n_chunks, int N_in, int N_out,
+                                                  int S, const int32_t* __restrict__ perm, float* __restrict__ out) {
   const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (k >= n) return;
+  if (k >= (int64_t)N_in * N_out) return;
+  const int64_t i = k / N_out;
+  const int c = (int)(k - i * N_out);
+  const int slot = min(max(perm[c], 0), S - 1);
+  const int64_t n = (int64_t)N_in * S;
   double s = 0.0;
-  for (int c = 0; c < n_chunks; ++c) s += (double)part[(int64_t)c * n + k];
+  for (int ch = 0; ch < n_chunks; ++ch) s += (double)part[ch * n + i * S + slot];
   out[k] = (float)s;
 }
 
@@ -423,7 +469,7 @@ MdwPlan plan_mdw(int T, int B, int N_in, int N_out) {
 size_t mdw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
   const MdwPlan p = plan_mdw(T, B, N_in, N_out);
   Carve c(nullptr);
-  if (p.n_chunks > 1) c.take<float>((size_t)p.n_chunks * N_in * N_out);
+  if (p.n_chunks > 1) c.take<float>((size_t)p.n_chunks * N_in * (4 * ((N_out + 3) / 4)));
   c.take<int32_t>((size_t)p.n_win * kMQLd);
   c.take<int2>((size_t)out_cap + 4);
   c.take<int32_t>((size_t)out_cap + 1);
@@ -446,7 +492,7 @@ struct MdwBufs {
 MdwBufs mdw_bufs(const MdwPlan& p, int N_in, int N_out, int64_t out_cap, void* workspace, float* dW) {
   Carve ws(workspace);
   MdwBufs b{};
-  b.part = p.n_chunks > 1 ? ws.take<float>((size_t)p.n_chunks * N_in * N_out) : dW;
+  b.part = p.n_chunks > 1 ? ws.take<float>((size_t)p.n_chunks * N_in * (4 * ((N_out + 3) / 4))) : dW;
   b.qoff = ws.take<int32_t>((size_t)p.n_win * kMQLd);
   b.rec = ws.take<int2>((size_t)out_cap + 4);
   b.src = ws.take<int32_t>((size_t)out_cap + 1);
@@ -478,10 +524,12 @@ void mdw_enqueue_rest(const float* trace_in, int T, int B, int N_in, int N_out, 
   hipLaunchKernelGGL(mdw_gate, dim3((unsigned)p.n_win), dim3(256), 0, s, b.qoff, out_cap, b.src, out_g, eps_out, b.rec);
   ensure_dynamic_lds((const void*)mdw_kernel, 2 * kMBuf);
   hipLaunchKernelGGL(mdw_kernel, dim3((unsigned)(p.n_itiles * p.n_chunks)), dim3(kMThreads), 2 * kMBuf, s, trace_in,
-                     T * B, N_in, N_out, b.qoff, b.rec, b.inv, out_cap, p.n_win, p.wpc, p.n_itiles, b.part);
+                     T * B, N_in, N_out, b.qoff, b.rec, b.inv, out_cap, p.n_win, p.wpc, p.n_itiles, b.part,
+                     p.n_chunks > 1);
   if (p.n_chunks > 1) {
     const int64_t n = (int64_t)N_in * N_out;
-    hipLaunchKernelGGL(mdw_reduce, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, b.part, p.n_chunks, n, dW);
+    hipLaunchKernelGGL(mdw_reduce, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, b.part, p.n_chunks, N_in, N_out,
+                       4 * ((N_out + 3) / 4), b.perm, dW);
   }
 }
 

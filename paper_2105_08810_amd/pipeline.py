@@ -150,27 +150,30 @@ class Network:
 
     def _sparse_backward_pipelined(self, csrs, ro_csr, ro_eps, aux, reg_coefs=None):
         """The spike gradients form a chain down the layers (each needs the one above), while a
-        layer's dW needs only its own eps: the chain runs on the current stream and every dW on
-        aux as soon as its eps is there, so the dW calls run back to back beside the chain."""
+        layer's dW needs only its own eps, and the structure-only part of every dW call needs only
+        the active sets. The layouts run on aux from the start, beside the readout's backward.
+        When a dW call fills the GPU by itself (big layers), the dW calls then run on the current
+        stream between the spike gradients (a dW beside a spike gradient would only take CUs
+        from it); for small layers every dW runs on a dW stream as soon as its eps is there, beside
+        the chain."""
         main = torch.cuda.current_stream()
         T, B, L = self.T, self.B, self.L
-        # dW streams taken in turn by layer, so that a layer's dW can start beside the previous
-        # layer's: two for small layers; one when each dW call fills the GPU by itself
         big = max(csrs[l].capacity * self.Ws[l].shape[0] for l in range(L)) >= 10 ** 9  # multiply-adds
         if not big and self._aux2 is None:
             self._aux2 = torch.cuda.Stream()  # default priority
-        streams = [aux] if big else [aux, self._aux2]
+        streams = [main] if big else [aux, self._aux2]
         aux.wait_stream(main)  # the active sets are ready: the dW parts that need only them start on aux
-        wss = []
+        wss, laid = [], []
         with torch.cuda.stream(aux):
-            for l in range(L):
+            for l in range(L - 1, -1, -1):  # top layer first: its dW comes first
                 n_in, n_out = self.Ws[l].shape
                 ws = snn.workspace(snn.snn_sparse_dw_workspace(T, B, n_in, n_out, csrs[l].capacity), self.X.device)
                 snn.sparse_dw_layout((T, B, n_in), csrs[l], n_out, ws, stream=aux)
-                wss.append(ws)
-        for sd in streams[1:]:
-            sd.wait_stream(aux)
-        eps = snn.sparse_grad_in(self.W_out, self.alpha_out, T, B, ro_csr, ro_eps, csrs[L - 1], share_cu=True,
+                ev = torch.cuda.Event()
+                ev.record(aux)
+                wss.insert(0, ws)
+                laid.insert(0, ev)
+        eps = snn.sparse_grad_in(self.W_out, self.alpha_out, T, B, ro_csr, ro_eps, csrs[L - 1], share_cu=not big,
                                  stream=main)
         dWs: List[Optional[torch.Tensor]] = [None] * L
         epss: List[Optional[torch.Tensor]] = [None] * L
@@ -180,15 +183,17 @@ class Network:
             epss[l] = eps
             sd = streams[(L - 1 - l) % len(streams)]
             sd.wait_stream(main)  # eps of layer l is ready
+            sd.wait_event(laid[l])  # and its layout
             with torch.cuda.stream(sd):
                 dWs[l] = snn.sparse_dw_prepared(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], wss[l], stream=sd)
             if l > 0:
-                eps = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=True,
+                eps = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=not big,
                                          stream=main)
         with torch.cuda.stream(aux):  # the readout's dW last: nothing below waits for it
             dW_out = snn.sparse_dw(self.trace_out, ro_csr, ro_eps, self.W_out.shape[1], stream=aux)
-        for sd in streams:
-            main.wait_stream(sd)
+        for sd in [aux] + streams:
+            if sd is not main:
+                main.wait_stream(sd)
         for t in dWs + [dW_out] + wss:
             t.record_stream(main)
         return dWs, dW_out, epss
