@@ -49,7 +49,7 @@ int cu_count();
 // is set once per device, kernel and size and remembered (thread-safe); later calls only look up.
 void ensure_dynamic_lds(const void* kernel, int bytes);
 
-// Sparse dW on the matrix cores (dw_mfma.hip), for 32 < N_out <= 1024 and N_in % 4 == 0.
+// Sparse dW on the matrix cores (dw_mfma.hip), for 512 <= N_out <= 1024 and N_in % 4 == 0.
 struct MdwPlan {
   int n_win, n_itiles, n_chunks, wpc;  // windows of rows, input tiles, chunks of windows, windows per chunk
 };

@@ -459,6 +459,16 @@ def test_parity_wide_layers(hidden, n_in, n_ro):
     check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
 
 
+@pytest.mark.parametrize("hidden,n_in,n_ro,T,B", [((600, 1000), 52, 520, 37, 3), ((1000,), 1024, 512, 300, 4)])
+def test_parity_matrix_core_widths(hidden, n_in, n_ro, T, B):
+    """Layers of 512..1024 outputs take the matrix-core dW: widths that leave wavefronts and lane
+    groups without columns (520, 600, 1000), a partial 64-input tile (52 inputs), a partial window
+    of rows (111 rows) and several windows and chunks (1200 rows)."""
+    inp = _wide(hidden, n_in, n_ro, T=T, B=B)
+    print(f"\n[case] matrix-core widths {n_in}->{hidden}->{n_ro} T={T} B={B}", flush=True)
+    check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
+
+
 @pytest.mark.parametrize("hidden,n_ro", [((24, 31), 3), ((31,), 8), ((24,), 9), ((40, 17), 16), ((32,), 32),
                                           ((29,), 33)])
 def test_parity_narrow_outputs(hidden, n_ro):
