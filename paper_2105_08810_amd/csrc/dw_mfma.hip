@@ -429,18 +429,19 @@ __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict_
 }
 
 // dW = sum of the chunk partials in chunk order, float64 (deterministic); 256 outputs per block.
-// Partials are rows of S column slots; output column c reads slot perm[c].
+// Partials are rows of S column slots, read in slot order (coalesced); slot v goes to column
+// inv[v] of dW (slots without a column hold -1 and are skipped).
 __global__ __launch_bounds__(256) void mdw_reduce(const float* __restrict__ part, int n_chunks, int N_in, int N_out,
-                                                  int S, const int32_t* __restrict__ perm, float* __restrict__ out) {
+                                                  int S, const int32_t* __restrict__ inv, float* __restrict__ out) {
   const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (k >= (int64_t)N_in * N_out) return;
-  const int64_t i = k / N_out;
-  const int c = (int)(k - i * N_out);
-  const int slot = min(max(perm[c], 0), S - 1);
   const int64_t n = (int64_t)N_in * S;
+  if (k >= n) return;
+  const int64_t i = k / S;
+  const int col = inv[k - i * S];
+  if (col < 0 || col >= N_out) return;
   double s = 0.0;
-  for (int ch = 0; ch < n_chunks; ++ch) s += (double)part[ch * n + i * S + slot];
-  out[k] = (float)s;
+  for (int ch = 0; ch < n_chunks; ++ch) s += (double)part[ch * n + k];
+  out[i * N_out + col] = (float)s;
 }
 
 }  // namespace
@@ -529,9 +530,10 @@ void mdw_enqueue_rest(const float* trace_in, int T, int B, int N_in, int N_out, 
                      T * B, N_in, N_out, b.qoff, b.rec, b.inv, out_cap, p.n_win, p.wpc, p.n_itiles, b.part,
                      p.n_chunks > 1);
   if (p.n_chunks > 1) {
-    const int64_t n = (int64_t)N_in * N_out;
+    const int S = 4 * ((N_out + 3) / 4);
+    const int64_t n = (int64_t)N_in * S;
     hipLaunchKernelGGL(mdw_reduce, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, b.part, p.n_chunks, N_in, N_out,
-                       4 * ((N_out + 3) / 4), b.perm, dW);
+                       S, b.inv, dW);
   }
 }
 
