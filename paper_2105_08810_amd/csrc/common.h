@@ -49,11 +49,12 @@ int cu_count();
 // is set once per device, kernel and size and remembered (thread-safe); later calls only look up.
 void ensure_dynamic_lds(const void* kernel, int bytes);
 
-// Sparse dW on the matrix cores (dw_mfma.hip), for 512 <= N_out <= 1024 and N_in % 4 == 0.
+// Sparse dW on the matrix cores (dw_mfma.hip), for 512 <= N_out <= 1024, N_in % 4 == 0 and at most
+// 10% of the entries active.
 struct MdwPlan {
   int n_win, n_itiles, n_chunks, wpc;  // windows of rows, input tiles, chunks of windows, windows per chunk
 };
-bool mdw_eligible(int T, int B, int N_in, int N_out);
+bool mdw_eligible(int T, int B, int N_in, int N_out, int64_t out_cap);
 MdwPlan plan_mdw(int T, int B, int N_in, int N_out);
 size_t mdw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap);
 // Structure-only part: sorts each window's entries by column quad into the workspace.

@@ -447,11 +447,13 @@ __global__ __launch_bounds__(256) void mdw_reduce(const float* __restrict__ part
 }  // namespace
 
 // A block's sixteen wavefronts own 64 columns each; below 512 columns more than half of them would
-// idle, and the slab kernels are as fast there (measured at 200, 300 and 400 columns).
-bool mdw_eligible(int T, int B, int N_in, int N_out) {
-  (void)T;
-  (void)B;
-  return N_out >= kMWaves * kWave / 2 && N_out <= kMWaves * kWave && N_in % 4 == 0;
+// idle, and the slab kernels are as fast there (measured at 200, 300 and 400 columns). Above ~10%
+// of the entries active (the capacity is the compaction's count) a window's entries need several
+// record rounds and the lockstep quads cost more than the slab kernel's atomics (stress at 27%
+// active: 67 against 45 ms); the dense chain is the faster one there anyway.
+bool mdw_eligible(int T, int B, int N_in, int N_out, int64_t out_cap) {
+  if (N_out < kMWaves * kWave / 2 || N_out > kMWaves * kWave || N_in % 4 != 0) return false;
+  return (double)out_cap <= 0.1 * (double)T * (double)B * (double)N_out;
 }
 
 MdwPlan plan_mdw(int T, int B, int N_in, int N_out) {

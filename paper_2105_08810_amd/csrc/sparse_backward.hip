@@ -967,7 +967,7 @@ size_t dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
     if (q.n_chunks > 1) c.take<float>((size_t)q.n_chunks * N_in * N_out);
     return c.off;
   }
-  if (mdw_eligible(T, B, N_in, N_out)) return mdw_workspace(T, B, N_in, N_out, out_cap);
+  if (mdw_eligible(T, B, N_in, N_out, out_cap)) return mdw_workspace(T, B, N_in, N_out, out_cap);
   const DwPlan p = plan_dw(T, B, N_in, N_out);
   const int nsp = p.n_slabs * T * B;
   Carve c(nullptr);
@@ -1053,7 +1053,7 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
     }
     return;
   }
-  if (mdw_eligible(T, B, N_in, N_out)) {  // matrix-core accumulation over windows sorted by column quad
+  if (mdw_eligible(T, B, N_in, N_out, out_cap)) {  // matrix-core accumulation over windows sorted by column quad
     if (layout) mdw_enqueue_layout(T, B, N_in, N_out, out_row_ptr, out_col_idx, out_cap, workspace, s);
     if (rest) mdw_enqueue_rest(trace_in, T, B, N_in, N_out, out_g, eps_out, out_cap, dW, workspace, s);
     return;
