@@ -108,7 +108,7 @@ snn_status snn_active_compact(const float* V, int T, int B, int N, float theta, 
  * Compaction from the bitset of snn_lif_forward_active: the same CSR as snn_active_compact with
  * the band used for the bitset (row_ptr, col_idx ascending, g_act = 1/(beta|V-theta|+1)^2 read
  * from V at the active entries only). V may be NULL when g_act is NULL. Capacity, nnz and
- * overflow behave as in snn_active_compact.
+ * overflow behave as in snn_active_compact. SNN_ERR_UNSUPPORTED when T*B > 8,388,608 rows.
  */
 size_t snn_active_compact_bits_workspace(int T, int B, int N);
 snn_status snn_active_compact_bits(const uint64_t* active_bits, const float* V, int T, int B, int N,

@@ -167,35 +167,74 @@ __device__ __forceinline__ uint64_t row_window(const uint64_t* __restrict__ bits
   return x;
 }
 
-// A wavefront takes RPW = 64 / nw rows when a row has nw <= 64 windows (lane l: row l / nw of
-// the wavefront's rows, window l % nw), else one row with the windows walked 64 at a time.
-// Positions inside a row come from a wavefront-wide inclusive scan minus its value just before
-// the row's first lane.
-__global__ __launch_bounds__(kThreads) void bits_count(const uint64_t* __restrict__ bits, int T, int B, int N,
-                                                       int rpw, int32_t* __restrict__ counts) {
+// Count and fill run over tiles of TR consecutive rows, one 1024-thread block per tile: the count
+// kernel writes every row's count and the tile's total; the fill kernel forms its tile's row
+// pointers itself (the totals of the tiles before it, at most kMaxTiles of them, plus a block
+// scan of its rows' counts), then places the entries. Two kernels instead of count, a
+// three-kernel scan and fill. A wavefront takes RPW = 64 / nw rows at a time when a row has
+// nw <= 64 windows (lane l: row l / nw of the group, window l % nw), else one row with the windows
+// walked 64 at a time; positions inside a row come from a wavefront-wide inclusive scan minus its
+// value just before the row's first lane.
+constexpr int kTileThreads = 1024;
+constexpr int kTileWaves = kTileThreads / kWave;
+constexpr int kMaxTiles = 4096;
+
+struct TilePlan {
+  int tr, n_tiles, rpw;
+};
+
+// Tiles of 64 rows (long rows, one per wavefront: 16), doubled until there are at most 1024
+// tiles (long rows: kMaxTiles). Measured: fewer, longer tiles cost more in the fill's V gathers
+// than the shorter sum over earlier tiles saves, except for long rows.
+TilePlan plan_tiles(int rows, int N) {
+  TilePlan p{};
+  const int nw = (N + kWave - 1) / kWave;
+  p.rpw = nw <= kWave ? kWave / nw : 1;
+  p.tr = p.rpw > 1 ? 64 : kTileWaves;
+  const int max_tiles = p.rpw > 1 ? 1024 : kMaxTiles;
+  while ((rows + p.tr - 1) / p.tr > max_tiles) p.tr *= 2;
+  p.n_tiles = (rows + p.tr - 1) / p.tr;
+  return p;
+}
+
+__global__ __launch_bounds__(kTileThreads) void bits_count(const uint64_t* __restrict__ bits, int T, int B, int N,
+                                                           int tr, int rpw, int32_t* __restrict__ counts,
+                                                           int32_t* __restrict__ tile_sum) {
+  __shared__ int wsum[kTileWaves];
   const int l = lane_id();
+  const int wv = threadIdx.x / kWave;
   const int rows = T * B;
   const int nw = (N + kWave - 1) / kWave;
   const size_t W64 = ((size_t)B * N + kWave - 1) / kWave;
-  const int r0 = (blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave)) * rpw;
-  if (r0 >= rows) return;
-  if (rpw > 1) {
-    const int k = l / nw, w = l - k * nw;
-    const int r = r0 + k;
-    const bool ok = k < rpw && r < rows;
-    const int c = ok ? __popcll(row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w)) : 0;
-    const int incl = wave_incl_scan(c);
-    const int first = k * nw;  // lane of the row's first window
-    const int before = __shfl(incl, max(first - 1, 0), kWave);  // every lane takes part in the exchange
-    if (ok && w == nw - 1) counts[r] = incl - (first > 0 ? before : 0);
-    return;
+  const int t0 = blockIdx.x * tr, t1 = min(rows, t0 + tr);
+  int total = 0;
+  for (int r0 = t0 + wv * rpw; r0 < t1; r0 += kTileWaves * rpw) {
+    if (rpw > 1) {
+      const int k = l / nw, w = l - k * nw;
+      const int r = r0 + k;
+      const bool ok = k < rpw && r < t1;
+      const int c = ok ? __popcll(row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w)) : 0;
+      const int incl = wave_incl_scan(c);
+      const int first = k * nw;  // lane of the row's first window
+      const int before = __shfl(incl, max(first - 1, 0), kWave);  // every lane takes part in the exchange
+      if (ok && w == nw - 1) counts[r] = incl - (first > 0 ? before : 0);
+      total += __shfl(incl, kWave - 1, kWave);
+    } else {
+      int c = 0;
+      for (int w0 = 0; w0 < nw; w0 += kWave)
+        if (w0 + l < nw) c += __popcll(row_window(bits, W64, r0 / B, (size_t)(r0 % B) * N, N, w0 + l));
+      c = wave_sum_int(c);
+      if (l == 0) counts[r0] = c;
+      total += c;
+    }
   }
-  const int r = r0;
-  int c = 0;
-  for (int w0 = 0; w0 < nw; w0 += kWave)
-    if (w0 + l < nw) c += __popcll(row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w0 + l));
-  c = wave_sum_int(c);
-  if (l == 0) counts[r] = c;
+  if (l == 0) wsum[wv] = total;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int k = 0; k < kTileWaves; ++k) s += wsum[k];
+    tile_sum[blockIdx.x] = s;
+  }
 }
 
 // Places a lane's set bits of one window at pos, pos + 1, ... (up to four V loads in flight).
@@ -225,42 +264,105 @@ __device__ __forceinline__ void place_window(uint64_t x, int jbase, int64_t pos,
   }
 }
 
-__global__ __launch_bounds__(kThreads) void bits_fill(const uint64_t* __restrict__ bits, const float* __restrict__ V,
-                                                      int T, int B, int N, int rpw, float theta, float beta,
-                                                      const int32_t* __restrict__ row_ptr,
-                                                      int32_t* __restrict__ col_idx, float* __restrict__ g_act,
-                                                      int64_t cap) {
+// tr <= kTileThreads * kMaxPerThread rows per tile.
+constexpr int kMaxPerThread = 8;
+
+__global__ __launch_bounds__(kTileThreads) void bits_fill(const uint64_t* __restrict__ bits, const float* __restrict__ V,
+                                                          int T, int B, int N, int tr, int rpw, float theta, float beta,
+                                                          const int32_t* __restrict__ counts,
+                                                          const int32_t* __restrict__ tile_sum,
+                                                          int32_t* __restrict__ row_ptr, int64_t* __restrict__ nnz,
+                                                          int32_t* __restrict__ col_idx, float* __restrict__ g_act,
+                                                          int64_t cap) {
+  extern __shared__ int rp_tile[];  // [tr + 1]: the tile's row pointers
+  __shared__ int red[kTileWaves];
+  __shared__ int base_s;
   const int l = lane_id();
+  const int wv = threadIdx.x / kWave;
   const int rows = T * B;
+  const int t0 = blockIdx.x * tr, t1 = min(rows, t0 + tr);
+  // the totals of the tiles before this one (fixed order: per thread, then the wavefronts in order)
+  int p = 0;
+  for (int k = threadIdx.x; k < (int)blockIdx.x; k += kTileThreads) p += tile_sum[k];
+  p = wave_sum_int(p);
+  if (l == 0) red[wv] = p;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int k = 0; k < kTileWaves; ++k) s += red[k];
+    base_s = s;
+  }
+  __syncthreads();
+  const int base = base_s;
+  // exclusive scan of the tile's row counts; thread x owns rows t0 + x * per .. + per - 1
+  const int per = (tr + kTileThreads - 1) / kTileThreads;
+  int c[kMaxPerThread];
+  int mine = 0;
+#pragma unroll
+  for (int u = 0; u < kMaxPerThread; ++u) {
+    const int r = t0 + threadIdx.x * per + u;
+    c[u] = (u < per && r < t1) ? counts[r] : 0;
+    mine += c[u];
+  }
+  const int incl = wave_incl_scan(mine);
+  __syncthreads();  // red is reused
+  if (l == kWave - 1) red[wv] = incl;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int k = 0; k < kTileWaves; ++k) {
+    const int v = red[k];
+    before += k < wv ? v : 0;
+    all += v;
+  }
+  int run = before + incl - mine;
+#pragma unroll
+  for (int u = 0; u < kMaxPerThread; ++u) {
+    const int rl = threadIdx.x * per + u;
+    if (u < per && t0 + rl < t1) {
+      rp_tile[rl] = base + run;
+      row_ptr[t0 + rl] = base + run;
+    }
+    run += c[u];
+  }
+  if (threadIdx.x == 0) {
+    rp_tile[t1 - t0] = base + all;
+    if (t1 == rows) {  // the last tile closes the row pointers and reports the true count
+      row_ptr[rows] = base + all;
+      *nnz = (int64_t)base + all;
+    }
+  }
+  __syncthreads();
+  if (cap <= 0) return;
   const int nw = (N + kWave - 1) / kWave;
   const size_t W64 = ((size_t)B * N + kWave - 1) / kWave;
-  const int r0 = (blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave)) * rpw;
-  if (r0 >= rows) return;
-  if (rpw > 1) {
-    const int k = l / nw, w = l - k * nw;
-    const int r = r0 + k;
-    const bool ok = k < rpw && r < rows;
-    const uint64_t x = ok ? row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w) : 0ull;
-    const int64_t dst = ok ? row_ptr[r] : 0;
-    const int c = __popcll(x);
-    const int incl = wave_incl_scan(c);
-    const int first = k * nw;
-    const int prev = __shfl(incl, max(first - 1, 0), kWave);  // every lane takes part in the exchange
-    const int before = first > 0 ? prev : 0;
-    place_window(x, kWave * w, dst + (incl - c - before), V + (size_t)(ok ? r : 0) * N, theta, beta, col_idx, g_act,
-                 cap);
-    return;
-  }
-  const int r = r0;
-  const float* vrow = V + (size_t)r * N;
-  int64_t base = row_ptr[r];
-  for (int w0 = 0; w0 < nw; w0 += kWave) {
-    const int w = w0 + l;
-    const uint64_t x = w < nw ? row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w) : 0ull;
-    const int c = __popcll(x);
-    const int incl = wave_incl_scan(c);
-    place_window(x, kWave * w, base + incl - c, vrow, theta, beta, col_idx, g_act, cap);
-    base += __shfl(incl, kWave - 1, kWave);
+  for (int r0 = t0 + wv * rpw; r0 < t1; r0 += kTileWaves * rpw) {
+    if (rpw > 1) {
+      const int k = l / nw, w = l - k * nw;
+      const int r = r0 + k;
+      const bool ok = k < rpw && r < t1;
+      const uint64_t x = ok ? row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w) : 0ull;
+      const int64_t dst = ok ? rp_tile[r - t0] : 0;
+      const int cw = __popcll(x);
+      const int in = wave_incl_scan(cw);
+      const int first = k * nw;
+      const int prev = __shfl(in, max(first - 1, 0), kWave);  // every lane takes part in the exchange
+      const int bef = first > 0 ? prev : 0;
+      place_window(x, kWave * w, dst + (in - cw - bef), V + (size_t)(ok ? r : 0) * N, theta, beta, col_idx, g_act,
+                   cap);
+    } else {
+      const int r = r0;
+      const float* vrow = V + (size_t)r * N;
+      int64_t b0 = rp_tile[r - t0];
+      for (int w0 = 0; w0 < nw; w0 += kWave) {
+        const int w = w0 + l;
+        const uint64_t x = w < nw ? row_window(bits, W64, r / B, (size_t)(r % B) * N, N, w) : 0ull;
+        const int cw = __popcll(x);
+        const int in = wave_incl_scan(cw);
+        place_window(x, kWave * w, b0 + in - cw, vrow, theta, beta, col_idx, g_act, cap);
+        b0 += __shfl(in, kWave - 1, kWave);
+      }
+    }
   }
 }
 
@@ -318,9 +420,10 @@ extern "C" snn_status snn_active_compact(const float* V, int T, int B, int N, fl
 extern "C" size_t snn_active_compact_bits_workspace(int T, int B, int N) {
   if (bad_dim(T) || bad_dim(B) || bad_dim(N) || too_big(T, B, N)) return 0;
   const int rows = T * B;
+  const TilePlan p = plan_tiles(rows, N);
   Carve c(nullptr);
   c.take<int32_t>(rows);
-  c.take<int32_t>(scan_temp_elems(rows));
+  c.take<int32_t>(p.n_tiles);
   return c.off;
 }
 
@@ -345,18 +448,16 @@ snn_status enqueue_compact_bits(const uint64_t* active_bits, const float* V, int
                                 float beta, int32_t* row_ptr, int32_t* col_idx, float* g_act, int64_t capacity,
                                 int64_t* nnz_dev, void* workspace, hipStream_t s) {
   const int rows = T * B;
+  const TilePlan p = plan_tiles(rows, N);
+  if (p.tr > kTileThreads * kMaxPerThread) return SNN_ERR_UNSUPPORTED;  // more than 8 M rows
   Carve ws(workspace);
   int32_t* counts = ws.take<int32_t>(rows);
-  int32_t* temp = ws.take<int32_t>(scan_temp_elems(rows));
-  const int nw = (N + kWave - 1) / kWave;
-  const int rpw = nw <= kWave ? kWave / nw : 1;  // rows per wavefront
-  const int waves = (rows + rpw - 1) / rpw;
-  const dim3 grid((waves + kRowsPerBlock - 1) / kRowsPerBlock);
-  hipLaunchKernelGGL(bits_count, grid, dim3(kThreads), 0, s, active_bits, T, B, N, rpw, counts);
-  launch_exclusive_scan(counts, rows, row_ptr, nnz_dev, temp, s);
-  if (capacity > 0)
-    hipLaunchKernelGGL(bits_fill, grid, dim3(kThreads), 0, s, active_bits, V, T, B, N, rpw, theta, beta, row_ptr,
-                       col_idx, g_act, capacity);
+  int32_t* tsum = ws.take<int32_t>(p.n_tiles);
+  hipLaunchKernelGGL(bits_count, dim3((unsigned)p.n_tiles), dim3(kTileThreads), 0, s, active_bits, T, B, N, p.tr, p.rpw,
+                     counts, tsum);
+  hipLaunchKernelGGL(bits_fill, dim3((unsigned)p.n_tiles), dim3(kTileThreads), (size_t)(p.tr + 1) * sizeof(int), s,
+                     active_bits, V, T, B, N, p.tr, p.rpw, theta, beta, counts, tsum, row_ptr, nnz_dev, col_idx, g_act,
+                     capacity);
   return launch_status();
 }
 
