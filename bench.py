@@ -601,6 +601,32 @@ class Runner:
                                                                    self.ws_dw[l]))
                 laid[l] = self.torch.cuda.Event()
                 laid[l].record(side)
+        if inline:
+            # One stream: each layer's spike gradient first (it needs no layout, so the chain starts
+            # while the layouts run on the side stream), then its dW. One event per boundary: a timing
+            # event is a barrier packet that costs the stream several microseconds.
+            mark = ev["ro1"]  # recorded at the current boundary of main
+            for l in range(L - 1, -1, -1):
+                i = L - 1 - l
+                ev["lay0"][i] = mark
+                if l > 0:
+                    ev["gi0"][i] = mark
+                    R(f"gi{l}", main, self._gi_call(l, eps, False))
+                    ev["gi1"][i].record(main)
+                    mark = ev["gi1"][i]
+                ev["dw0"][i] = mark
+                if laid[l] is not None:
+                    main.wait_event(laid[l])
+                R(f"dw{l}", main, self._dw_call(l, eps, K, prepared=not K))
+                ev["dw1"][i].record(main)
+                mark = ev["lay1"][i] = ev["dw1"][i]
+                if l > 0:
+                    eps = self.eps[l - 1]
+            main.wait_stream(side)
+            ev["bw1"].record(main)
+            R("ro_dw", main, lambda: snn.sparse_dw(net.trace_out, r[0], r[1], net.W_out.shape[1], ws=self.ws_ro,
+                                                  dW=self.dW_out))
+            return
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
             sd = dw_streams[i % len(dw_streams)]

@@ -950,6 +950,158 @@ void launch_walk(dim3 grid, size_t lds, hipStream_t s, const float* W, int T, in
                      og, oeps, ocap, irp, ici, icap, D, eps_in);
 }
 
+// The walk for layers whose outputs are a multiple of 4 (and more than 256): lane l holds
+// delta at j = 4 l + 256 m + u (u < 4), so a W row arrives in 16-byte loads, NJ / 4 per lane.
+// G[t] goes into delta through a per-wavefront LDS row: the step's output entries are stored
+// at their columns (one lane each, no two alike inside a row), every lane then takes its
+// columns with 16-byte reads (delta <- alpha delta + G) and the entries' columns are cleared
+// again. This replaces a register-indexed add per output entry.
+template <int NJ>
+__global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk_x4(
+    const float* __restrict__ W, int T, int B, int N_in, int N_out, float alpha, int P, int C,
+    const int32_t* __restrict__ orp, const int32_t* __restrict__ oci, const float* __restrict__ og,
+    const float* __restrict__ oeps, int64_t ocap, const int32_t* __restrict__ irp,
+    const int32_t* __restrict__ ici, int64_t icap, const float* __restrict__ D, float* __restrict__ eps_in) {
+  static_assert(NJ % 4 == 0, "whole 16-byte columns per lane");
+  constexpr int NQ = NJ / 4;
+  extern __shared__ float4 gq_all[];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  float4* gq = gq_all + (size_t)w * NQ * kWave;  // the wavefront's G row: column j at float j
+  float* gcol = reinterpret_cast<float*>(gq);
+#pragma unroll
+  for (int m = 0; m < NQ; ++m) gq[l + kWave * m] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int q = blockIdx.x * kWalkWaves + w; q < C * B; q += gridDim.x * kWalkWaves) {
+    const int c = q / B;
+    const int b = q - c * B;
+    float d[NJ];
+#pragma unroll
+    for (int m = 0; m < NQ; ++m) {
+      const int j = 4 * l + 4 * kWave * m;
+      const float4 v = j < N_out ? *reinterpret_cast<const float4*>(D + (size_t)q * N_out + j)
+                                 : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      d[4 * m + 0] = v.x;
+      d[4 * m + 1] = v.y;
+      d[4 * m + 2] = v.z;
+      d[4 * m + 3] = v.w;
+    }
+    const int t_lo = c * P;
+    const int t_hi = min(T, t_lo + P);
+    int ia = 0, ib = 0, oa = 0, ob = 0;
+    if (l < t_hi - t_lo) {
+      const int r = (t_lo + l) * B + b;
+      ia = clamp_entry(irp[r], icap);
+      ib = clamp_entry(irp[r + 1], icap);
+      oa = clamp_entry(orp[r], ocap);
+      ob = clamp_entry(orp[r + 1], ocap);
+    }
+    // entry l of step k's rows (clamped into the row; only lanes below the row length are used)
+    auto in_idx = [&](int k) {
+      const int a = rdlane(ia, k), z = rdlane(ib, k);
+      return z > a ? ici[min(a + l, z - 1)] : -1;
+    };
+    auto out_col = [&](int k) {
+      const int a = rdlane(oa, k), z = rdlane(ob, k);
+      return z > a ? oci[min(a + l, z - 1)] : -1;
+    };
+    auto out_g = [&](int k) {
+      const int a = rdlane(oa, k), z = rdlane(ob, k);
+      const int e = min(a + l, max(z - 1, 0));
+      return z > a ? oeps[e] * (og ? og[e] : 1.0f) : 0.0f;
+    };
+    int k = t_hi - 1 - t_lo;
+    int vi = in_idx(k), vj = out_col(k);
+    float vg = out_g(k);
+    for (; k >= 0; --k) {
+      const int kn = max(k - 1, 0);
+      const int vi_n = in_idx(kn), vj_n = out_col(kn);
+      const float vg_n = out_g(kn);
+      // eps_in at the input-active entries of row (t, b), with delta[t] = d
+      const int i0 = rdlane(ia, k);
+      const int i1 = rdlane(ib, k);
+      for (int e0 = i0; e0 < i1; e0 += kWave) {
+        const int vc = e0 == i0 ? vi : ici[min(e0 + l, i1 - 1)];  // entry e0 + l
+        const int ne = min(kWave, i1 - e0);
+        for (int x = 0; x < ne; x += kGinBatch) {
+          int iv[kGinBatch];
+#pragma unroll
+          for (int u = 0; u < kGinBatch; ++u) {
+            const int xi = rdlane(vc, min(x + u, kWave - 1));
+            iv[u] = (x + u < ne && (unsigned)xi < (unsigned)N_in) ? xi : -1;
+          }
+          float wv[kGinBatch][NJ];
+#pragma unroll
+          for (int u = 0; u < kGinBatch; ++u) {
+            const __amdgpu_buffer_rsrc_t rs = row_rsrc(W + (size_t)(iv[u] >= 0 ? iv[u] : 0) * N_out, N_out);
+#pragma unroll
+            for (int m = 0; m < NQ; ++m) {
+              const auto v4 = __builtin_amdgcn_raw_buffer_load_b128(rs, (4 * l + 4 * kWave * m) * 4, 0, 0);
+              wv[u][4 * m + 0] = __uint_as_float(v4[0]);
+              wv[u][4 * m + 1] = __uint_as_float(v4[1]);
+              wv[u][4 * m + 2] = __uint_as_float(v4[2]);
+              wv[u][4 * m + 3] = __uint_as_float(v4[3]);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          float acc[kGinBatch];
+#pragma unroll
+          for (int u = 0; u < kGinBatch; ++u) {
+            acc[u] = 0.0f;
+#pragma unroll
+            for (int m = 0; m < NJ; ++m) acc[u] += wv[u][m] * d[m];  // d = 0 past N_out
+            acc[u] = iv[u] >= 0 ? acc[u] : 0.0f;
+          }
+          const float tot = wave_sum4(acc[0], acc[1], acc[2], acc[3]);
+          const int u = l >> 4;
+          if ((l & 15) == 0 && x + u < ne) eps_in[e0 + x + u] = tot;
+        }
+      }
+      // delta[t-1] = alpha delta[t] + G[t], G through the LDS row
+      const int o0 = rdlane(oa, k);
+      const int o1 = rdlane(ob, k);
+      for (int e0 = o0; e0 < o1; e0 += kWave) {
+        int jv = vj;
+        float gv = vg;
+        if (e0 > o0) {  // rows with more than 64 active outputs: the rest is read here
+          const int ec = min(e0 + l, o1 - 1);
+          jv = oci[ec];
+          gv = oeps[ec] * (og ? og[ec] : 1.0f);
+        }
+        if (e0 + l < o1 && (unsigned)jv < (unsigned)N_out) gcol[jv] = gv;
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int m = 0; m < NQ; ++m) {
+        const float4 g4 = gq[l + kWave * m];
+        d[4 * m + 0] = alpha * d[4 * m + 0] + g4.x;
+        d[4 * m + 1] = alpha * d[4 * m + 1] + g4.y;
+        d[4 * m + 2] = alpha * d[4 * m + 2] + g4.z;
+        d[4 * m + 3] = alpha * d[4 * m + 3] + g4.w;
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (o1 - o0 <= kWave) {
+        if (o0 + l < o1 && (unsigned)vj < (unsigned)N_out) gcol[vj] = 0.0f;
+      } else {
+#pragma unroll
+        for (int m = 0; m < NQ; ++m) gq[l + kWave * m] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      }
+      __builtin_amdgcn_wave_barrier();
+      vi = vi_n;
+      vj = vj_n;
+      vg = vg_n;
+    }
+  }
+}
+
+template <int NJ>
+void launch_walk_x4(dim3 grid, hipStream_t s, const float* W, int T, int B, int N_in, int N_out, float alpha, int P,
+                    int C, const int32_t* orp, const int32_t* oci, const float* og, const float* oeps, int64_t ocap,
+                    const int32_t* irp, const int32_t* ici, int64_t icap, const float* D, float* eps_in) {
+  const size_t lds = (size_t)kWalkWaves * NJ * kWave * sizeof(float);
+  hipLaunchKernelGGL(gin_walk_x4<NJ>, grid, dim3(kWalkThreads), lds, s, W, T, B, N_in, N_out, alpha, P, C, orp, oci,
+                     og, oeps, ocap, irp, ici, icap, D, eps_in);
+}
+
 }  // namespace
 }  // namespace snn
 
@@ -1217,6 +1369,17 @@ void enqueue_grad_in(const float* W, int T, int B, int N_in, int N_out, float al
                      Lbuf);
   const int nj = (N_out + kWave - 1) / kWave;
   const dim3 walk_grid(share_cu ? std::min<unsigned>(wgrid.x, 2u * (unsigned)cu_count()) : wgrid.x);
+  if (nj > 4 && N_out % 4 == 0) {
+#define SNN_WALK4(NJ_)                                                                                        \
+  launch_walk_x4<NJ_>(walk_grid, s, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, \
+                      eps_out, out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)
+    if (nj <= 8) SNN_WALK4(8);
+    else if (nj <= 16) SNN_WALK4(16);
+    else if (nj <= 32) SNN_WALK4(32);
+    else SNN_WALK4(64);
+#undef SNN_WALK4
+    return;
+  }
 #define SNN_WALK(NJ_)                                                                                             \
   launch_walk<NJ_>(walk_grid, 0, s, W, T, B, N_in, N_out, alpha, wp.P, wp.C, out_row_ptr, out_col_idx, out_g, eps_out, \
                    out_cap, in_row_ptr, in_col_idx, in_cap, Lbuf, eps_in)

@@ -153,8 +153,8 @@ class Network:
         layer's dW needs only its own eps, and the structure-only part of every dW call needs only
         the active sets. The layouts run on aux from the start, beside the readout's backward.
         When a dW call fills the GPU by itself (big layers), the dW calls then run on the current
-        stream between the spike gradients (a dW beside a spike gradient would only take CUs
-        from it); for small layers every dW runs on a dW stream as soon as its eps is there, beside
+        stream, each after its layer's spike gradient (a dW beside a spike gradient would only take
+        CUs from it, and the chain then starts without waiting for a layout); for small layers every dW runs on a dW stream as soon as its eps is there, beside
         the chain."""
         main = torch.cuda.current_stream()
         T, B, L = self.T, self.B, self.L
@@ -181,14 +181,18 @@ class Network:
             if reg_coefs is not None:
                 snn.activity_reg_grad(reg_coefs[l], T, eps, csrs[l])
             epss[l] = eps
+            eps_below = None
+            if big and l > 0:  # one stream: the spike gradient first, it needs no layout
+                eps_below = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1],
+                                               share_cu=False, stream=main)
             sd = streams[(L - 1 - l) % len(streams)]
             sd.wait_stream(main)  # eps of layer l is ready
             sd.wait_event(laid[l])  # and its layout
             with torch.cuda.stream(sd):
                 dWs[l] = snn.sparse_dw_prepared(self.trace[l], csrs[l], eps, self.Ws[l].shape[1], wss[l], stream=sd)
             if l > 0:
-                eps = snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps, csrs[l - 1], share_cu=not big,
-                                         stream=main)
+                eps = eps_below if big else snn.sparse_grad_in(self.Ws[l], self.alphas[l], T, B, csrs[l], eps,
+                                                               csrs[l - 1], share_cu=True, stream=main)
         with torch.cuda.stream(aux):  # the readout's dW last: nothing below waits for it
             dW_out = snn.sparse_dw(self.trace_out, ro_csr, ro_eps, self.W_out.shape[1], stream=aux)
         for sd in [aux] + streams:
