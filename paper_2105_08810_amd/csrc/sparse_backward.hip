@@ -1004,30 +1004,54 @@ __global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk_x4(
       const int a = rdlane(oa, k), z = rdlane(ob, k);
       return z > a ? oci[min(a + l, z - 1)] : -1;
     };
-    auto out_g = [&](int k) {
+    // eps and g of entry l of step k's output row, multiplied where they are used (a product here
+    // would wait for the loads at once)
+    auto out_e = [&](int k) {
       const int a = rdlane(oa, k), z = rdlane(ob, k);
-      const int e = min(a + l, max(z - 1, 0));
-      return z > a ? oeps[e] * (og ? og[e] : 1.0f) : 0.0f;
+      return z > a ? oeps[min(a + l, z - 1)] : 0.0f;
+    };
+    auto out_gg = [&](int k) {
+      const int a = rdlane(oa, k), z = rdlane(ob, k);
+      return (z > a && og) ? og[min(a + l, z - 1)] : 1.0f;
     };
     int k = t_hi - 1 - t_lo;
     int vi = in_idx(k), vj = out_col(k);
-    float vg = out_g(k);
+    float ve = out_e(k), vgg = out_gg(k);
     for (; k >= 0; --k) {
-      const int kn = max(k - 1, 0);
-      const int vi_n = in_idx(kn), vj_n = out_col(kn);
-      const float vg_n = out_g(kn);
       // eps_in at the input-active entries of row (t, b), with delta[t] = d
       const int i0 = rdlane(ia, k);
       const int i1 = rdlane(ib, k);
+      // This step's entries are copied out of the registers the next step's requests go to, and
+      // the first batch's inputs read, before those requests: vector memory counts retire in order,
+      // so a later read of these registers would wait for the new requests too.
+      int iv0[kGinBatch];
+#pragma unroll
+      for (int u = 0; u < kGinBatch; ++u) {
+        const int xi = rdlane(vi, u);
+        iv0[u] = (u < i1 - i0 && (unsigned)xi < (unsigned)N_in) ? xi : -1;
+      }
+      int vc = vi;  // entry i0 + l
+      const int vj_k = vj;
+      const float vg_k = ve * vgg;
+      const int kn = max(k - 1, 0);
+      vi = in_idx(kn);
+      vj = out_col(kn);
+      ve = out_e(kn);
+      vgg = out_gg(kn);
       for (int e0 = i0; e0 < i1; e0 += kWave) {
-        const int vc = e0 == i0 ? vi : ici[min(e0 + l, i1 - 1)];  // entry e0 + l
+        if (e0 > i0) vc = ici[min(e0 + l, i1 - 1)];  // entry e0 + l
         const int ne = min(kWave, i1 - e0);
         for (int x = 0; x < ne; x += kGinBatch) {
           int iv[kGinBatch];
+          if (e0 == i0 && x == 0) {
 #pragma unroll
-          for (int u = 0; u < kGinBatch; ++u) {
-            const int xi = rdlane(vc, min(x + u, kWave - 1));
-            iv[u] = (x + u < ne && (unsigned)xi < (unsigned)N_in) ? xi : -1;
+            for (int u = 0; u < kGinBatch; ++u) iv[u] = iv0[u];
+          } else {
+#pragma unroll
+            for (int u = 0; u < kGinBatch; ++u) {
+              const int xi = rdlane(vc, min(x + u, kWave - 1));
+              iv[u] = (x + u < ne && (unsigned)xi < (unsigned)N_in) ? xi : -1;
+            }
           }
           float wv[kGinBatch][NJ];
 #pragma unroll
@@ -1060,8 +1084,8 @@ __global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk_x4(
       const int o0 = rdlane(oa, k);
       const int o1 = rdlane(ob, k);
       for (int e0 = o0; e0 < o1; e0 += kWave) {
-        int jv = vj;
-        float gv = vg;
+        int jv = vj_k;
+        float gv = vg_k;
         if (e0 > o0) {  // rows with more than 64 active outputs: the rest is read here
           const int ec = min(e0 + l, o1 - 1);
           jv = oci[ec];
@@ -1080,15 +1104,12 @@ __global__ __launch_bounds__(kWalkThreads, NJ <= 16 ? 4 : 1) void gin_walk_x4(
       }
       __builtin_amdgcn_wave_barrier();
       if (o1 - o0 <= kWave) {
-        if (o0 + l < o1 && (unsigned)vj < (unsigned)N_out) gcol[vj] = 0.0f;
+        if (o0 + l < o1 && (unsigned)vj_k < (unsigned)N_out) gcol[vj_k] = 0.0f;
       } else {
 #pragma unroll
         for (int m = 0; m < NQ; ++m) gq[l + kWave * m] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       }
       __builtin_amdgcn_wave_barrier();
-      vi = vi_n;
-      vj = vj_n;
-      vg = vg_n;
     }
   }
 }
