@@ -96,12 +96,15 @@ __global__ __launch_bounds__(256) void mdw_colcount(int TB, int N_out, const int
 
 // Column c's rank (descending count, ties by index) gives its slot v in the quad layout (snake
 // dealing over nq = ceil(N_out / 4) quads): perm[c] = v, inv[v] = c, and inv[v] = -1 for the slots
-// of ranks N_out .. 4 nq - 1 (no column). Each block ranks 64 columns; its 16 wavefronts split the
-// comparisons and add their partial ranks in LDS.
-__global__ __launch_bounds__(kMQ * 4) void mdw_perm(int N_out, const int32_t* __restrict__ cnt,
-                                                    int32_t* __restrict__ perm, int32_t* __restrict__ inv) {
+// of ranks N_out .. 4 nq - 1 (no column). Each block ranks 64 columns; its four wavefronts split
+// the comparisons and add their partial ranks in LDS. (Small blocks: this runs on a side stream
+// beside other kernels and must find room on a busy compute unit.)
+constexpr int kPermWaves = 4;
+constexpr int kPermCmp = kMQ * 4 / kPermWaves;  // comparisons per wavefront
+__global__ __launch_bounds__(kPermWaves * kWave) void mdw_perm(int N_out, const int32_t* __restrict__ cnt,
+                                                               int32_t* __restrict__ perm, int32_t* __restrict__ inv) {
   __shared__ __attribute__((aligned(16))) int cs[kMQ * 4];
-  __shared__ int part[16][kWave];
+  __shared__ int part[kPermWaves][kWave];
   const int t = threadIdx.x;
   const int nq = (N_out + 3) / 4;
   for (int k = t; k < kMQ * 4; k += blockDim.x) cs[k] = k < N_out ? cnt[k] : INT_MIN;
@@ -110,9 +113,9 @@ __global__ __launch_bounds__(kMQ * 4) void mdw_perm(int N_out, const int32_t* __
   const int c = blockIdx.x * kWave + l;
   const int mine = c < N_out ? cs[c] : 0;
   int rank = 0;
-  const int k0 = w * kWave;  // this wavefront's 64 comparisons (entries past N_out hold INT_MIN)
+  const int k0 = w * kPermCmp;  // this wavefront's comparisons (entries past N_out hold INT_MIN)
 #pragma unroll 4
-  for (int k = k0; k < k0 + kWave; k += 4) {
+  for (int k = k0; k < k0 + kPermCmp; k += 4) {
     const int4 o = *reinterpret_cast<const int4*>(cs + k);
     rank += (o.x > mine) || (o.x == mine && k < c);
     rank += (o.y > mine) || (o.y == mine && k + 1 < c);
@@ -128,12 +131,12 @@ __global__ __launch_bounds__(kMQ * 4) void mdw_perm(int N_out, const int32_t* __
   if (w == 0 && c < N_out) {
     int r = 0;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) r += part[k][l];
+    for (int k = 0; k < kPermWaves; ++k) r += part[k][l];
     const int v = slot_of(r);
     perm[c] = v;
     inv[v] = c;
   }
-  if (blockIdx.x == 0 && t >= N_out && t < 4 * nq) inv[slot_of(t)] = -1;
+  if (blockIdx.x == 0 && N_out + t < 4 * nq) inv[slot_of(N_out + t)] = -1;  // at most three
 }
 
 // Layout: one block per window. The window's entries (its CSR range) are split into four contiguous
@@ -516,7 +519,7 @@ void mdw_enqueue_layout(int T, int B, int N_in, int N_out, const int32_t* out_ro
   const int cblocks = std::max(1, std::min(cu_count(), (int)((out_cap + 4095) / 4096)));
   hipLaunchKernelGGL(mdw_colcount, dim3((unsigned)cblocks), dim3(256), 0, s, T * B, N_out, out_row_ptr, out_col_idx,
                      out_cap, b.cnt);
-  hipLaunchKernelGGL(mdw_perm, dim3((unsigned)((N_out + kWave - 1) / kWave)), dim3(kMQ * 4), 0, s, N_out, b.cnt,
+  hipLaunchKernelGGL(mdw_perm, dim3((unsigned)((N_out + kWave - 1) / kWave)), dim3(kPermWaves * kWave), 0, s, N_out, b.cnt,
                      b.perm, b.inv);
   hipLaunchKernelGGL(mdw_layout, dim3((unsigned)p.n_win), dim3(kLayWaves * kWave), 0, s, T * B, N_out, out_row_ptr,
                      out_col_idx, out_cap, b.perm, b.qoff, b.rec, b.src);
