@@ -2,17 +2,20 @@
 // V[0] = 0, the strict Heaviside of Eq. (spike_fn), and the input trace that Eq. (w_grad)
 // reuses (the filtered input of Eq. (lif_unrolled)).
 //
-// Two kernels, so that no block walks the whole time axis with gathers on its critical path:
-//   lif_gather  one wavefront per row (t, b), t < T-1: the ascending list of spiking inputs of
-//               S_in[t,b,:] (ballots over 1024-input segments, list in LDS), then
-//               I[t,b,:] = sum over that list of W[i,:], summed in ascending i. The row-parallel
-//               sums have no dependence on time, so every row's W gathers can be in flight at
-//               once. I[t,b,:] is parked in the slot of V[t+1,b,:].
-//   lif_scan    one thread per (b, j): the membrane recurrence over t, reading I from V[t+1]
-//               and overwriting it with V[t+1]; S_out[t] = V[t] > theta. And one thread per
-//               (b, four inputs): the input trace over t. Loads run 16 steps ahead.
+// The weighted input of a row (t, b) is I[t,b,:] = sum of W[i,:] over the row's spiking inputs,
+// added in ascending i (the list of spiking inputs comes from ballots over the row's bytes), and
+// the recurrence V[t+1] = (alpha V[t] + I[t]) - S_out[t], S_out[t] = V[t] > theta, walks time per
+// neuron. Two forms:
+//   lif_fused   (the default) one block per (sample, group of columns) walks time in tiles: its
+//               wavefronts form a tile's weighted inputs two rows each into LDS, then every
+//               thread runs its column's recurrence over the tile from LDS. V, S_out, the active
+//               bitset and the input trace are written once; the weighted inputs never reach HBM.
+//   lif_gather + lif_scan  (widths whose bitset words straddle samples, or whose W rows are not
+//               whole float4 columns) one wavefront per row parks I[t,b,:] in the slot of
+//               V[t+1,b,:]; then one thread per (b, j) runs the recurrence over t, overwriting it
+//               with V[t+1], and one thread per (b, four inputs) the input trace.
 // Float32 with separately rounded operations (__fmul_rn / __fadd_rn) and the ascending
-// summation order make V a deterministic function of the inputs.
+// summation order make V a deterministic function of the inputs; both forms give the same bits.
 #include "common.h"
 
 namespace snn {
@@ -34,22 +37,74 @@ __device__ __forceinline__ uint32_t load4(const uint8_t* p, int i, int n) {
   return x;
 }
 
-// NQ float4 column groups per lane: lane l holds columns 4 (l + 64 m) .. +3, m < NQ.
-// The row's spike bytes are read kSegPieces pieces at a time (all loads issued first), their
-// spiking inputs listed in LDS in ascending order, and the list's W rows summed in batches.
-template <bool ALIGNED, bool VEC, int NQ>
-__global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t* __restrict__ s_in,
-                                                                   const float* __restrict__ W, int T, int B,
-                                                                   int N_in, int N_out, float* __restrict__ V) {
-  constexpr int kBatch = NQ >= 16 ? 1 : (NQ >= 8 ? 2 : 4);  // W rows in flight: kBatch * NQ float4 loads
-  __shared__ uint16_t seg_list[kGatherWaves][kSegPieces * kPiece];
-  const int w = threadIdx.x / kWave;
+// The spike bytes of one segment of a row (kSegPieces pieces of 4 bytes per lane; bytes past
+// N_in read as no spike).
+template <bool ALIGNED>
+__device__ __forceinline__ void load_segment(const uint8_t* __restrict__ row, int s0, int N_in,
+                                             uint32_t (&x)[kSegPieces]) {
   const int l = lane_id();
-  const long r = (long)blockIdx.x * kGatherWaves + w;  // row r = t * B + b, t < T - 1
-  if (r >= (long)(T - 1) * B) return;
-  const uint8_t* row = s_in + (size_t)r * N_in;
-  uint16_t* lst = seg_list[w];
-  float acc[NQ][4];
+#pragma unroll
+  for (int c = 0; c < kSegPieces; ++c) x[c] = load4<ALIGNED>(row, s0 + c * kPiece + 4 * l, N_in);
+}
+
+// Ascending list (offsets inside the segment) of a segment's spiking inputs in lst; returns its
+// length.
+__device__ __forceinline__ int segment_list(const uint32_t (&x)[kSegPieces], uint16_t* lst) {
+  const int l = lane_id();
+  int base = 0;
+#pragma unroll
+  for (int c = 0; c < kSegPieces; ++c) {
+    const bool a0 = (x[c] & 0xffu) != 0, a1 = (x[c] & 0xff00u) != 0, a2 = (x[c] & 0xff0000u) != 0,
+               a3 = (x[c] & 0xff000000u) != 0;
+    const uint64_t m0 = __ballot(a0), m1 = __ballot(a1), m2 = __ballot(a2), m3 = __ballot(a3);
+    int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+    const int o = c * kPiece + 4 * l;
+    if (a0) lst[pos++] = (uint16_t)o;
+    if (a1) lst[pos++] = (uint16_t)(o + 1);
+    if (a2) lst[pos++] = (uint16_t)(o + 2);
+    if (a3) lst[pos++] = (uint16_t)(o + 3);
+    base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+  }
+  return base;
+}
+
+// Ascending list of a segment's spiking inputs as byte offsets inside their piece (piece c's
+// entries at [starts[c], starts[c + 1]) of lst); returns its length.
+__device__ __forceinline__ int segment_list8(const uint32_t (&x)[kSegPieces], uint8_t* lst, int (&starts)[kSegPieces]) {
+  const int l = lane_id();
+  int base = 0;
+#pragma unroll
+  for (int c = 0; c < kSegPieces; ++c) {
+    starts[c] = base;
+    const bool a0 = (x[c] & 0xffu) != 0, a1 = (x[c] & 0xff00u) != 0, a2 = (x[c] & 0xff0000u) != 0,
+               a3 = (x[c] & 0xff000000u) != 0;
+    const uint64_t m0 = __ballot(a0), m1 = __ballot(a1), m2 = __ballot(a2), m3 = __ballot(a3);
+    int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
+    const int o = 4 * l;
+    if (a0) lst[pos++] = (uint8_t)o;
+    if (a1) lst[pos++] = (uint8_t)(o + 1);
+    if (a2) lst[pos++] = (uint8_t)(o + 2);
+    if (a3) lst[pos++] = (uint8_t)(o + 3);
+    base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
+  }
+  return base;
+}
+
+// Input index of list entry e (s0: the segment's first input).
+__device__ __forceinline__ int list8_input(const uint8_t* lst, const int (&starts)[kSegPieces], int e, int s0) {
+  const int c = (e >= starts[1]) + (e >= starts[2]) + (e >= starts[3]);
+  return s0 + c * kPiece + (int)lst[e];
+}
+
+// The weighted input of one row (t, b) at NQ float4 column groups per lane: lane l sums columns
+// col0 + 4 (l + 64 m) .. +3, m < NQ, over the row's spiking inputs in ascending i, from +0.0 with
+// separately rounded adds. The row's spike bytes are read kSegPieces pieces at a time (all loads
+// issued first), their spiking inputs listed in lst (LDS) in ascending order, and the list's W
+// rows summed KB at a time (KB * NQ float4 loads in flight).
+template <bool ALIGNED, bool VEC, int NQ, int KB>
+__device__ __forceinline__ void row_input_sums(const uint8_t* __restrict__ row, const float* __restrict__ W, int N_in,
+                                               int N_out, int col0, uint16_t* lst, float (&acc)[NQ][4]) {
+  const int l = lane_id();
 #pragma unroll
   for (int m = 0; m < NQ; ++m)
 #pragma unroll
@@ -57,49 +112,34 @@ __global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t
 
   for (int s0 = 0; s0 < N_in; s0 += kSegPieces * kPiece) {
     uint32_t x[kSegPieces];
-#pragma unroll
-    for (int c = 0; c < kSegPieces; ++c) x[c] = load4<ALIGNED>(row, s0 + c * kPiece + 4 * l, N_in);
-    // ascending list of the segment's spiking inputs (offsets inside the segment)
-    int base = 0;
-#pragma unroll
-    for (int c = 0; c < kSegPieces; ++c) {
-      const bool a0 = (x[c] & 0xffu) != 0, a1 = (x[c] & 0xff00u) != 0, a2 = (x[c] & 0xff0000u) != 0,
-                 a3 = (x[c] & 0xff000000u) != 0;
-      const uint64_t m0 = __ballot(a0), m1 = __ballot(a1), m2 = __ballot(a2), m3 = __ballot(a3);
-      int pos = base + mask_prefix(m0) + mask_prefix(m1) + mask_prefix(m2) + mask_prefix(m3);
-      const int o = c * kPiece + 4 * l;
-      if (a0) lst[pos++] = (uint16_t)o;
-      if (a1) lst[pos++] = (uint16_t)(o + 1);
-      if (a2) lst[pos++] = (uint16_t)(o + 2);
-      if (a3) lst[pos++] = (uint16_t)(o + 3);
-      base += __popcll(m0) + __popcll(m1) + __popcll(m2) + __popcll(m3);
-    }
-    const int n = base;
+    load_segment<ALIGNED>(row, s0, N_in, x);
+    const int n = segment_list(x, lst);
     __builtin_amdgcn_wave_barrier();
-    // sums in ascending i, kBatch W rows in flight; positions past the list are clamped to its
-    // last entry and their sums skipped by a select
-    for (int k = 0; k < n; k += kBatch) {
-      float4 wv[kBatch][NQ];
+    // sums in ascending i, KB W rows in flight; positions past the list are clamped to its last
+    // entry and their sums skipped by a select
+    for (int k = 0; k < n; k += KB) {
+      float4 wv[KB][NQ];
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int u = 0; u < KB; ++u) {
         const int ii = s0 + (int)lst[min(k + u, n - 1)];
-        const float* wr = W + (size_t)ii * N_out;
+        const float* wr = W + (size_t)ii * N_out + col0;
 #pragma unroll
         for (int m = 0; m < NQ; ++m) {
           const int j = 4 * (l + kWave * m);
+          const int jn = N_out - col0;  // columns of the row from col0 on
           if (VEC) {
-            wv[u][m] = j < N_out ? *reinterpret_cast<const float4*>(wr + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+            wv[u][m] = j < jn ? *reinterpret_cast<const float4*>(wr + j) : make_float4(0.f, 0.f, 0.f, 0.f);
           } else {
-            wv[u][m].x = j < N_out ? wr[j] : 0.0f;
-            wv[u][m].y = j + 1 < N_out ? wr[j + 1] : 0.0f;
-            wv[u][m].z = j + 2 < N_out ? wr[j + 2] : 0.0f;
-            wv[u][m].w = j + 3 < N_out ? wr[j + 3] : 0.0f;
+            wv[u][m].x = j < jn ? wr[j] : 0.0f;
+            wv[u][m].y = j + 1 < jn ? wr[j + 1] : 0.0f;
+            wv[u][m].z = j + 2 < jn ? wr[j + 2] : 0.0f;
+            wv[u][m].w = j + 3 < jn ? wr[j + 3] : 0.0f;
           }
         }
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int u = 0; u < KB; ++u) {
         const bool take = k + u < n;
 #pragma unroll
         for (int m = 0; m < NQ; ++m) {
@@ -112,6 +152,22 @@ __global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t
     }
     __builtin_amdgcn_wave_barrier();  // the list is rewritten by the next segment
   }
+}
+
+// One wavefront per row (t, b), t < T - 1: the row's weighted input over every column, parked in
+// the slot of V[t+1, b, :].
+template <bool ALIGNED, bool VEC, int NQ>
+__global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t* __restrict__ s_in,
+                                                                   const float* __restrict__ W, int T, int B,
+                                                                   int N_in, int N_out, float* __restrict__ V) {
+  constexpr int kBatch = NQ >= 16 ? 1 : (NQ >= 8 ? 2 : 4);  // W rows in flight: kBatch * NQ float4 loads
+  __shared__ uint16_t seg_list[kGatherWaves][kSegPieces * kPiece];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  const long r = (long)blockIdx.x * kGatherWaves + w;  // row r = t * B + b, t < T - 1
+  if (r >= (long)(T - 1) * B) return;
+  float acc[NQ][4];
+  row_input_sums<ALIGNED, VEC, NQ, kBatch>(s_in + (size_t)r * N_in, W, N_in, N_out, 0, seg_list[w], acc);
   float* dst = V + (size_t)(r + B) * N_out;  // slot of V[t+1, b, :]
 #pragma unroll
   for (int m = 0; m < NQ; ++m) {
@@ -122,6 +178,46 @@ __global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         if (j + q < N_out) dst[j + q] = acc[m][q];
+    }
+  }
+}
+
+// The input trace of input quad k = b * ceil(N_in / 4) + quad over the whole time axis:
+// trace[0] = 0, trace[t+1] = alpha trace[t] + S_in[t] (loads kScanAhead steps ahead).
+template <bool ALIGNED>
+__device__ __forceinline__ void trace_walk(size_t k, const uint8_t* __restrict__ s_in, int T, int B, int N_in,
+                                           float alpha, float* __restrict__ trace) {
+  const int nq = (N_in + 3) / 4;
+  if (k >= (size_t)B * nq) return;
+  const int b = (int)(k / nq);
+  const int i = 4 * (int)(k - (size_t)b * nq);
+  const size_t step = (size_t)B * N_in;
+  float* dst0 = trace + (size_t)b * N_in + i;
+  float tr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (i + q < N_in) dst0[q] = 0.0f;
+  const uint8_t* src0 = s_in + (size_t)b * N_in;
+  for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
+    const int np = min(kScanAhead, T - 1 - t0);
+    uint32_t x[kScanAhead];
+#pragma unroll
+    for (int p = 0; p < kScanAhead; ++p) x[p] = load4<ALIGNED>(src0 + (size_t)(t0 + min(p, np - 1)) * step, i, N_in);
+#pragma unroll
+    for (int p = 0; p < kScanAhead; ++p) {
+      if (p < np) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          tr[q] = __fadd_rn(__fmul_rn(alpha, tr[q]), ((x[p] >> (8 * q)) & 0xffu) ? 1.0f : 0.0f);
+        float* dst = dst0 + (size_t)(t0 + p + 1) * step;
+        if (ALIGNED) {
+          *reinterpret_cast<float4*>(dst) = make_float4(tr[0], tr[1], tr[2], tr[3]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (i + q < N_in) dst[q] = tr[q];
+        }
+      }
     }
   }
 }
@@ -174,41 +270,201 @@ __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restri
     }
     if (valid) s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
   } else {
-    const int nq = (N_in + 3) / 4;
-    const size_t k = (size_t)(blockIdx.x - nv) * kScanThreads + threadIdx.x;  // b * nq + quad
-    if (k >= (size_t)B * nq) return;
-    const int b = (int)(k / nq);
-    const int i = 4 * (int)(k - (size_t)b * nq);
-    const size_t step = (size_t)B * N_in;
-    float* dst0 = trace + (size_t)b * N_in + i;
-    float tr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    trace_walk<ALIGNED>((size_t)(blockIdx.x - nv) * kScanThreads + threadIdx.x, s_in, T, B, N_in, alpha, trace);
+  }
+}
+
+// The weighted inputs of two rows at once (the sums and order of row_input_sums for each): the
+// rows' spike lists are formed segment by segment and their W rows summed together, KB of each
+// row in flight. x0 / x1 hold the first segment's spike bytes (loaded by the caller ahead of
+// time); a null row has no spikes.
+template <bool ALIGNED, int NQ, int KB>
+__device__ __forceinline__ void row_pair_sums(const uint8_t* r0, const uint8_t* r1, const uint32_t (&x0)[kSegPieces],
+                                              const uint32_t (&x1)[kSegPieces], const float* __restrict__ W,
+                                              int N_in, int N_out, int col0, uint8_t* lst0, uint8_t* lst1,
+                                              float (&acc0)[NQ][4], float (&acc1)[NQ][4]) {
+  const int l = lane_id();
+  const int jn = N_out - col0;  // columns of a W row from col0 on (a multiple of 4)
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (i + q < N_in) dst0[q] = 0.0f;
-    const uint8_t* src0 = s_in + (size_t)b * N_in;
-    for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
-      const int np = min(kScanAhead, T - 1 - t0);
-      uint32_t x[kScanAhead];
+  for (int m = 0; m < NQ; ++m)
 #pragma unroll
-      for (int p = 0; p < kScanAhead; ++p) x[p] = load4<ALIGNED>(src0 + (size_t)(t0 + min(p, np - 1)) * step, i, N_in);
+    for (int q = 0; q < 4; ++q) acc0[m][q] = acc1[m][q] = 0.0f;
+  for (int s0 = 0; s0 < N_in; s0 += kSegPieces * kPiece) {
+    uint32_t y0[kSegPieces], y1[kSegPieces];
 #pragma unroll
-      for (int p = 0; p < kScanAhead; ++p) {
-        if (p < np) {
+    for (int c = 0; c < kSegPieces; ++c) y0[c] = y1[c] = 0u;
+    if (s0 == 0) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            tr[q] = __fadd_rn(__fmul_rn(alpha, tr[q]), ((x[p] >> (8 * q)) & 0xffu) ? 1.0f : 0.0f);
-          float* dst = dst0 + (size_t)(t0 + p + 1) * step;
-          if (ALIGNED) {
-            *reinterpret_cast<float4*>(dst) = make_float4(tr[0], tr[1], tr[2], tr[3]);
-          } else {
+      for (int c = 0; c < kSegPieces; ++c) {
+        y0[c] = x0[c];
+        y1[c] = x1[c];
+      }
+    } else {
+      if (r0) load_segment<ALIGNED>(r0, s0, N_in, y0);
+      if (r1) load_segment<ALIGNED>(r1, s0, N_in, y1);
+    }
+    int st0[kSegPieces], st1[kSegPieces];
+    const int n0 = segment_list8(y0, lst0, st0);
+    const int n1 = segment_list8(y1, lst1, st1);
+    __builtin_amdgcn_wave_barrier();
+    const int n = max(n0, n1);
+    for (int k = 0; k < n; k += KB) {
+      float4 wa[KB][NQ], wb[KB][NQ];
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-              if (i + q < N_in) dst[q] = tr[q];
-          }
+      for (int u = 0; u < KB; ++u) {
+        const int i0 = n0 > 0 ? list8_input(lst0, st0, min(k + u, n0 - 1), s0) : s0;
+        const int i1 = n1 > 0 ? list8_input(lst1, st1, min(k + u, n1 - 1), s0) : s0;
+        const float* w0 = W + (size_t)i0 * N_out + col0;
+        const float* w1 = W + (size_t)i1 * N_out + col0;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m) {
+          const int j = 4 * (l + kWave * m);
+          wa[u][m] = j < jn ? *reinterpret_cast<const float4*>(w0 + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+          wb[u][m] = j < jn ? *reinterpret_cast<const float4*>(w1 + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int u = 0; u < KB; ++u) {
+        const bool t0 = k + u < n0, t1 = k + u < n1;
+#pragma unroll
+        for (int m = 0; m < NQ; ++m) {
+          acc0[m][0] = t0 ? __fadd_rn(acc0[m][0], wa[u][m].x) : acc0[m][0];
+          acc0[m][1] = t0 ? __fadd_rn(acc0[m][1], wa[u][m].y) : acc0[m][1];
+          acc0[m][2] = t0 ? __fadd_rn(acc0[m][2], wa[u][m].z) : acc0[m][2];
+          acc0[m][3] = t0 ? __fadd_rn(acc0[m][3], wa[u][m].w) : acc0[m][3];
+          acc1[m][0] = t1 ? __fadd_rn(acc1[m][0], wb[u][m].x) : acc1[m][0];
+          acc1[m][1] = t1 ? __fadd_rn(acc1[m][1], wb[u][m].y) : acc1[m][1];
+          acc1[m][2] = t1 ? __fadd_rn(acc1[m][2], wb[u][m].z) : acc1[m][2];
+          acc1[m][3] = t1 ? __fadd_rn(acc1[m][3], wb[u][m].w) : acc1[m][3];
         }
       }
     }
+    __builtin_amdgcn_wave_barrier();  // the lists are rewritten by the next segment
   }
+}
+
+// Fused forward. Blocks [0, nfb): one per (sample b, column group cg of JW = 256 NQ columns),
+// walking the time axis in tiles of kFuseP = 2 kFuseWaves steps. In a tile each wavefront forms the
+// weighted inputs of two of the tile's rows (row_pair_sums) in an LDS tile; after a barrier each
+// thread runs the membrane recurrence of its column over the tile's steps from the LDS tile, so
+// V, S_out and the active bitset are written once and the weighted inputs never reach HBM; the
+// spike bytes of the next tile's rows are requested before the recurrence. Blocks [nfb, ...):
+// the input trace, one thread per input quad (trace_walk), beside them. Bit-identical to
+// lif_gather + lif_scan. With a bitset each wavefront's 64 columns must be one bitset word
+// (N_out % 64 == 0, checked by the caller).
+constexpr int kFuseThreads = 512;
+constexpr int kFuseWaves = kFuseThreads / kWave;
+constexpr int kFuseP = 2 * kFuseWaves;  // steps per tile: two rows per wavefront
+
+template <bool ALIGNED, int NQ, bool STASH>
+__global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(4))) void lif_fused(
+    const uint8_t* __restrict__ s_in, const float* __restrict__ W, int T, int B, int N_in, int N_out, int G, int nfb,
+    float alpha, float theta, float b_th, float* __restrict__ V, uint8_t* __restrict__ s_out,
+    float* __restrict__ trace, uint64_t* __restrict__ bits) {
+  constexpr int JW = 4 * kWave * NQ;  // columns of a group
+  constexpr int KB = NQ >= 2 ? 4 : 8;
+  static_assert(JW <= kFuseThreads, "one scan thread per column of the group");
+  static_assert(!STASH || ALIGNED, "stashed spike bytes are whole input quads");
+  if (!STASH && (int)blockIdx.x >= nfb) {
+    trace_walk<ALIGNED>((size_t)(blockIdx.x - nfb) * kFuseThreads + threadIdx.x, s_in, T, B, N_in, alpha, trace);
+    return;
+  }
+  __shared__ __attribute__((aligned(16))) float tile[kFuseP][JW];
+  __shared__ uint8_t lists[2 * kFuseWaves][kSegPieces * kPiece];
+  // STASH (N_in <= one segment): the tile's spike bytes, input quad q of step p at [p][q], for the trace
+  __shared__ uint32_t rowbytes[STASH ? kFuseP : 1][kSegPieces * kWave];
+  const int w = threadIdx.x / kWave;
+  const int l = lane_id();
+  const int b = blockIdx.x / G;
+  const int cg = blockIdx.x - b * G;
+  const int c0 = cg * JW;
+  const size_t vstep = (size_t)B * N_out;
+  const size_t W64 = (vstep + kWave - 1) / kWave;
+  const size_t istep = (size_t)B * N_in;
+  // scan thread k: column c0 + k of sample b; wavefronts whose first column is past N_out skip
+  const int k = threadIdx.x;
+  const int kw = k - l;  // the wavefront's first column slot
+  const bool scan_wave = kw < JW && c0 + kw < N_out;
+  const bool valid = scan_wave && c0 + k < N_out;
+  const size_t vk = (size_t)b * N_out + c0 + (valid ? k : kw);
+  const size_t wword = ((size_t)b * N_out + c0 + kw) / kWave;
+  // rows w and w + kFuseWaves of tile t0 (null past T - 2)
+  auto row_of = [&](int t0, int p) -> const uint8_t* {
+    const int t = t0 + p;
+    return t < T - 1 ? s_in + (size_t)t * istep + (size_t)b * N_in : nullptr;
+  };
+  uint32_t x0[kSegPieces], x1[kSegPieces];
+  auto prefetch = [&](int t0) {
+    const uint8_t* r0 = row_of(t0, w);
+    const uint8_t* r1 = row_of(t0, w + kFuseWaves);
+#pragma unroll
+    for (int c = 0; c < kSegPieces; ++c) x0[c] = x1[c] = 0u;
+    if (r0) load_segment<ALIGNED>(r0, 0, N_in, x0);
+    if (r1) load_segment<ALIGNED>(r1, 0, N_in, x1);
+  };
+  // STASH: the trace of the group's input quads, thread k taking quad q_lo + k
+  const int nq = (N_in + 3) / 4;
+  const int qpg = (nq + G - 1) / G;
+  const int tq = (cg * qpg + k < nq && k < qpg) ? cg * qpg + k : -1;
+  float tr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (STASH && trace && tq >= 0)
+    *reinterpret_cast<float4*>(trace + (size_t)b * N_in + 4 * tq) = make_float4(0.f, 0.f, 0.f, 0.f);
+  float v = 0.0f;
+  if (valid) V[vk] = 0.0f;
+  if (bits && scan_wave) mark_active(bits, wword, valid, v, theta, b_th);
+  prefetch(0);
+  for (int t0 = 0; t0 < T - 1; t0 += kFuseP) {
+    const int np = min(kFuseP, T - 1 - t0);
+    if (STASH) {
+#pragma unroll
+      for (int c = 0; c < kSegPieces; ++c) {
+        rowbytes[w][c * kWave + l] = x0[c];
+        rowbytes[w + kFuseWaves][c * kWave + l] = x1[c];
+      }
+    }
+    {
+      float acc0[NQ][4], acc1[NQ][4];
+      row_pair_sums<ALIGNED, NQ, KB>(row_of(t0, w), row_of(t0, w + kFuseWaves), x0, x1, W, N_in, N_out, c0,
+                                     lists[w], lists[w + kFuseWaves], acc0, acc1);
+#pragma unroll
+      for (int m = 0; m < NQ; ++m) {
+        const int j = 4 * (l + kWave * m);
+        *reinterpret_cast<float4*>(&tile[w][j]) = make_float4(acc0[m][0], acc0[m][1], acc0[m][2], acc0[m][3]);
+        *reinterpret_cast<float4*>(&tile[w + kFuseWaves][j]) =
+            make_float4(acc1[m][0], acc1[m][1], acc1[m][2], acc1[m][3]);
+      }
+    }
+    __syncthreads();
+    prefetch(t0 + kFuseP);  // in flight during the recurrence
+    if (scan_wave) {
+#pragma unroll
+      for (int p = 0; p < kFuseP; ++p) {
+        if (p < np) {
+          const int t = t0 + p;
+          const bool sp = v > theta;
+          if (valid) s_out[(size_t)t * vstep + vk] = (uint8_t)sp;
+          v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), tile[p][k]), sp ? -1.0f : -0.0f);
+          if (valid) V[(size_t)(t + 1) * vstep + vk] = v;
+          if (bits) mark_active(bits, (size_t)(t + 1) * W64 + wword, valid, v, theta, b_th);
+        }
+      }
+    }
+    if (STASH && trace && tq >= 0) {
+      float* dst0 = trace + (size_t)b * N_in + 4 * tq;
+#pragma unroll
+      for (int p = 0; p < kFuseP; ++p) {
+        if (p < np) {
+          const uint32_t x = rowbytes[p][tq];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) tr[q] = __fadd_rn(__fmul_rn(alpha, tr[q]), ((x >> (8 * q)) & 0xffu) ? 1.0f : 0.0f);
+          *reinterpret_cast<float4*>(dst0 + (size_t)(t0 + p + 1) * istep) = make_float4(tr[0], tr[1], tr[2], tr[3]);
+        }
+      }
+    }
+    __syncthreads();  // the tile is rewritten by the next tile's sums
+  }
+  if (valid) s_out[(size_t)(T - 1) * vstep + vk] = (uint8_t)(v > theta);
 }
 
 template <bool ALIGNED, bool VEC>
@@ -347,6 +603,30 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool al = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0;
+  {  // the fused kernel: whole float4 W columns, whole bitset words per wavefront, a 16-byte aligned trace
+    const int fq = N_out > 4 * kWave ? 2 : 1;
+    const int G = (N_out + 4 * kWave * fq - 1) / (4 * kWave * fq);
+    if ((N_out % 4) == 0 && (reinterpret_cast<uintptr_t>(W) % 16) == 0 && (!bits || N_out % kWave == 0) &&
+        (!trace_in || !al || (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0)) {
+      // the trace from the tile's stashed spike bytes when a row is one segment and the group's input
+      // quads fit one per thread; otherwise trace blocks beside the fused blocks
+      const bool stash = al && N_in <= kSegPieces * kPiece && ((N_in + 3) / 4 + G - 1) / G <= kFuseThreads;
+      const int nfb = B * G;
+      const int ntb = (trace_in && !stash) ? (int)(((size_t)B * ((N_in + 3) / 4) + kFuseThreads - 1) / kFuseThreads) : 0;
+      const dim3 g((unsigned)(nfb + ntb));
+#define SNN_F(A, Q, ST)                                                                                           \
+  hipLaunchKernelGGL((lif_fused<A, Q, ST>), g, dim3(kFuseThreads), 0, s, s_in, W, T, B, N_in, N_out, G, nfb, alpha, \
+                     theta, b_th, V, s_out, trace_in, bits)
+      if (stash && fq == 2) SNN_F(true, 2, true);
+      else if (stash) SNN_F(true, 1, true);
+      else if (al && fq == 2) SNN_F(true, 2, false);
+      else if (al) SNN_F(true, 1, false);
+      else if (fq == 2) SNN_F(false, 2, false);
+      else SNN_F(false, 1, false);
+#undef SNN_F
+      return launch_status();
+    }
+  }
   const bool vec = (N_out % 4) == 0 && (reinterpret_cast<uintptr_t>(W) % 16) == 0 &&
                    (reinterpret_cast<uintptr_t>(V) % 16) == 0;
   const int NQ = (N_out + 4 * kWave - 1) / (4 * kWave);
