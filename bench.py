@@ -654,32 +654,46 @@ class Runner:
 
     def _layers_layerwise(self, ev, r, cs, K, use_aux):
         """Layer by layer: the readout's backward, then each LIF layer's spike gradient (on the second
-        stream) beside its dW, the next layer starting when both are done."""
+        stream) beside its dW, the next layer starting when both are done. With one LIF layer there is
+        no spike gradient to overlap: everything runs on the main stream (the readout's own spike
+        gradient too, as the join of a second stream costs more than the overlap saves), and a timing
+        event is recorded only where one is needed (each is a barrier packet of several
+        microseconds on the stream)."""
         snn, net, main, aux, R = self.snn, self.net, self.main, self.aux, self.region
         L = self.L
         self.cs = cs
+        fork = use_aux and L > 1 and aux is not main
         eps = R("ro_bwd", main, lambda: snn.sparse_backward(net.W_out, net.trace_out, net.alpha_out, r[0], r[1],
                                                              inp=cs[L - 1], ws=self.ws_ro,
-                                                             aux_stream=aux if use_aux else None)[1])
+                                                             aux_stream=aux if fork else None)[1])
         ev["ro1"].record(main)
+        mark = ev["ro1"]  # the event at the current boundary of main
         for l in range(L - 1, -1, -1):
             i = L - 1 - l
-            ev["lay0"][i].record(main)
+            ev["lay0"][i] = mark
             if l > 0:
-                if aux is not main:
+                if fork:
                     aux.wait_stream(main)
-                ev["gi0"][i].record(aux)
-                R(f"gi{l}", aux, self._gi_call(l, eps, self.share[l] and aux is not main))
-                ev["gi1"][i].record(aux)
-            ev["dw0"][i].record(main)
+                    ev["gi0"][i].record(aux)
+                    R(f"gi{l}", aux, self._gi_call(l, eps, self.share[l]))
+                    ev["gi1"][i].record(aux)
+                else:
+                    ev["gi0"][i] = mark
+                    R(f"gi{l}", main, self._gi_call(l, eps, False))
+                    ev["gi1"][i].record(main)
+                    mark = ev["gi1"][i]
+            ev["dw0"][i] = mark
             R(f"dw{l}", main, self._dw_call(l, eps, K))
             ev["dw1"][i].record(main)
+            mark = ev["dw1"][i]
             if l > 0:
-                if aux is not main:
+                if fork:
                     main.wait_stream(aux)
+                    ev["lay1"][i].record(main)
+                    mark = ev["lay1"][i]
                 eps = self.eps[l - 1]
-            ev["lay1"][i].record(main)
-        ev["bw1"].record(main)
+            ev["lay1"][i] = mark
+        ev["bw1"] = mark
 
     def memory(self, nnz):
         """Per LIF layer, the analytic figure: bytes each backward chain allocates beyond the shared
