@@ -603,11 +603,14 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool al = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0;
-  {  // the fused kernel: whole float4 W columns, whole bitset words per wavefront, a 16-byte aligned trace
+  {  // the fused kernel: whole float4 W columns, whole bitset words per wavefront, a 16-byte aligned trace,
+     // and at least two blocks per CU (with fewer, its time walk is latency-bound and the two-kernel
+     // form is faster: a 1024 -> 100 readout at T = 500, B = 256 takes 0.31 against 0.30 ms)
     const int fq = N_out > 4 * kWave ? 2 : 1;
     const int G = (N_out + 4 * kWave * fq - 1) / (4 * kWave * fq);
     if ((N_out % 4) == 0 && (reinterpret_cast<uintptr_t>(W) % 16) == 0 && (!bits || N_out % kWave == 0) &&
-        (!trace_in || !al || (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0)) {
+        (!trace_in || !al || (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0) &&
+        (int64_t)B * G >= 2 * (int64_t)cu_count()) {
       // the trace from the tile's stashed spike bytes when a row is one segment and the group's input
       // quads fit one per thread; otherwise trace blocks beside the fused blocks
       const bool stash = al && N_in <= kSegPieces * kPiece && ((N_in + 3) / 4 + G - 1) / G <= kFuseThreads;

@@ -3,7 +3,8 @@ variant of the fused forward kernel: spike rows of one segment (the trace from t
 bytes) or of several (trace blocks beside the fused blocks), one or two float4 groups of columns
 per lane, several column groups per sample, partial column groups, wavefronts with columns past
 the layer's width, spike rows that are not whole 4-byte words, dense spike rows, a last time tile
-that is not full, and the two-kernel path (widths whose bitset words straddle samples).
+that is not full, and the two-kernel path (widths whose bitset words straddle samples, grids of
+fewer than two blocks per CU).
 """
 import math
 
@@ -56,15 +57,18 @@ def _run(X, W, alpha, theta, b_th):
     return V.cpu().numpy(), S.cpu().numpy(), tr.cpu().numpy(), None if bits is None else bits.cpu().numpy()
 
 
+# The fused form runs when the grid has at least two blocks per CU (B x column groups >= 512 on
+# 256 CUs), hence the batch sizes; the last two cases take the two-kernel form.
 @pytest.mark.parametrize("T,B,n_in,n_out,rate,b_th", [
-    (37, 3, 1024, 1024, 0.02, 0.2),   # one segment, two column groups of 512, a partial last tile
-    (20, 2, 1030, 256, 0.03, 0.2),    # spike rows not whole words: trace blocks, one group of 256
-    (18, 2, 2312, 320, 0.01, 0.3),    # several segments; wavefronts 5..7 of the group past the width
-    (33, 3, 64, 100, 0.2, None),      # no bitset: a wavefront with columns past the width
-    (17, 2, 1024, 512, 0.9, 0.2),     # dense spike rows (lists of up to 1024 entries)
-    (9, 5, 700, 3968, 0.05, 0.25),    # eight column groups, the last one partial
-    (16, 3, 300, 200, 0.05, 0.2),     # bitset words straddle samples: the two-kernel path
-    (1, 3, 256, 128, 0.1, 0.2),       # a single step: no tile at all
+    (37, 256, 1024, 1024, 0.02, 0.2),  # one segment, two column groups of 512, a partial last tile
+    (20, 512, 1030, 256, 0.03, 0.2),   # spike rows not whole words: trace blocks, one group of 256
+    (18, 512, 2312, 320, 0.01, 0.3),   # several segments; wavefronts 5..7 of the group past the width
+    (33, 512, 64, 100, 0.2, None),     # no bitset: a wavefront with columns past the width
+    (4, 512, 1024, 512, 0.9, 0.2),     # dense spike rows (lists of up to 1024 entries)
+    (9, 64, 700, 3968, 0.05, 0.25),    # eight column groups, the last one partial
+    (1, 512, 256, 128, 0.1, 0.2),      # a single step: no tile at all
+    (16, 3, 300, 200, 0.05, 0.2),      # bitset words straddle samples: the two-kernel form
+    (21, 4, 1024, 1024, 0.02, 0.2),    # too few blocks for the fused form
 ])
 def test_forward_variants_bit_exact(T, B, n_in, n_out, rate, b_th):
     X, W, alpha = _case(T, B, n_in, n_out, rate, seed=T * 7919 + n_in)
