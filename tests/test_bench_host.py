@@ -163,5 +163,8 @@ def test_bench_line_on_conv(extra):
     assert ("conv-layer CSR" in line["sparse_chain"]) == ("--conv-csr" in extra)
     rl = line["roofline"]
     assert rl["bound"] == "hbm" and 0 < rl["frac"] < 1 and math.isclose(rl["frac"], rl["achieved"] / rl["peak"])
+    # the roofline covers the whole chain; the pooled active set is a secondary figure
+    assert math.isclose(rl["launch_ms"], line["sparse_backward_ms"]) and 0 < rl["pooled_active_set"]["frac"] < 1
+    assert 0 < line["value_pooled_entries"] < line["value"]
     if "--no-dense" not in extra:
         assert line["dense_backward_ms"] > 0 and line["speedup_vs_dense"] > 1
