@@ -6,10 +6,12 @@ chain, and the dense matrix-core baseline chain. HIP events time each part; the 
 the sparse backward (compaction + sparse backward of every LIF layer; the readout's own
 backward and the loss are outside both chains, as are the forward passes).
 
-In each LIF layer the spike gradient (snn_sparse_grad_in) runs on an auxiliary stream beside
-dW (snn_sparse_dw) on the main stream; the layer's time is taken on the main stream from the
-fork to the join. dW is the dominant kernel: events on the main stream bracket each of its
-calls, and the roofline object is computed from those durations.
+Schedule of the LIF layers' backward: with two or more LIF layers the spike gradients form a chain
+on the main stream and the dW calls' structure-only layouts run on a side stream from the start of
+the chain; a dW call that fills the GPU by itself (stress) runs on the main stream after its
+layer's spike gradient, smaller ones on dW streams beside the chain. With one LIF layer everything
+runs on one stream. HIP events on the stream each call runs on bracket every dW call and spike
+gradient; dW is the dominant kernel and the roofline object is computed from its calls' durations.
 
 Prints ONE JSON line. `value` = active neuron-steps per second of the sparse backward
 (sum over LIF layers of the active entries, divided by its time); the dense time and the
