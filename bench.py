@@ -596,7 +596,9 @@ class Runner:
         T, B, L = self.T, self.B, self.L
         self.cs = cs
         inline = self.n_dw == 1  # one dW call fills the GPU
-        dw_streams = [main] if inline else ([side] + self.dw_extra)[:self.n_dw]
+        # the dW streams: the extra ones first, so that the top layer's dW waits only for its own
+        # layout, not behind every layout queued on the side stream
+        dw_streams = [main] if inline else (self.dw_extra + [side])[:self.n_dw]
         eps = R("ro_gi", main, lambda: snn.sparse_grad_in(net.W_out, net.alpha_out, T, B, r[0], r[1], cs[L - 1],
                                                          share_cu=not inline, ws=self.ws_gi, eps_in=self.eps[L - 1]))
         ev["ro1"].record(main)
@@ -636,6 +638,7 @@ class Runner:
             R("ro_dw", main, lambda: snn.sparse_dw(net.trace_out, r[0], r[1], net.W_out.shape[1], ws=self.ws_ro,
                                                   dW=self.dW_out))
             return
+        mark = ev["ro1"]  # timing events only where a span needs one (each is a barrier packet)
         for l in range(L - 1, -1, -1):
             i = L - 1 - l  # top layer first
             sd = dw_streams[i % len(dw_streams)]
@@ -643,15 +646,16 @@ class Runner:
                 sd.wait_stream(main)  # eps of layer l is ready
             if laid[l] is not None:
                 sd.wait_event(laid[l])
-            ev["lay0"][i].record(sd)
             ev["dw0"][i].record(sd)
+            ev["lay0"][i] = ev["dw0"][i]
             R(f"dw{l}", sd, self._dw_call(l, eps, K, prepared=not K))
             ev["dw1"][i].record(sd)
-            ev["lay1"][i].record(sd)
+            ev["lay1"][i] = ev["dw1"][i]
             if l > 0:
-                ev["gi0"][i].record(main)
+                ev["gi0"][i] = mark
                 R(f"gi{l}", main, self._gi_call(l, eps, not inline))
                 ev["gi1"][i].record(main)
+                mark = ev["gi1"][i]
                 eps = self.eps[l - 1]
         for sd in [side] + dw_streams:
             if sd is not main:
