@@ -53,6 +53,7 @@ namespace {
 constexpr int kScanThreads = 256;
 constexpr int kScanPerThread = 8;
 constexpr int kScanTile = kScanThreads * kScanPerThread;
+constexpr int kOwnPrefixTiles = 1024;
 
 // Block-wide exclusive scan of one value per thread; returns the block total through *total.
 __device__ int block_excl_scan(int v, int* total) {
@@ -115,23 +116,35 @@ __global__ __launch_bounds__(kScanThreads) void scan_sums(int32_t* sums, int nb)
   }
 }
 
+// Each tile's offset is sums[tile] (scanned by scan_sums), or, with own_prefix, the sum of the
+// earlier tiles' totals formed by the block itself (few tiles: one kernel less on the chain).
 __global__ __launch_bounds__(kScanThreads) void scan_apply(const int32_t* counts, int n, const int32_t* sums,
-                                                           int nb, int32_t* out, int64_t* total64) {
+                                                           int nb, int32_t* out, int64_t* total64, int own_prefix) {
   int x[kScanPerThread];
   const int base = blockIdx.x * kScanTile + threadIdx.x * kScanPerThread;
   load_tile(counts, n, base, x);
+  int prefix;
+  if (own_prefix) {
+    int p = 0;
+    for (int k = threadIdx.x; k < (int)blockIdx.x; k += kScanThreads) p += sums[k];
+    int all;
+    (void)block_excl_scan(p, &all);
+    prefix = all;
+  } else {
+    prefix = sums[blockIdx.x];
+  }
   int s = 0;
 #pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) s += x[k];
   int total;
-  int ex = block_excl_scan(s, &total) + sums[blockIdx.x];
+  int ex = block_excl_scan(s, &total) + prefix;
 #pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) {
     if (base + k < n) out[base + k] = ex;
     ex += x[k];
   }
   if ((int)blockIdx.x == nb - 1 && threadIdx.x == 0) {
-    int grand = sums[blockIdx.x] + total;
+    int grand = prefix + total;
     out[n] = grand;
     if (total64) *total64 = (int64_t)grand;
   }
@@ -144,9 +157,13 @@ size_t scan_temp_elems(int n) { return (size_t)((n + kScanTile - 1) / kScanTile)
 void launch_exclusive_scan(const int32_t* counts, int n, int32_t* out, int64_t* total64, int32_t* temp,
                            hipStream_t stream) {
   const int nb = (n + kScanTile - 1) / kScanTile;
+  // up to kOwnPrefixTiles tiles each block adds the earlier tiles' totals itself (two kernels);
+  // beyond, one block scans the tile totals first (three kernels)
+  const bool own = nb <= kOwnPrefixTiles;
   hipLaunchKernelGGL(scan_tile_sums, dim3(nb), dim3(kScanThreads), 0, stream, counts, n, temp);
-  hipLaunchKernelGGL(scan_sums, dim3(1), dim3(kScanThreads), 0, stream, temp, nb);
-  hipLaunchKernelGGL(scan_apply, dim3(nb), dim3(kScanThreads), 0, stream, counts, n, temp, nb, out, total64);
+  if (!own) hipLaunchKernelGGL(scan_sums, dim3(1), dim3(kScanThreads), 0, stream, temp, nb);
+  hipLaunchKernelGGL(scan_apply, dim3(nb), dim3(kScanThreads), 0, stream, counts, n, temp, nb, out, total64,
+                     own ? 1 : 0);
 }
 
 }  // namespace snn
