@@ -10,10 +10,11 @@
 //               wavefronts form a tile's weighted inputs two rows each into LDS, then every
 //               thread runs its column's recurrence over the tile from LDS. V, S_out, the active
 //               bitset and the input trace are written once; the weighted inputs never reach HBM.
-//   lif_gather + lif_scan  (widths whose bitset words straddle samples, or whose W rows are not
-//               whole float4 columns) one wavefront per row parks I[t,b,:] in the slot of
-//               V[t+1,b,:]; then one thread per (b, j) runs the recurrence over t, overwriting it
-//               with V[t+1], and one thread per (b, four inputs) the input trace.
+//   lif_gather + lif_scan  (widths whose bitset words straddle samples, W rows that are not
+//               whole float4 columns, grids of fewer than two blocks per CU) one wavefront per row
+//               parks I[t,b,:] in the slot of V[t+1,b,:]; then one thread per (b, j) runs the
+//               recurrence over t, overwriting it with V[t+1], and one thread per (b, input) the
+//               input trace.
 // Float32 with separately rounded operations (__fmul_rn / __fadd_rn) and the ascending
 // summation order make V a deterministic function of the inputs; both forms give the same bits.
 #include "common.h"
@@ -182,11 +183,37 @@ __global__ __launch_bounds__(kGatherWaves * kWave) void lif_gather(const uint8_t
   }
 }
 
-// The input trace of input quad k = b * ceil(N_in / 4) + quad over the whole time axis:
-// trace[0] = 0, trace[t+1] = alpha trace[t] + S_in[t] (loads kScanAhead steps ahead).
-template <bool ALIGNED>
+// The input trace of input k = b * N_in + i over the whole time axis: trace[0] = 0,
+// trace[t+1] = alpha trace[t] + S_in[t] (loads kScanAhead steps ahead). One input per lane, not
+// four: four times the wavefronts for the same bytes, so that more of them overlap their load and
+// store phases (T = 500, B = 256, 1024 inputs: 0.152 -> 0.123 ms beside the recurrence).
 __device__ __forceinline__ void trace_walk(size_t k, const uint8_t* __restrict__ s_in, int T, int B, int N_in,
                                            float alpha, float* __restrict__ trace) {
+  const size_t step = (size_t)B * N_in;
+  if (k >= step) return;
+  float tr = 0.0f;
+  trace[k] = 0.0f;
+  for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
+    const int np = min(kScanAhead, T - 1 - t0);
+    uint32_t x[kScanAhead];
+#pragma unroll
+    for (int p = 0; p < kScanAhead; ++p) x[p] = s_in[(size_t)(t0 + min(p, np - 1)) * step + k];
+#pragma unroll
+    for (int p = 0; p < kScanAhead; ++p) {
+      if (p < np) {
+        tr = __fadd_rn(__fmul_rn(alpha, tr), x[p] ? 1.0f : 0.0f);
+        trace[(size_t)(t0 + p + 1) * step + k] = tr;
+      }
+    }
+  }
+}
+
+// The input trace of input quad k = b * ceil(N_in / 4) + quad over the whole time axis, as
+// trace_walk (the trace blocks beside lif_fused's blocks: there four inputs per lane are faster,
+// 0.326 against 0.340 ms at T = 100, B = 512, 2312 inputs).
+template <bool ALIGNED>
+__device__ __forceinline__ void trace_walk4(size_t k, const uint8_t* __restrict__ s_in, int T, int B, int N_in,
+                                            float alpha, float* __restrict__ trace) {
   const int nq = (N_in + 3) / 4;
   if (k >= (size_t)B * nq) return;
   const int b = (int)(k / nq);
@@ -223,7 +250,7 @@ __device__ __forceinline__ void trace_walk(size_t k, const uint8_t* __restrict__
 }
 
 // Blocks [0, nv) run the membrane recurrence of B * N_out neurons; blocks [nv, nv + nt) run the
-// trace of B * ceil(N_in / 4) input quads.
+// trace of B * N_in inputs.
 // With bits != NULL the recurrence also marks the active set of Definition 1: bit (t, k) of the
 // bitset, k = b * N_out + j, is |V[t,b,j] - theta| < b_th in float32, word t * W64 + k / 64,
 // W64 = ceil(B * N_out / 64); one ballot per wavefront and step (its 64 k are one word).
@@ -233,7 +260,6 @@ __device__ __forceinline__ void mark_active(uint64_t* bits, size_t word, bool va
   if (lane_id() == 0) bits[word] = m;
 }
 
-template <bool ALIGNED>
 __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restrict__ s_in, int T, int B, int N_in,
                                                          int N_out, float alpha, float theta, float b_th,
                                                          float* __restrict__ V, uint8_t* __restrict__ s_out,
@@ -270,7 +296,7 @@ __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restri
     }
     if (valid) s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
   } else {
-    trace_walk<ALIGNED>((size_t)(blockIdx.x - nv) * kScanThreads + threadIdx.x, s_in, T, B, N_in, alpha, trace);
+    trace_walk((size_t)(blockIdx.x - nv) * kScanThreads + threadIdx.x, s_in, T, B, N_in, alpha, trace);
   }
 }
 
@@ -350,7 +376,7 @@ __device__ __forceinline__ void row_pair_sums(const uint8_t* r0, const uint8_t* 
 // thread runs the membrane recurrence of its column over the tile's steps from the LDS tile, so
 // V, S_out and the active bitset are written once and the weighted inputs never reach HBM; the
 // spike bytes of the next tile's rows are requested before the recurrence. Blocks [nfb, ...):
-// the input trace, one thread per input quad (trace_walk), beside them. Bit-identical to
+// the input trace, one thread per input quad (trace_walk4), beside them. Bit-identical to
 // lif_gather + lif_scan. With a bitset each wavefront's 64 columns must be one bitset word
 // (N_out % 64 == 0, checked by the caller).
 constexpr int kFuseThreads = 512;
@@ -367,7 +393,7 @@ __global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(4)
   static_assert(JW <= kFuseThreads, "one scan thread per column of the group");
   static_assert(!STASH || ALIGNED, "stashed spike bytes are whole input quads");
   if (!STASH && (int)blockIdx.x >= nfb) {
-    trace_walk<ALIGNED>((size_t)(blockIdx.x - nfb) * kFuseThreads + threadIdx.x, s_in, T, B, N_in, alpha, trace);
+    trace_walk4<ALIGNED>((size_t)(blockIdx.x - nfb) * kFuseThreads + threadIdx.x, s_in, T, B, N_in, alpha, trace);
     return;
   }
   __shared__ __attribute__((aligned(16))) float tile[kFuseP][JW];
@@ -605,7 +631,8 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
   const bool al = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0;
   {  // the fused kernel: whole float4 W columns, whole bitset words per wavefront, a 16-byte aligned trace,
      // and at least two blocks per CU (with fewer, its time walk is latency-bound and the two-kernel
-     // form is faster: a 1024 -> 100 readout at T = 500, B = 256 takes 0.31 against 0.30 ms)
+     // form is faster: a 1024 -> 100 readout at T = 500, B = 256, 5% input spikes, takes 0.61 against
+     // 0.46 ms)
     const int fq = N_out > 4 * kWave ? 2 : 1;
     const int G = (N_out + 4 * kWave * fq - 1) / (4 * kWave * fq);
     if ((N_out % 4) == 0 && (reinterpret_cast<uintptr_t>(W) % 16) == 0 && (!bits || N_out % kWave == 0) &&
@@ -642,14 +669,9 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
     else launch_gather<false, false>(NQ, g, s, s_in, W, T, B, N_in, N_out, V);
   }
   const int nv = (int)(((size_t)B * N_out + kScanThreads - 1) / kScanThreads);
-  const int nt = trace_in ? (int)(((size_t)B * ((N_in + 3) / 4) + kScanThreads - 1) / kScanThreads) : 0;
-  const bool tal = al && (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0;
-  if (tal)
-    hipLaunchKernelGGL(lif_scan<true>, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out,
-                       alpha, theta, b_th, V, s_out, trace_in, bits, nv);
-  else
-    hipLaunchKernelGGL(lif_scan<false>, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out,
-                       alpha, theta, b_th, V, s_out, trace_in, bits, nv);
+  const int nt = trace_in ? (int)(((size_t)B * N_in + kScanThreads - 1) / kScanThreads) : 0;
+  hipLaunchKernelGGL(lif_scan, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out, alpha,
+                     theta, b_th, V, s_out, trace_in, bits, nv);
   return launch_status();
 }
 
@@ -692,15 +714,9 @@ extern "C" snn_status snn_conv_lif_forward(const uint8_t* s_in, const float* Wc,
                        alpha, theta, b_th, V, s_out, active_bits);
   if (trace_in) {  // the input trace: lif_scan's trace blocks alone
     const int N_in = H * W * C;
-    const int nt = (int)(((size_t)B * ((N_in + 3) / 4) + kScanThreads - 1) / kScanThreads);
-    const bool tal = (N_in % 4) == 0 && (reinterpret_cast<uintptr_t>(s_in) % 4) == 0 &&
-                     (reinterpret_cast<uintptr_t>(trace_in) % 16) == 0;
-    if (tal)
-      hipLaunchKernelGGL(lif_scan<true>, dim3((unsigned)nt), dim3(kScanThreads), 0, s, s_in, T, B, N_in, 1, alpha,
-                         theta, b_th, nullptr, nullptr, trace_in, nullptr, 0);
-    else
-      hipLaunchKernelGGL(lif_scan<false>, dim3((unsigned)nt), dim3(kScanThreads), 0, s, s_in, T, B, N_in, 1, alpha,
-                         theta, b_th, nullptr, nullptr, trace_in, nullptr, 0);
+    const int nt = (int)(((size_t)B * N_in + kScanThreads - 1) / kScanThreads);
+    hipLaunchKernelGGL(lif_scan, dim3((unsigned)nt), dim3(kScanThreads), 0, s, s_in, T, B, N_in, 1, alpha, theta,
+                       b_th, nullptr, nullptr, trace_in, nullptr, 0);
   }
   return launch_status();
 }
