@@ -94,10 +94,14 @@ def test_workspace_queries(lib):
     assert lib.snn_sparse_backward_workspace(500, 256, 1024, 1024, 10 ** 6) > 0
     assert lib.snn_sparse_backward_workspace(10, 4, 0, 16, 10) == 0
     assert lib.snn_sparse_backward_workspace(10, 4, 8, 16, -1) == 0
-    # the slab-major entry copy grows with the entry capacity (layers of more than 32 outputs);
-    # narrow layers use a dense G of T*B*N_out instead, whatever the capacity
+    # the slab-major entry copy grows with the entry capacity (layers of more than 300 outputs, or
+    # of more than 1024 inputs, that do not take the matrix cores); layers of 33..300 outputs and
+    # at most 1024 inputs read the CSR directly and narrow layers use a dense G of T*B*N_out,
+    # whatever the capacity
+    assert (lib.snn_sparse_backward_workspace(10, 4, 8, 2048, 10 ** 5)
+            > lib.snn_sparse_backward_workspace(10, 4, 8, 2048, 10))
     assert (lib.snn_sparse_backward_workspace(10, 4, 8, 64, 10 ** 5)
-            > lib.snn_sparse_backward_workspace(10, 4, 8, 64, 10))
+            == lib.snn_sparse_backward_workspace(10, 4, 8, 64, 10) > 0)
     assert (lib.snn_sparse_backward_workspace(10, 4, 8, 16, 10 ** 5)
             == lib.snn_sparse_backward_workspace(10, 4, 8, 16, 10) >= 2 * 10 * 4 * 16 * 4)
     assert lib.snn_dense_backward_workspace(500, 256, 1024, 1024) >= 2 * 500 * 256 * 1024 * 4
