@@ -619,9 +619,18 @@ __global__ void fill_zero(float* __restrict__ p, size_t n) {
 }
 
 __global__ void reduce_chunks(const float* __restrict__ part, int n_chunks, size_t n, float* __restrict__ out) {
+  constexpr int kAhead = 8;  // partials loaded before any is added (the adds keep chunk order)
   for (size_t k = blockIdx.x * (size_t)blockDim.x + threadIdx.x; k < n; k += (size_t)gridDim.x * blockDim.x) {
     double s = 0.0;  // fixed order, rounded once
-    for (int c = 0; c < n_chunks; ++c) s += (double)part[(size_t)c * n + k];
+    int c = 0;
+    for (; c + kAhead <= n_chunks; c += kAhead) {
+      float v[kAhead];
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) v[u] = part[(size_t)(c + u) * n + k];
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) s += (double)v[u];
+    }
+    for (; c < n_chunks; ++c) s += (double)part[(size_t)c * n + k];
     out[k] = (float)s;
   }
 }
@@ -933,7 +942,19 @@ __global__ void gin_carries(int T, int B, int N_out, float alpha, int P, int C, 
   float aLast = 1.0f;
   for (int s = 0; s < last_len; ++s) aLast *= alpha;
   float x = 0.0f;
-  for (int c = C - 1; c >= 0; --c) {
+  constexpr int kAhead = 8;  // chunk sums loaded before the carries overwrite them
+  int c = C - 1;
+  for (; c + 1 >= kAhead; c -= kAhead) {
+    float Lv[kAhead];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) Lv[u] = buf[(size_t)(c - u) * BN + k];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+      buf[(size_t)(c - u) * BN + k] = x;
+      x = (c - u == C - 1 ? aLast : aP) * x + Lv[u];
+    }
+  }
+  for (; c >= 0; --c) {
     const float Lc = buf[(size_t)c * BN + k];
     buf[(size_t)c * BN + k] = x;
     x = (c == C - 1 ? aLast : aP) * x + Lc;
