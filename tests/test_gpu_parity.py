@@ -469,6 +469,19 @@ def test_parity_matrix_core_widths(hidden, n_in, n_ro, T, B):
     check_all(inp, 0.4, _gpu(inp, 0.4), _oracle(inp, 0.4))
 
 
+@pytest.mark.parametrize("b_th", [0.6, 1.2])
+def test_parity_csr_direct_dw_dense_rows(b_th):
+    """The CSR-direct dW (layers of up to 300 outputs and 1024 inputs) with most neurons active:
+    batches of 8 rows with more than 64 entries take their rest in pieces of 64 (second pass),
+    two hidden layers so the spike gradient walk runs between them."""
+    inp = _wide((200, 150), 40, 10, T=30, B=4)
+    print(f"\n[case] CSR-direct dW dense rows 40->(200, 150)->10 b_th={b_th}", flush=True)
+    g = _gpu(inp, b_th)
+    per_row = [c.nnz() / (30 * 4) for c in g["csrs"]]
+    assert max(per_row) > 8, per_row  # more than 64 entries per batch of 8 rows on average
+    check_all(inp, b_th, g, _oracle(inp, b_th))
+
+
 @pytest.mark.parametrize("hidden,n_ro", [((24, 31), 3), ((31,), 8), ((24,), 9), ((40, 17), 16), ((32,), 32),
                                           ((29,), 33)])
 def test_parity_narrow_outputs(hidden, n_ro):
