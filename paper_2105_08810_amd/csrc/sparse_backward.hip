@@ -68,6 +68,20 @@ DwPlan plan_dw(int T, int B, int N_in, int N_out) {
   return p;
 }
 
+// dw_slab_kernel's grid: plan_dw's slabs and input tiles, and one round of blocks over the CUs
+// in chunks of interleaved row groups (about eight rounds of time-sliced chunks before: the
+// last round left CUs idle and the busiest time slice set the pace; audio 700 -> 400 dW 0.099
+// -> 0.089 ms, event 2312 -> 200 0.436 -> 0.383, stress at B_th 1.2 126 -> 118 ms).
+DwPlan plan_dw_interleaved(int T, int B, int N_in, int N_out) {
+  DwPlan p = plan_dw(T, B, N_in, N_out);
+  const int per_cu = (int)std::max<size_t>(1, std::min<size_t>(2, (160 * 1024) / p.lds));
+  int nc = cu_count() * per_cu / (p.n_itiles * p.n_slabs);
+  nc = std::min(nc, (T * B + kDwWaves * kRowsPerBatch - 1) / (kDwWaves * kRowsPerBatch));  // a row group each
+  p.n_chunks = std::max(1, std::min(nc, 64));
+  p.rows_per_chunk = 0;  // chunks take row groups round-robin
+  return p;
+}
+
 // dW of layers of up to kRowsOutMax outputs and kRowsInMax inputs (dw_rows_kernel): a block
 // holds all of the layer's columns for 64 inputs, so it walks the output CSR directly (no record
 // passes before it); about one round of blocks over the CUs. Wider layers (two or more slabs)
@@ -229,7 +243,7 @@ __global__ __launch_bounds__(kRowWaves * kWave) void slab_fill(int TB, int N_out
 __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __restrict__ trace, int TB, int N_in,
                                                              int N_out, const int32_t* __restrict__ sp,
                                                              const SlabRec* __restrict__ rec, int64_t nrec,
-                                                             float* __restrict__ out, int rows_per_chunk,
+                                                             float* __restrict__ out, int n_chunks,
                                                              int n_itiles, int n_slabs, int slab) {
   extern __shared__ double acc[];  // [slab][kLd]
   int id = blockIdx.x;
@@ -254,26 +268,28 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   for (int k = tid; k < slab * kLd; k += kDwThreads) acc[k] = 0.0;
   __syncthreads();
 
-  const int r_lo = c * rows_per_chunk;
-  const int r_hi = min(TB, r_lo + rows_per_chunk);
+  // Chunk c takes the groups of kDwWaves * kRowsPerBatch rows c, c + n_chunks, ...: every chunk
+  // spans the whole time axis, so that one round of blocks finishes together wherever the
+  // activity lies in time. Wavefront w takes rows [8 w, 8 w + 8) of each of its chunk's groups.
+  const int r_hi = TB;
   const int2* rec2 = reinterpret_cast<const int2*>(rec);
   // Software pipeline over batches of 8 rows: while a batch is processed, the next batch's
   // trace values and records are in flight and the row pointers of the one after it. Rows past
-  // r_hi read sp[r_hi] (empty ranges); a row with no entry in this slab reads the chunk's first
+  // TB read sp[TB] (empty ranges); a row with no entry in this slab reads the batch's first
   // trace row instead of its own (a cache hit, never used).
   auto load_sp = [&](int rb) { return spl[min(rb + min(l, kRowsPerBatch), r_hi)]; };
   auto load_rest = [&](int rb, int spv, float* t0, float* t1, int2& ra) {
 #pragma unroll
     for (int k = 0; k < kRowsPerBatch; ++k) {
       const bool any = rdlane(spv, k + 1) > rdlane(spv, k);
-      const size_t row = (size_t)(any ? min(rb + k, r_hi - 1) : r_lo) * N_in;
+      const size_t row = (size_t)(any ? min(rb + k, r_hi - 1) : min(rb, r_hi - 1)) * N_in;
       t0[k] = trace[row + ic0];
       t1[k] = trace[row + ic1];
     }
     ra = rec2[min((int64_t)rdlane(spv, 0) + l, nrec - 1)];  // lane s holds the batch's record s
   };
-  constexpr int kStride = kDwWaves * kRowsPerBatch;
-  int rb = r_lo + w * kRowsPerBatch;
+  const int kStride = kDwWaves * kRowsPerBatch * n_chunks;
+  int rb = c * kDwWaves * kRowsPerBatch + w * kRowsPerBatch;
   int spv = load_sp(rb);
   float tr0[kRowsPerBatch], tr1[kRowsPerBatch];
   int2 ra;
@@ -1318,7 +1334,7 @@ size_t dw_workspace(int T, int B, int N_in, int N_out, int64_t out_cap) {
     const DwPlan p = plan_dw_rows(T, B, N_in, N_out);
     return p.n_chunks > 1 ? (size_t)p.n_chunks * N_in * N_out * sizeof(float) : 256;
   }
-  const DwPlan p = plan_dw(T, B, N_in, N_out);
+  const DwPlan p = plan_dw_interleaved(T, B, N_in, N_out);
   const int nsp = p.n_slabs * T * B;
   Carve c(nullptr);
   if (p.n_chunks > 1) c.take<float>((size_t)p.n_chunks * N_in * N_out);
@@ -1430,7 +1446,7 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
     return;
   }
   const int TB = T * B;
-  const DwPlan p = plan_dw(T, B, N_in, N_out);
+  const DwPlan p = plan_dw_interleaved(T, B, N_in, N_out);
   Carve ws(workspace);
   float* part = p.n_chunks > 1 ? ws.take<float>((size_t)p.n_chunks * N_in * N_out) : dW;
   const int nsp = p.n_slabs * TB;
@@ -1459,7 +1475,7 @@ void enqueue_dw(const float* trace_in, int T, int B, int N_in, int N_out, const 
   const dim3 dgrid((unsigned)(p.n_itiles * p.n_slabs * p.n_chunks));
   ensure_dynamic_lds((const void*)dw_slab_kernel, (int)p.lds);
   hipLaunchKernelGGL(dw_slab_kernel, dgrid, dim3(kDwThreads), p.lds, s, trace_in, TB, N_in, N_out, sp, rec, nrec,
-                     part, p.rows_per_chunk, p.n_itiles, p.n_slabs, p.slab);
+                     part, p.n_chunks, p.n_itiles, p.n_slabs, p.slab);
   if (p.n_chunks > 1) {
     const size_t n = (size_t)N_in * N_out;
     const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
