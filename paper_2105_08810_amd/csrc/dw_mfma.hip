@@ -22,8 +22,10 @@
 // are in flight while the current window is accumulated. A window whose entries do not fit the LDS
 // record area is processed in several rounds of whole quads.
 //
-// Blocks: (input tile of 64 inputs) x (chunk of windows); each block writes a partial dW for its
-// chunk with columns in slot order (a wavefront's 64 slots are contiguous, so the stores coalesce);
+// Blocks: (input tile of 64 inputs) x (chunk of windows: chunk c of n takes windows c, c + n, ...,
+// so every chunk spans the whole time axis and the chunks end together wherever the activity lies
+// in time; contiguous runs of windows made stress's dW calls 2-4% slower); each block writes a
+// partial dW for its chunk with columns in slot order (a wavefront's 64 slots are contiguous, so the stores coalesce);
 // mdw_reduce sums the partials in a fixed order in float64 and puts each column in its place, so
 // dW is bitwise reproducible.
 #include "common.h"
@@ -248,8 +250,7 @@ __global__ void mdw_gate(const int32_t* __restrict__ qoff, int64_t cap, const in
 __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict__ trace, int TB, int N_in, int N_out,
                                                         const int32_t* __restrict__ qoff, const int2* __restrict__ rec,
                                                         const int32_t* __restrict__ inv, int64_t cap, int n_win,
-                                                        int wpc, int n_itiles, float* __restrict__ part,
-                                                        bool chunked) {
+                                                        int n_itiles, float* __restrict__ part, bool chunked) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   int it, ch;
   if ((gridDim.x & 7) == 0 && ((gridDim.x >> 3) % n_itiles) == 0) {
@@ -269,7 +270,9 @@ __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict_
   f4v C[16];
 #pragma unroll
   for (int q = 0; q < 16; ++q) C[q] = f4v{0.f, 0.f, 0.f, 0.f};
-  const int wlo = ch * wpc, whi = min(n_win, wlo + wpc);
+  // chunk ch takes windows ch, ch + nch, ch + 2 nch, ...: every chunk spans the whole time axis
+  const int nch = (int)gridDim.x / n_itiles;
+  auto win_of = [&](int k) { return ch + k * nch; };
 
   // Direct loads of window win into buffer bi: its trace rows (input tile it; lanes past the row's
   // 64 inputs fill the padding), its first round of sorted entries and its qoff row. Every source
@@ -306,34 +309,33 @@ __global__ __launch_bounds__(kMThreads) void mdw_kernel(const float* __restrict_
     }
   };
 
-  // Entry ranges of the chunk's windows, 64 at a time: lane l holds window wlo + 64 g + l. A group
-  // is loaded right after a barrier, before any staging load is in flight.
+  // Entry ranges of the chunk's windows, 64 at a time: lane l holds the chunk's window 64 g + l. A
+  // group is loaded right after a barrier, before any staging load is in flight.
   int rng_lo = 0, rng_hi = 0;
-  auto range_of = [&](int win, int& lo, int& hi) {
-    const int rel = win - wlo;
-    if ((rel & (kWave - 1)) == 0) {
-      const int wv = win + l;
-      const int a = wv < whi ? clampi(qoff[(size_t)wv * kMQLd], cap) : 0;
+  auto range_of = [&](int k, int& lo, int& hi) {
+    if ((k & (kWave - 1)) == 0) {
+      const int wv = win_of(k + l);
+      const int a = wv < n_win ? clampi(qoff[(size_t)wv * kMQLd], cap) : 0;
       rng_lo = a;
-      rng_hi = wv < whi ? max(a, clampi(qoff[(size_t)wv * kMQLd + kMQ], cap)) : 0;
+      rng_hi = wv < n_win ? max(a, clampi(qoff[(size_t)wv * kMQLd + kMQ], cap)) : 0;
     }
-    lo = __builtin_amdgcn_readlane(rng_lo, rel & (kWave - 1));
-    hi = __builtin_amdgcn_readlane(rng_hi, rel & (kWave - 1));
+    lo = __builtin_amdgcn_readlane(rng_lo, k & (kWave - 1));
+    hi = __builtin_amdgcn_readlane(rng_hi, k & (kWave - 1));
   };
   int cur_lo = 0, cur_hi = 0;
-  if (wlo < whi) {
-    range_of(wlo, cur_lo, cur_hi);
-    stage(0, wlo, cur_lo, cur_hi);
+  if (win_of(0) < n_win) {
+    range_of(0, cur_lo, cur_hi);
+    stage(0, win_of(0), cur_lo, cur_hi);
   }
-  for (int win = wlo; win < whi; ++win) {
-    const int bi = (win - wlo) & 1;
+  for (int k = 0; win_of(k) < n_win; ++k) {
+    const int bi = k & 1;
     char* buf = smem + bi * kMBuf;
     mdw_wait_dma();
     __syncthreads();
     int nxt_lo = 0, nxt_hi = 0;
-    if (win + 1 < whi) {
-      range_of(win + 1, nxt_lo, nxt_hi);
-      stage(bi ^ 1, win + 1, nxt_lo, nxt_hi);
+    if (win_of(k + 1) < n_win) {
+      range_of(k + 1, nxt_lo, nxt_hi);
+      stage(bi ^ 1, win_of(k + 1), nxt_lo, nxt_hi);
     }
     const int e_lo = cur_lo, e_hi = cur_hi;
     cur_lo = nxt_lo;
@@ -532,7 +534,7 @@ void mdw_enqueue_rest(const float* trace_in, int T, int B, int N_in, int N_out, 
   hipLaunchKernelGGL(mdw_gate, dim3((unsigned)p.n_win), dim3(256), 0, s, b.qoff, out_cap, b.src, out_g, eps_out, b.rec);
   ensure_dynamic_lds((const void*)mdw_kernel, 2 * kMBuf);
   hipLaunchKernelGGL(mdw_kernel, dim3((unsigned)(p.n_itiles * p.n_chunks)), dim3(kMThreads), 2 * kMBuf, s, trace_in,
-                     T * B, N_in, N_out, b.qoff, b.rec, b.inv, out_cap, p.n_win, p.wpc, p.n_itiles, b.part,
+                     T * B, N_in, N_out, b.qoff, b.rec, b.inv, out_cap, p.n_win, p.n_itiles, b.part,
                      p.n_chunks > 1);
   if (p.n_chunks > 1) {
     const int S = 4 * ((N_out + 3) / 4);
