@@ -491,12 +491,12 @@ class Runner:
         self.net.forward(None if self.args.unfused else b_th)
         csrs = self.net.compact(b_th)
         self.caps = [c.capacity for c in csrs]
-        # dW streams of the pipelined schedule: two when the dW calls are small (one does not fill
-        # the GPU, so the next layer's can run beside it); one when a dW call fills the GPU by itself
-        # (more than ~1e9 multiply-adds: a second stream gains ~1.5% at the stress size at B_th = 0.2
-        # and overlapping dW calls blur their per-call timing)
-        big = max(self.caps[l] * sizes[l] for l in range(L)) >= 10 ** 9
-        self.n_dw = min(1 + len(self.dw_extra), self.args.dw_streams or (1 if big else 2))
+        # dW streams of the pipelined schedule: one by default, the dW calls in line with the spike
+        # gradients. Beside them on a second stream each spike gradient shares the GPU with a dW
+        # call: deep 0.48-0.55 ms against 0.44-0.45 in line (its walks 0.08 against 0.035 ms),
+        # stress 2.83 against 2.47 ms (the walk is gather-bound, the dW call LDS- and
+        # matrix-core-bound, yet together they slow each other more than they overlap).
+        self.n_dw = min(1 + len(self.dw_extra), self.args.dw_streams or 1)
         K = self.args.recompute
         if K:  # trace recompute: dW from the input spikes and checkpoints of the trace every K steps
             self.ws_dw = [snn.workspace(snn.snn_sparse_dw_spikes_workspace(T, B, sizes[l], sizes[l + 1],
@@ -548,11 +548,11 @@ class Runner:
         E("cmp0").record(main)
         self.deferred = self.pipelined and use_aux and L >= 3 and not K and self.n_dw == 1
         if self.deferred:
-            # big layers (one stream of dW calls and spike gradients): the top two layers' active
-            # sets now (the readout's and the top layer's spike gradients need them), the others on
-            # the side stream beside the chain, each before the spike gradient that needs it (stress:
-            # 2.51 -> 2.48 ms). With small layers the chain is short and the waits cost more than
-            # the overlap saves (deep: 0.475 -> 0.515 ms), so they are all compacted first.
+            # one stream of dW calls and spike gradients: the top two layers' active sets now (the
+            # readout's and the top layer's spike gradients need them), the others on the side
+            # stream beside the chain, each before the spike gradient that needs it (stress: 2.51
+            # -> 2.48 ms). With the dW calls on a second stream the chain's waits cost more than the
+            # overlap saves (deep: 0.475 -> 0.515 ms), so there they are all compacted first.
             top = R("compact", main, lambda: [net.compact_layer(l, self.b_th, self._cap(l)) for l in (L - 2, L - 1)])
             cs = [None] * (L - 2) + top
         else:
@@ -601,14 +601,14 @@ class Runner:
 
     def _layers_pipelined(self, ev, r, cs, K):
         """The spike gradients form a chain (each layer's needs the one above); a layer's dW needs only
-        its own eps, and its structure-only layout only the active sets. The layouts run on a side
-        stream from the start, beside the readout's spike gradient. When one dW call fills the GPU
-        (big layers), the dW calls then run on main between the spike gradients; for small layers
-        each dW runs on a dW stream as soon as its eps is there, beside the chain."""
+        its own eps, and its structure-only layout only the active sets. The layouts (and the lower
+        layers' compactions) run on a side stream from the start of the chain. By default the dW
+        calls run on main between the spike gradients; with --dw-streams N > 1 each dW runs on a dW
+        stream as soon as its eps is there, beside the chain."""
         snn, net, main, side, R = self.snn, self.net, self.main, self.aux, self.region
         T, B, L = self.T, self.B, self.L
         self.cs = cs
-        inline = self.n_dw == 1  # one dW call fills the GPU
+        inline = self.n_dw == 1  # dW calls in line with the spike gradients
         # the dW streams: the extra ones first, so that the top layer's dW waits only for its own
         # layout, not behind every layout queued on the side stream
         dw_streams = [main] if inline else (self.dw_extra + [side])[:self.n_dw]
@@ -953,8 +953,8 @@ def build_parser() -> argparse.ArgumentParser:
                     help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
                          "or layer by layer (auto: pipelined for two or more LIF layers)")
     ap.add_argument("--dw-streams", type=int, default=0, metavar="N",
-                    help="pipelined schedule: streams the dW calls take in turn, layer by layer (default: 2 for "
-                         "small layers, 1 when a dW call fills the GPU)")
+                    help="pipelined schedule: streams the dW calls take in turn, layer by layer (default 1: "
+                         "in line with the spike gradients)")
     ap.add_argument("--recompute", type=int, default=0, metavar="K",
                     help="trace recompute: dW rebuilds the input trace from the spikes and checkpoints every K steps")
     ap.add_argument("--graph", action="store_true",
