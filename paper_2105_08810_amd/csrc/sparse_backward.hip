@@ -116,7 +116,10 @@ struct WalkPlan {
 
 WalkPlan plan_walk(int T) {
   WalkPlan w{};
-  w.P = std::max(4, std::min(64, (T + 31) / 32));
+  // short sequences: chunks of two steps (T = 100: 50 chunks; deep's spike gradients 0.036-0.047
+  // -> 0.031-0.042 ms, the walks being latency-bound); longer ones: T / 32 steps (stress, T = 500:
+  // 16; 8 made it slower, the chunk sums and carries growing with the chunk count)
+  w.P = T <= 128 ? 2 : std::min(64, (T + 31) / 32);
   w.C = (T + w.P - 1) / w.P;
   return w;
 }
