@@ -348,11 +348,9 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_kernel(const float* __rest
   __syncthreads();
   float* dst = out + (size_t)c * N_in * N_out;
   const int width = j1 - j0;
-  for (int k = tid; k < kItile * width; k += kDwThreads) {
-    const int ii = k / width;
-    const int jj = k - ii * width;
-    if (it * kItile + ii < N_in) dst[(size_t)(it * kItile + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
-  }
+  for (int ii = w; ii < kItile && it * kItile + ii < N_in; ii += kDwWaves)  // a wavefront per input row
+    for (int jj = l; jj < width; jj += kWave)
+      dst[(size_t)(it * kItile + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
 }
 
 // Block (c, it) of dw_rows: inputs [64 it, 64 it + 64) (one per lane), every output, the rows of
@@ -472,11 +470,8 @@ __global__ __launch_bounds__(kDwThreads) void dw_rows_kernel(const float* __rest
   }
   __syncthreads();
   float* dst = out + (size_t)c * N_in * N_out;
-  for (int k = tid; k < kWave * N_out; k += kDwThreads) {
-    const int ii = k / N_out;
-    const int jj = k - ii * N_out;
-    if (it * kWave + ii < N_in) dst[(size_t)(it * kWave + ii) * N_out + jj] = (float)acc[jj * kRowsLd + ii];
-  }
+  for (int ii = w; ii < kWave && it * kWave + ii < N_in; ii += kDwWaves)  // a wavefront per input row
+    for (int jj = l; jj < N_out; jj += kWave) dst[(size_t)(it * kWave + ii) * N_out + jj] = (float)acc[jj * kRowsLd + ii];
 }
 
 // dW with the input trace rebuilt from the input spikes (trace recompute). The trace at every
@@ -602,11 +597,9 @@ __global__ __launch_bounds__(kDwThreads) void dw_slab_spikes_kernel(
   __syncthreads();
   float* dst = out + (size_t)c * N_in * N_out;
   const int width = j1 - j0;
-  for (int k = tid; k < kItile * width; k += kDwThreads) {
-    const int ii = k / width;
-    const int jj = k - ii * width;
-    if (it * kItile + ii < N_in) dst[(size_t)(it * kItile + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
-  }
+  for (int ii = w; ii < kItile && it * kItile + ii < N_in; ii += kDwWaves)  // a wavefront per input row
+    for (int jj = l; jj < width; jj += kWave)
+      dst[(size_t)(it * kItile + ii) * N_out + j0 + jj] = (float)acc[jj * kLd + ii];
 }
 
 // Trace checkpoints: ck[q, b, i] = the input trace at step q K (q < ceil(T / K)), from the spikes
