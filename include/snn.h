@@ -151,10 +151,12 @@ snn_status snn_active_compact_bits_noalloc(const uint64_t* active_bits, const fl
  *   non-decreasing, columns strictly ascending inside a row. Entries with a column outside
  *   [0, N) are skipped; for other malformed input the results are unspecified, but every memory
  *   access stays inside the arrays and workspace given (indices are clamped).
- *   Workspace: for N_out > 32 its size depends on out_cap (a slab-major copy of the active
- *   entries is built in it); for N_out <= 32 (narrow layers: G written densely, padded to 8, 16
- *   or 32 columns) it holds that G and delta (T*B*ld floats each), a bitset of the rows with an
- *   entry and per-chunk partial dW, and does not depend on out_cap.
+ *   Workspace: for layers of 33..300 outputs and at most 1024 inputs it holds per-chunk partial
+ *   dW only (the dW kernel reads the CSR directly) and does not depend on out_cap; for other
+ *   layers of more than 32 outputs its size depends on out_cap (a slab-major or window-sorted
+ *   copy of the active entries is built in it); for N_out <= 32 (narrow layers: G written
+ *   densely, padded to 8, 16 or 32 columns) it holds that G and delta (T*B*ld floats each), a
+ *   bitset of the rows with an entry and per-chunk partial dW, and does not depend on out_cap.
  *   aux_stream (may be NULL): a second hipStream_t. When given, the spike-gradient part runs on
  *   it beside the dW part on `stream`; the call makes aux_stream wait for the work already on
  *   `stream`, and `stream` wait for the aux work, so work enqueued on `stream` afterwards sees
@@ -195,8 +197,8 @@ snn_status snn_sparse_dw(const float* trace_in, int T, int B, int N_in, int N_ou
  * snn_sparse_dw in two parts, so that the part that needs only the active set's structure can
  * run early (right after compaction, before any eps exists) and off the critical path:
  * snn_sparse_dw_layout reads out_row_ptr and out_col_idx only and writes the per-(row, column
- * slab) entry counts and offsets (or, for N_out <= 32, the bitset of rows with an entry) into the
- * workspace; snn_sparse_dw_prepared then does the rest of snn_sparse_dw (arguments as there) and
+ * slab) entry counts and offsets (or, for N_out <= 32, the bitset of rows with an entry; for
+ * layers that take the CSR-direct dW, nothing) into the workspace; snn_sparse_dw_prepared then does the rest of snn_sparse_dw (arguments as there) and
  * gives the same dW bit for bit, provided the layout ran on the same workspace with a CSR of the
  * same structure (row pointers and columns) and out_cap, and the workspace was not used in
  * between. Workspace from snn_sparse_dw_workspace. Errors as snn_sparse_dw.
