@@ -383,9 +383,9 @@ __global__ __launch_bounds__(kDwThreads) void dw_rows_kernel(const float* __rest
   for (int k = tid; k < N_out * kRowsLd; k += kDwThreads) acc[k] = 0.0;
   __syncthreads();
 
-  // Chunk c takes the groups of kStride rows c, c + n_chunks, c + 2 n_chunks, ...: every chunk
-  // spans the whole time axis, so that chunks get about as many entries wherever the activity
-  // lies in time. Wavefront w takes rows [8 w, 8 w + 8) of each of its chunk's groups.
+  // Chunk c takes the groups of kGroup = 128 rows c, c + n_chunks, c + 2 n_chunks, ...: every
+  // chunk spans the whole time axis, so that chunks get about as many entries wherever the
+  // activity lies in time. Wavefront w takes rows [8 w, 8 w + 8) of each of its chunk's groups.
   // lane k <= kRowsPerBatch: row pointer rb + k (rows past TB read TB's: empty ranges)
   auto load_rp = [&](int rb) { return clamp_entry(row_ptr[min(rb + min(l, kRowsPerBatch), TB)], cap); };
   // the batch's trace values (a row with no entry reads the batch's first row instead: a cache
