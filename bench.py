@@ -931,7 +931,7 @@ class Runner:
 def build_parser() -> argparse.ArgumentParser:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100)  # stress: ~2 s of timed GPU work
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="stress")
     ap.add_argument("--b-th", type=float, default=None)
