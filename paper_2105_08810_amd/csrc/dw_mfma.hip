@@ -444,8 +444,17 @@ __global__ __launch_bounds__(256) void mdw_reduce(const float* __restrict__ part
   const int64_t i = k / S;
   const int col = inv[k - i * S];
   if (col < 0 || col >= N_out) return;
+  constexpr int kAhead = 8;  // partials loaded before any is added (the adds keep chunk order)
   double s = 0.0;
-  for (int ch = 0; ch < n_chunks; ++ch) s += (double)part[ch * n + k];
+  int ch = 0;
+  for (; ch + kAhead <= n_chunks; ch += kAhead) {
+    float v[kAhead];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) v[u] = part[(ch + u) * n + k];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) s += (double)v[u];
+  }
+  for (; ch < n_chunks; ++ch) s += (double)part[ch * n + k];
   out[i * N_out + col] = (float)s;
 }
 
