@@ -238,9 +238,25 @@ __global__ void mdw_gate(const int32_t* __restrict__ qoff, int64_t cap, const in
   const int win = blockIdx.x;
   const int a = clampi(qoff[(size_t)win * kMQLd], cap);
   const int z = clampi(qoff[(size_t)win * kMQLd + kMQ], cap);
-  for (int d = a + threadIdx.x; d < z; d += blockDim.x) {
-    const int e = clampi(src[d], cap - 1);
-    rec[d].y = __float_as_int(g ? eps[e] * g[e] : eps[e]);
+  // kAhead entries per thread at a time: their indices, then their eps and g, are all requested
+  // before any is used (one dependent round trip per kAhead entries instead of per entry)
+  constexpr int kAhead = 8;
+  const int step = (int)blockDim.x;
+  for (int d0 = a + threadIdx.x; d0 < z; d0 += kAhead * step) {
+    int e[kAhead];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+      const int d = d0 + u * step;
+      e[u] = d < z ? clampi(src[d], cap - 1) : 0;
+    }
+    float v[kAhead];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) v[u] = g ? eps[e[u]] * g[e[u]] : eps[e[u]];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+      const int d = d0 + u * step;
+      if (d < z) rec[d].y = __float_as_int(v[u]);
+    }
   }
 }
 
