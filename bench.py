@@ -950,8 +950,9 @@ def build_parser() -> argparse.ArgumentParser:
                     help="skip the allocator-peak memory measurement after the timed steps (for counter runs that "
                          "should hold the timed step's dispatches only)")
     ap.add_argument("--schedule", choices=("auto", "pipelined", "layerwise"), default="auto",
-                    help="LIF layers' backward: dW calls on a stream of their own beside the spike-gradient chain, "
-                         "or layer by layer (auto: pipelined for two or more LIF layers)")
+                    help="LIF layers' backward: pipelined (the dW layouts and the lower layers' compactions on a "
+                         "side stream beside the spike-gradient chain) or layer by layer (auto: pipelined for two or "
+                         "more LIF layers)")
     ap.add_argument("--dw-streams", type=int, default=0, metavar="N",
                     help="pipelined schedule: streams the dW calls take in turn, layer by layer (default 1: "
                          "in line with the spike gradients)")
