@@ -7,11 +7,11 @@ the sparse backward (compaction + sparse backward of every LIF layer; the readou
 backward and the loss are outside both chains, as are the forward passes).
 
 Schedule of the LIF layers' backward: with two or more LIF layers the spike gradients form a chain
-on the main stream and the dW calls' structure-only layouts run on a side stream from the start of
-the chain; a dW call that fills the GPU by itself (stress) runs on the main stream after its
-layer's spike gradient, smaller ones on dW streams beside the chain. With one LIF layer everything
-runs on one stream. HIP events on the stream each call runs on bracket every dW call and spike
-gradient; dW is the dominant kernel and the roofline object is computed from its calls' durations.
+on the main stream, each followed by its layer's dW call; the dW calls' structure-only layouts and
+the compactions of the layers below the top two run on a side stream from the start of the chain
+(`--dw-streams N` puts the dW calls on streams beside the chain instead). With one LIF layer
+everything runs on one stream. HIP events bracket every dW call and spike gradient; dW is the
+dominant kernel and the roofline object is computed from its calls' durations.
 
 Prints ONE JSON line. `value` = active neuron-steps per second of the sparse backward
 (sum over LIF layers of the active entries, divided by its time); the dense time and the
