@@ -221,6 +221,42 @@ def test_compaction_capacity_overflow_is_safe():
     assert torch.isfinite(dW).all()
 
 
+@pytest.mark.parametrize("width", [200, 400, 600])
+def test_dw_truncated_csr_each_path(width):
+    """A CSR whose compaction overflowed its capacity (half of nnz): dW sums exactly the entries
+    below the capacity, element by element against a float64 sum over them, on each dW path
+    (200 outputs: CSR-direct; 400: slab records; 600: matrix cores)."""
+    inp = _wide((width,), 40, 10, T=30, B=8)
+    print(f"\n[case] truncated CSR dW, 40->{width}", flush=True)
+    net = pipeline.from_inputs(inp).forward()
+    V = net.V[0]
+    T, B, N = V.shape
+    full = snn.active_compact(V, 1.0, 0.2, 100.0)
+    cap = full.nnz() // 2
+    assert cap > 64
+    col = torch.full((cap,), -7, dtype=torch.int32, device="cuda")
+    gg = torch.full((cap,), -7.0, dtype=torch.float32, device="cuda")
+    row_ptr = torch.empty(T * B + 1, dtype=torch.int32, device="cuda")
+    nnz_dev = torch.empty(1, dtype=torch.int64, device="cuda")
+    ws = snn.workspace(snn.snn_active_compact_workspace(T, B, N))
+    snn.snn_active_compact(V, T, B, N, 1.0, 0.2, 100.0, row_ptr, col, gg, cap, nnz_dev, ws)
+    eps = torch.from_numpy(np.random.default_rng(width).standard_normal(cap).astype(np.float32)).cuda()
+    trunc = snn.Csr(row_ptr, col, gg, nnz_dev, cap)
+    dW = snn.sparse_dw(net.trace[0], trunc, eps, N)
+    torch.cuda.synchronize()
+    rp = np.minimum(_np(row_ptr).astype(np.int64), cap)
+    rows = np.repeat(np.arange(T * B), np.diff(rp))
+    G = (_np(eps) * _np(gg)).astype(np.float32).astype(np.float64)  # the kernels form G in float32
+    tr = _np(net.trace[0]).reshape(T * B, -1).astype(np.float64)[rows]
+    ref = np.zeros((tr.shape[1], N))
+    mag = np.zeros((tr.shape[1], N))
+    np.add.at(ref.T, _np(col), G[:, None] * tr)
+    np.add.at(mag.T, _np(col), np.abs(G)[:, None] * np.abs(tr))
+    x = _np(dW).astype(np.float64)
+    bad = np.abs(x - ref) > 2e-6 * mag + 1e-30
+    assert not bad.any(), f"{int(bad.sum())} elements differ from the sum over the entries below capacity"
+
+
 def test_run_to_run_determinism():
     inp = _case("latency", list(range(32)))
     a = _gpu(inp, 0.2, dense=False)
