@@ -269,6 +269,19 @@ def test_run_to_run_determinism():
         assert torch.equal(a["eps"][l][:n], b["eps"][l][:n])  # grad_in sums in a fixed order
 
 
+def test_matrix_core_dw_is_reproducible():
+    """The matrix-core dW (stress layers: 1024 outputs at about 2% active) accumulates each window's
+    entries in a fixed order and sums the chunk partials in chunk order in float64: two runs give
+    the same dW bit for bit. (The float64 LDS atomics of the other dW paths commit in any order;
+    their float32 results differ only where a float64 sum falls within ~1e-16 of a rounding
+    boundary.)"""
+    inp = _case("stress", list(range(8)))
+    a = _gpu(inp, 0.2, dense=False)
+    b = _gpu(inp, 0.2, dense=False)
+    for l in range(len(inp.Ws)):
+        assert torch.equal(a["dW"][l], b["dW"][l]), f"dW[{l}]"
+
+
 @pytest.mark.parametrize("name,batch,b_th", [("latency", list(range(32)), 0.2), ("stress", list(range(8)), 0.2),
                                              ("tiny", None, math.inf)])
 def test_aux_stream_overlap(name, batch, b_th):
