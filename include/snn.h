@@ -88,6 +88,23 @@ snn_status snn_lif_forward_active(const uint8_t* s_in, const float* W, int T, in
                                   float* trace_in, uint64_t* active_bits, void* stream);
 
 /*
+ * The forward that also writes the trace of its own output spikes, which the next layer (a
+ * readout, say) reads as its input trace (Eq. (w_grad)), so that layer's forward can be called
+ * with trace_in = NULL instead of walking the spikes again.
+ *   trace_out    [T,B,N_out] float32 (written unless NULL): trace_out[0] = 0,
+ *                trace_out[t+1] = alpha_next*trace_out[t] + s_out[t], bit-identical to the
+ *                trace_in that a forward of the next layer writes from s_out
+ *   alpha_next   the leak of that trace (the next layer's alpha), in (0,1]; checked only when
+ *                trace_out is not NULL
+ *   active_bits  as snn_lif_forward_active, or NULL for no active set (b_th is then ignored)
+ * Everything else as snn_lif_forward; trace_out must not overlap the other buffers.
+ */
+snn_status snn_lif_forward_traces(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
+                                  float alpha, float theta, float b_th, float* V, uint8_t* s_out,
+                                  float* trace_in, float* trace_out, float alpha_next, uint64_t* active_bits,
+                                  void* stream);
+
+/*
  * Active-set compaction (Definition 1) with the truncated spike derivative (Definition 2).
  *   V        [T,B,N] float32 (read)
  *   active   |V - theta| < b_th in float32, strictly (b_th = +INFINITY: every finite V)

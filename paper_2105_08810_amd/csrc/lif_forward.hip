@@ -10,6 +10,8 @@
 //               wavefronts form a tile's weighted inputs two rows each into LDS, then every
 //               thread runs its column's recurrence over the tile from LDS. V, S_out, the active
 //               bitset and the input trace are written once; the weighted inputs never reach HBM.
+//               The trace of the output spikes (the next layer's input trace) can be written
+//               beside V from the spike bits the recurrence has in hand.
 //   lif_gather + lif_scan  (widths whose bitset words straddle samples, W rows that are not
 //               whole float4 columns, grids of fewer than two blocks per CU) one wavefront per row
 //               parks I[t,b,:] in the slot of V[t+1,b,:]; then one thread per (b, j) runs the
@@ -263,8 +265,8 @@ __device__ __forceinline__ void mark_active(uint64_t* bits, size_t word, bool va
 __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restrict__ s_in, int T, int B, int N_in,
                                                          int N_out, float alpha, float theta, float b_th,
                                                          float* __restrict__ V, uint8_t* __restrict__ s_out,
-                                                         float* __restrict__ trace, uint64_t* __restrict__ bits,
-                                                         int nv) {
+                                                         float* __restrict__ trace, float* __restrict__ trace_out,
+                                                         float alpha_next, uint64_t* __restrict__ bits, int nv) {
   if ((int)blockIdx.x < nv) {
     const size_t k0 = (size_t)blockIdx.x * kScanThreads + (threadIdx.x & ~(kWave - 1));
     if (k0 >= (size_t)B * N_out) return;  // whole wavefront past the end
@@ -274,8 +276,9 @@ __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restri
     const size_t step = (size_t)B * N_out;
     const size_t W64 = (step + kWave - 1) / kWave;
     const size_t wword = k0 / kWave;
-    float v = 0.0f;
+    float v = 0.0f, to = 0.0f;
     if (valid) V[k] = 0.0f;
+    if (trace_out && valid) trace_out[k] = 0.0f;
     if (bits) mark_active(bits, wword, valid, v, theta, b_th);
     for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
       const int np = min(kScanAhead, T - 1 - t0);
@@ -290,6 +293,10 @@ __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restri
           if (valid) s_out[(size_t)t * step + k] = (uint8_t)sp;
           v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), in[p]), sp ? -1.0f : -0.0f);
           if (valid) V[(size_t)(t + 1) * step + k] = v;
+          if (trace_out) {
+            to = __fadd_rn(__fmul_rn(alpha_next, to), sp ? 1.0f : 0.0f);
+            if (valid) trace_out[(size_t)(t + 1) * step + k] = to;
+          }
           if (bits) mark_active(bits, (size_t)(t + 1) * W64 + wword, valid, v, theta, b_th);
         }
       }
@@ -383,11 +390,11 @@ constexpr int kFuseThreads = 512;
 constexpr int kFuseWaves = kFuseThreads / kWave;
 constexpr int kFuseP = 2 * kFuseWaves;  // steps per tile: two rows per wavefront
 
-template <bool ALIGNED, int NQ, bool STASH>
+template <bool ALIGNED, int NQ, bool STASH, bool TOUT>
 __global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(4))) void lif_fused(
     const uint8_t* __restrict__ s_in, const float* __restrict__ W, int T, int B, int N_in, int N_out, int G, int nfb,
     float alpha, float theta, float b_th, float* __restrict__ V, uint8_t* __restrict__ s_out,
-    float* __restrict__ trace, uint64_t* __restrict__ bits) {
+    float* __restrict__ trace, float* __restrict__ trace_out, float alpha_next, uint64_t* __restrict__ bits) {
   constexpr int JW = 4 * kWave * NQ;  // columns of a group
   constexpr int KB = NQ >= 2 ? 4 : 8;
   static_assert(JW <= kFuseThreads, "one scan thread per column of the group");
@@ -436,8 +443,9 @@ __global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(4)
   float tr[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (STASH && trace && tq >= 0)
     *reinterpret_cast<float4*>(trace + (size_t)b * N_in + 4 * tq) = make_float4(0.f, 0.f, 0.f, 0.f);
-  float v = 0.0f;
+  float v = 0.0f, to = 0.0f;
   if (valid) V[vk] = 0.0f;
+  if (TOUT && valid) trace_out[vk] = 0.0f;
   if (bits && scan_wave) mark_active(bits, wword, valid, v, theta, b_th);
   prefetch(0);
   for (int t0 = 0; t0 < T - 1; t0 += kFuseP) {
@@ -472,6 +480,10 @@ __global__ __launch_bounds__(kFuseThreads) __attribute__((amdgpu_waves_per_eu(4)
           if (valid) s_out[(size_t)t * vstep + vk] = (uint8_t)sp;
           v = __fadd_rn(__fadd_rn(__fmul_rn(alpha, v), tile[p][k]), sp ? -1.0f : -0.0f);
           if (valid) V[(size_t)(t + 1) * vstep + vk] = v;
+          if (TOUT) {
+            to = __fadd_rn(__fmul_rn(alpha_next, to), sp ? 1.0f : 0.0f);
+            if (valid) trace_out[(size_t)(t + 1) * vstep + vk] = to;
+          }
           if (bits) mark_active(bits, (size_t)(t + 1) * W64 + wword, valid, v, theta, b_th);
         }
       }
@@ -618,13 +630,14 @@ __global__ __launch_bounds__(kScanThreads) void conv_scan(const uint8_t* __restr
 }
 
 snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out, float alpha,
-                            float theta, float b_th, float* V, uint8_t* s_out, float* trace_in, uint64_t* bits,
-                            void* stream) {
+                            float theta, float b_th, float* V, uint8_t* s_out, float* trace_in, float* trace_out,
+                            float alpha_next, uint64_t* bits, void* stream) {
   if (!s_in || !W || !V || !s_out) return SNN_ERR_INVALID_ARG;
   if (bad_dim(T) || bad_dim(B) || bad_dim(N_in) || bad_dim(N_out)) return SNN_ERR_INVALID_ARG;
   if (too_big(T, B, N_in) || too_big(T, B, N_out)) return SNN_ERR_INVALID_ARG;
   if (bad_alpha(alpha) || isnan(theta)) return SNN_ERR_INVALID_ARG;
   if (bits && (isnan(b_th) || b_th < 0.0f)) return SNN_ERR_INVALID_ARG;
+  if (trace_out && bad_alpha(alpha_next)) return SNN_ERR_INVALID_ARG;
   if (N_out > 16 * 4 * kWave) return SNN_ERR_UNSUPPORTED;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -644,9 +657,15 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
       const int nfb = B * G;
       const int ntb = (trace_in && !stash) ? (int)(((size_t)B * ((N_in + 3) / 4) + kFuseThreads - 1) / kFuseThreads) : 0;
       const dim3 g((unsigned)(nfb + ntb));
-#define SNN_F(A, Q, ST)                                                                                           \
-  hipLaunchKernelGGL((lif_fused<A, Q, ST>), g, dim3(kFuseThreads), 0, s, s_in, W, T, B, N_in, N_out, G, nfb, alpha, \
-                     theta, b_th, V, s_out, trace_in, bits)
+#define SNN_F(A, Q, ST)                                                                                              \
+  do {                                                                                                               \
+    if (trace_out)                                                                                                   \
+      hipLaunchKernelGGL((lif_fused<A, Q, ST, true>), g, dim3(kFuseThreads), 0, s, s_in, W, T, B, N_in, N_out, G,     \
+                         nfb, alpha, theta, b_th, V, s_out, trace_in, trace_out, alpha_next, bits);                  \
+    else                                                                                                             \
+      hipLaunchKernelGGL((lif_fused<A, Q, ST, false>), g, dim3(kFuseThreads), 0, s, s_in, W, T, B, N_in, N_out, G,    \
+                         nfb, alpha, theta, b_th, V, s_out, trace_in, nullptr, 1.0f, bits);                          \
+  } while (0)
       if (stash && fq == 2) SNN_F(true, 2, true);
       else if (stash) SNN_F(true, 1, true);
       else if (al && fq == 2) SNN_F(true, 2, false);
@@ -671,7 +690,7 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
   const int nv = (int)(((size_t)B * N_out + kScanThreads - 1) / kScanThreads);
   const int nt = trace_in ? (int)(((size_t)B * N_in + kScanThreads - 1) / kScanThreads) : 0;
   hipLaunchKernelGGL(lif_scan, dim3((unsigned)(nv + nt)), dim3(kScanThreads), 0, s, s_in, T, B, N_in, N_out, alpha,
-                     theta, b_th, V, s_out, trace_in, bits, nv);
+                     theta, b_th, V, s_out, trace_in, trace_out, alpha_next, bits, nv);
   return launch_status();
 }
 
@@ -680,7 +699,8 @@ snn_status lif_forward_impl(const uint8_t* s_in, const float* W, int T, int B, i
 extern "C" snn_status snn_lif_forward(const uint8_t* s_in, const float* W, int T, int B, int N_in, int N_out,
                                       float alpha, float theta, float* V, uint8_t* s_out, float* trace_in,
                                       void* stream) {
-  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, 0.0f, V, s_out, trace_in, nullptr, stream);
+  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, 0.0f, V, s_out, trace_in, nullptr, 1.0f,
+                          nullptr, stream);
 }
 
 extern "C" size_t snn_active_bits_words(int T, int B, int N) {
@@ -692,7 +712,16 @@ extern "C" snn_status snn_lif_forward_active(const uint8_t* s_in, const float* W
                                              float alpha, float theta, float b_th, float* V, uint8_t* s_out,
                                              float* trace_in, uint64_t* active_bits, void* stream) {
   if (!active_bits) return SNN_ERR_INVALID_ARG;
-  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, active_bits, stream);
+  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, nullptr, 1.0f,
+                          active_bits, stream);
+}
+
+extern "C" snn_status snn_lif_forward_traces(const uint8_t* s_in, const float* W, int T, int B, int N_in,
+                                             int N_out, float alpha, float theta, float b_th, float* V,
+                                             uint8_t* s_out, float* trace_in, float* trace_out,
+                                             float alpha_next, uint64_t* active_bits, void* stream) {
+  return lif_forward_impl(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, trace_out, alpha_next,
+                          active_bits, stream);
 }
 
 extern "C" snn_status snn_conv_lif_forward(const uint8_t* s_in, const float* Wc, int T, int B, int H, int W, int C,
@@ -716,7 +745,7 @@ extern "C" snn_status snn_conv_lif_forward(const uint8_t* s_in, const float* Wc,
     const int N_in = H * W * C;
     const int nt = (int)(((size_t)B * N_in + kScanThreads - 1) / kScanThreads);
     hipLaunchKernelGGL(lif_scan, dim3((unsigned)nt), dim3(kScanThreads), 0, s, s_in, T, B, N_in, 1, alpha, theta,
-                       b_th, nullptr, nullptr, trace_in, nullptr, 0);
+                       b_th, nullptr, nullptr, trace_in, nullptr, 1.0f, nullptr, 0);
   }
   return launch_status();
 }

@@ -37,6 +37,7 @@ _SIGNATURES = {
                                  _P, _P]),
     "snn_active_bits_words": (_SZ, [_I, _I, _I]),
     "snn_lif_forward_active": (_I, [_P, _P, _I, _I, _I, _I, _F, _F, _F, _P, _P, _P, _P, _P]),
+    "snn_lif_forward_traces": (_I, [_P, _P, _I, _I, _I, _I, _F, _F, _F, _P, _P, _P, _P, _F, _P, _P]),
     "snn_active_compact_bits_workspace": (_SZ, [_I, _I, _I]),
     "snn_active_compact_bits": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P, _SZ, _P]),
     "snn_active_compact_bits_noalloc": (_I, [_P, _P, _I, _I, _I, _F, _F, _P, _P, _P, _I64, _P, _P]),
@@ -145,6 +146,15 @@ def snn_lif_forward_active(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_
         _ptr(s_in, torch.uint8, "s_in"), _ptr(W, torch.float32, "W"), T, B, N_in, N_out, float(alpha), float(theta),
         float(b_th), _ptr(V, torch.float32, "V"), _ptr(s_out, torch.uint8, "s_out"),
         _ptr(trace_in, torch.float32, "trace_in"), _ptr(active_bits, torch.int64, "active_bits"), _stream(stream)))
+
+
+def snn_lif_forward_traces(s_in, W, T, B, N_in, N_out, alpha, theta, b_th, V, s_out, trace_in, trace_out,
+                           alpha_next, active_bits=None, stream=None):
+    _check("snn_lif_forward_traces", lib().snn_lif_forward_traces(
+        _ptr(s_in, torch.uint8, "s_in"), _ptr(W, torch.float32, "W"), T, B, N_in, N_out, float(alpha), float(theta),
+        float(b_th), _ptr(V, torch.float32, "V"), _ptr(s_out, torch.uint8, "s_out"),
+        _ptr(trace_in, torch.float32, "trace_in"), _ptr(trace_out, torch.float32, "trace_out"), float(alpha_next),
+        _ptr(active_bits, torch.int64, "active_bits"), _stream(stream)))
 
 
 def snn_active_compact_bits_workspace(T, B, N) -> int:

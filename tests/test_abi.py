@@ -261,6 +261,18 @@ def test_fused_forward_rejects(lib):
     assert lib.snn_active_bits_words(0, 5, 100) == 0
 
 
+def test_forward_traces_rejects(lib):
+    f = lambda **kw: lib.snn_lif_forward_traces(  # noqa: E731
+        kw.get("s", FAKE), FAKE, 10, 4, 32, 16, 0.9, 1.0, kw.get("b", 0.2), FAKE, FAKE, FAKE, kw.get("to", FAKE),
+        kw.get("an", 0.9), kw.get("bits", FAKE), None)
+    for an in (0.0, -0.5, 1.5, NAN):  # the output trace's leak must lie in (0, 1]
+        assert f(an=an) == snn.SNN_ERR_INVALID_ARG
+    assert f(b=NAN) == snn.SNN_ERR_INVALID_ARG
+    assert f(b=-0.5) == snn.SNN_ERR_INVALID_ARG
+    assert f(s=None) == snn.SNN_ERR_INVALID_ARG
+    assert f(s=None, to=None, bits=None, an=NAN, b=NAN) == snn.SNN_ERR_INVALID_ARG
+
+
 def _cb(lib, **kw):
     a = dict(bits=FAKE, V=FAKE, T=10, B=4, N=16, theta=1.0, beta=100.0, rp=FAKE, ci=FAKE, g=FAKE, cap=100, nnz=FAKE,
              ws=FAKE, ws_bytes=1 << 30)

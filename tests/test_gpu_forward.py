@@ -81,3 +81,42 @@ def test_forward_variants_bit_exact(T, B, n_in, n_out, rate, b_th):
     assert np.array_equal(tr.view(np.uint32), rtr.view(np.uint32)), "trace differs from the oracle"
     if bits is not None:
         assert np.array_equal(bits.reshape(T, -1), _bits_from(rV, theta, F32(b_th))), "active bitset differs"
+
+
+@pytest.mark.parametrize("T,B,n_in,n_out,rate,b_th", [
+    (37, 256, 1024, 1024, 0.02, 0.2),  # fused, trace from the staged spike bytes (two groups of 512)
+    (20, 512, 1030, 256, 0.03, 0.2),   # fused with trace blocks beside it
+    (33, 512, 64, 100, 0.2, None),     # fused, no bitset, columns past the width
+    (9, 64, 700, 3968, 0.05, 0.25),    # eight column groups, the last one partial
+    (1, 512, 256, 128, 0.1, 0.2),      # a single step
+    (16, 3, 300, 200, 0.05, 0.2),      # the two-kernel form
+    (21, 4, 1024, 1024, 0.02, None),   # the two-kernel form without a bitset
+])
+def test_forward_output_trace_bit_exact(T, B, n_in, n_out, rate, b_th):
+    """snn_lif_forward_traces: the trace of the layer's own spikes, written beside V, equals bit for
+    bit the input trace that the oracle forms from those spikes with the next layer's leak (Eq.
+    (w_grad)), and V, spikes, input trace and bitset are those of the other forward entry points."""
+    X, W, alpha = _case(T, B, n_in, n_out, rate, seed=T * 104729 + n_out)
+    theta = F32(1.0)
+    alpha_next = F32(np.exp(-1.0 / 15.0))  # not this layer's leak
+    V0, S0, tr0, bits0 = _run(X, W, alpha, theta, b_th)
+    x = torch.from_numpy(X).cuda()
+    w = torch.from_numpy(W).cuda()
+    V = torch.empty((T, B, n_out), dtype=torch.float32, device="cuda")
+    S = torch.empty((T, B, n_out), dtype=torch.uint8, device="cuda")
+    tr = torch.empty((T, B, n_in), dtype=torch.float32, device="cuda")
+    to = torch.full((T, B, n_out), float("nan"), dtype=torch.float32, device="cuda")
+    bits = None if b_th is None else torch.empty(snn.snn_active_bits_words(T, B, n_out), dtype=torch.int64,
+                                                 device="cuda")
+    snn.snn_lif_forward_traces(x, w, T, B, n_in, n_out, alpha, theta, 0.0 if b_th is None else b_th, V, S, tr, to,
+                               alpha_next, bits)
+    torch.cuda.synchronize()
+    assert np.array_equal(V.cpu().numpy().view(np.uint32), V0.view(np.uint32))
+    assert np.array_equal(S.cpu().numpy(), S0)
+    assert np.array_equal(tr.cpu().numpy().view(np.uint32), tr0.view(np.uint32))
+    if b_th is not None:
+        assert np.array_equal(bits.cpu().numpy(), bits0)
+    rS = oracle.lif_forward(X, W, alpha, theta)[1]
+    assert (rS[:-1] != 0).any() or T == 1, "the case should spike"
+    ref = oracle.lif_forward(rS, np.zeros((n_out, 1), F32), alpha_next, theta)[2]
+    assert np.array_equal(to.cpu().numpy().view(np.uint32), ref.view(np.uint32)), "output trace differs"
