@@ -280,11 +280,16 @@ __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restri
     if (valid) V[k] = 0.0f;
     if (trace_out && valid) trace_out[k] = 0.0f;
     if (bits) mark_active(bits, wword, valid, v, theta, b_th);
-    for (int t0 = 0; t0 < T - 1; t0 += kScanAhead) {
+    // Two groups of kScanAhead steps in flight: a group's loads are issued before the previous
+    // group's stores, so waiting for them (the memory counter retires in order) does not wait
+    // for those stores as well. A group's loads read slots no earlier store writes.
+    auto load = [&](float (&in)[kScanAhead], int t0) {
       const int np = min(kScanAhead, T - 1 - t0);
-      float in[kScanAhead];
 #pragma unroll
       for (int p = 0; p < kScanAhead; ++p) in[p] = V[(size_t)(t0 + min(p, np - 1) + 1) * step + kc];
+    };
+    auto walk = [&](const float (&in)[kScanAhead], int t0) {
+      const int np = min(kScanAhead, T - 1 - t0);
 #pragma unroll
       for (int p = 0; p < kScanAhead; ++p) {
         if (p < np) {
@@ -299,6 +304,17 @@ __global__ __launch_bounds__(kScanThreads) void lif_scan(const uint8_t* __restri
           }
           if (bits) mark_active(bits, (size_t)(t + 1) * W64 + wword, valid, v, theta, b_th);
         }
+      }
+    };
+    float ina[kScanAhead], inb[kScanAhead];
+    if (T > 1) load(ina, 0);
+    for (int t0 = 0; t0 < T - 1; t0 += 2 * kScanAhead) {
+      const int t1 = t0 + kScanAhead;
+      if (t1 < T - 1) load(inb, t1);
+      walk(ina, t0);
+      if (t1 < T - 1) {
+        if (t1 + kScanAhead < T - 1) load(ina, t1 + kScanAhead);
+        walk(inb, t1);
       }
     }
     if (valid) s_out[(size_t)(T - 1) * step + k] = (uint8_t)(v > theta);
